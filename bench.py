@@ -1,0 +1,300 @@
+#!/usr/bin/env python3
+"""Throughput of the fibattn hot path on one MI355X.
+
+One step = one layer of the 60M-model shape (B=8, H=8, T=1024, d_head=64, bf16,
+W=8, Fibonacci base K=15, alpha=1): RoPE of q and k at true positions, the forward
+(o, lse), the backward (dq, dk, dv, dalpha) and R^T carrying dq, dk back to the
+unrotated inputs, all in libfibattn.so's HIP kernels on one stream.  Inputs are
+seeded N(0,1) tensors resident in HBM; several buffer sets rotate so that the
+256 MB last-level cache cannot hold a step's working set.  Steps are replayed from
+HIP graphs (one captured step per buffer set).
+
+Printed: one JSON line with queries*heads per second, the roofline of the dominant
+kernel (algorithmic bytes per launch over its mean launch duration, timed with HIP
+events on the launch stream), and the fp64 CPU oracle timed on the host's cores as
+a reported baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
+METRIC = "fwd+bwd queries·heads/s at T=1024 and T=4096; achieved HBM GB/s vs peak"
+
+
+def parse_args():
+    p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=40)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="layer_60m_fixed_T1024")
+    p.add_argument("--sets", type=int, default=0, help="buffer sets to rotate (0: enough for > 320 MB)")
+    p.add_argument("--eager", action="store_true", help="launch eagerly instead of replaying graphs")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the oracle sample")
+    p.add_argument("--no-t4096", action="store_true", help="skip the T=4096 figure")
+    p.add_argument("--copy-probe-mb", type=int, default=0,
+                   help="also run one plain device copy of this many MiB (counter calibration)")
+    return p.parse_args()
+
+
+# algorithmic bytes per query-head (s = bytes per element, D = d_head)
+def alg_bytes(kernel: str, D: int, s: int) -> int:
+    return {
+        "forward": 4 * D * s + 4,        # read q, k, v; write o, lse
+        "bwd_dq": 6 * D * s + 8,         # read q, k, v, o, dO, lse; write dq, Delta
+        "bwd_dkdv": 6 * D * s + 8,       # read q, k, v, dO, lse, Delta; write dk, dv
+        "rope": 2 * D * s,               # read x; write y (per rotated tensor)
+        "fwd+bwd": 12 * D * s + 8,       # forward + backward compulsory traffic
+    }[kernel]
+
+
+class Step:
+    """Buffers of one rotation set and the launches of one step."""
+
+    def __init__(self, wl, call, set_index):
+        import torch
+
+        from paper_2606_28560_amd import inputs
+        from paper_2606_28560_amd import fibattn as F
+
+        self.F = F
+        self.call = call
+        x = inputs.attention_inputs(wl.B, wl.H, wl.T, wl.D, wl.dtype, wl.case, 1000 + set_index)
+        dev = "cuda"
+        self.q, self.k, self.v, self.dO = (x[n].to(dev) for n in ("q", "k", "v", "dO"))
+        self.qr, self.kr, self.o = (torch.empty_like(self.q) for _ in range(3))
+        self.dq, self.dk, self.dv = (torch.empty_like(self.q) for _ in range(3))
+        self.lse = torch.empty((wl.B, wl.H, wl.T), device=dev, dtype=torch.float32)
+        self.da = torch.empty(1, device=dev, dtype=torch.float32)
+        need = F.fibattn_backward_workspace_bytes(wl.B, wl.H, wl.T, wl.D, call.W, len(call.base))
+        self.ws = torch.empty(need, device=dev, dtype=torch.uint8)
+
+    def forward(self):
+        F, c = self.F, self.call
+        F.fibattn_rope(self.q, out=self.qr)
+        F.fibattn_rope(self.k, out=self.kr)
+        F.fibattn_forward(self.qr, self.kr, self.v, c.W, c.base, c.alpha, o=self.o, lse=self.lse)
+
+    def backward(self):
+        F, c = self.F, self.call
+        F.fibattn_backward(self.qr, self.kr, self.v, self.o, self.lse, self.dO, c.W, c.base, c.alpha,
+                           dq=self.dq, dk=self.dk, dv=self.dv, dalpha=self.da, workspace=self.ws)
+        F.fibattn_rope(self.dq, transpose=True, out=self.dq)
+        F.fibattn_rope(self.dk, transpose=True, out=self.dk)
+
+    def __call__(self):
+        self.forward()
+        self.backward()
+
+
+def capture(fn):
+    import torch
+
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        fn()  # warm the allocator-free path once outside the graph
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        fn()
+    torch.cuda.synchronize()
+    return g
+
+
+def timed(run, steps: int, warmup: int):
+    """Mean ms per step over `steps` calls of run(i), after `warmup` calls."""
+    import torch
+
+    for i in range(warmup):
+        run(i)
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    t0.record()
+    for i in range(steps):
+        run(i)
+    t1.record()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - w0) * 1e3 / steps
+    return t0.elapsed_time(t1) / steps, wall
+
+
+def kernel_time(F, sets, kernel: str, steps: int, per_step: int):
+    """Mean launch duration (ms) of one library kernel over `steps` eager steps, from
+    HIP events the library records around each launch on the launch stream."""
+    import torch
+
+    torch.cuda.synchronize()
+    F.fibattn_timing_begin(kernel, steps * per_step)
+    for i in range(steps):
+        sets[i % len(sets)]()
+    ms, n = F.fibattn_timing_end()
+    return ms, n
+
+
+def cpu_baseline(wl, call, target_s: float):
+    """The fp64 oracle (as it stands) on a bounded sample of the same step."""
+    import oracle
+    from paper_2606_28560_amd import inputs
+
+    b = wl.B  # the whole layer: B x H x T query-heads (OpenMP over the B*H pairs)
+    x = inputs.attention_inputs(b, wl.H, wl.T, wl.D, wl.dtype, wl.case, 1000)
+    q, k, v, dO = (x[n].double().numpy() for n in ("q", "k", "v", "dO"))
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        qr, kr = oracle.rope(q), oracle.rope(k)
+        oracle.forward(qr, kr, v, call.W, call.base, call.alpha)
+        dq, dk, dv, da, _ = oracle.backward(qr, kr, v, dO, call.W, call.base, call.alpha)
+        oracle.rope(dq, transpose=True)
+        oracle.rope(dk, transpose=True)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= target_s or reps >= 1000:
+            break
+    qh = reps * b * wl.H * wl.T
+    return {
+        "value": qh / el,
+        "unit": "queries·heads/s",
+        "cores": min(oracle.num_threads(), b * wl.H),
+        "kind": "oracle",
+        "sample": f"{reps} x the full step (RoPE, forward, backward, R^T) of one layer "
+                  f"({b}x{wl.H}x{wl.T} query-heads), {el:.1f} s",
+    }
+
+
+def t4096_figure(steps: int, warmup: int, eager: bool):
+    """fwd+bwd step at the 4x-length shape (B=4, H=8, T=4096, coprime layer 1)."""
+    from paper_2606_28560_amd import workloads
+
+    wl = workloads.workload("extrap_coprime16_T4096")
+    call = wl.calls[1]
+    sets = [Step(wl, call, i) for i in range(3)]
+    if eager:
+        run = lambda i: sets[i % len(sets)]()  # noqa: E731
+        fwd = lambda i: sets[i % len(sets)].forward()  # noqa: E731
+    else:
+        gs = [capture(s) for s in sets]
+        gf = [capture(s.forward) for s in sets]
+        run = lambda i: gs[i % len(gs)].replay()  # noqa: E731
+        fwd = lambda i: gf[i % len(gf)].replay()  # noqa: E731
+    ms, _ = timed(run, steps, warmup)
+    msf, _ = timed(fwd, steps, warmup)
+    qh = wl.queries_heads
+    return {"workload": wl.name, "alpha": float(call.alpha), "ms_per_step": ms,
+            "value": qh / (ms * 1e-3), "fwd_only_ms": msf, "fwd_only_value": qh / (msf * 1e-3)}
+
+
+def main():
+    args = parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): "
+              "this build has no multi-GPU path; rerun with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2606_28560_amd import fibattn as F
+    from paper_2606_28560_amd import workloads
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    F.lib()
+    wl = workloads.workload(args.workload)
+    call = wl.calls[0]
+    s = 2 if wl.dtype == "bf16" else 4
+    per_set = wl.queries_heads * wl.D * s * 10
+    nsets = args.sets or max(3, -(-320 * 2**20 // per_set))
+    print(f"# workload {wl.name}: B{wl.B} H{wl.H} T{wl.T} D{wl.D} {wl.dtype} W{call.W} "
+          f"{call.base_name} alpha={float(call.alpha)}; {nsets} buffer sets", file=sys.stderr, flush=True)
+    sets = [Step(wl, call, i) for i in range(nsets)]
+    torch.cuda.synchronize()
+
+    if args.eager:
+        run = lambda i: sets[i % nsets]()  # noqa: E731
+    else:
+        graphs = [capture(st) for st in sets]
+        run = lambda i: graphs[i % nsets].replay()  # noqa: E731
+    ms, wall_ms = timed(run, args.steps, args.warmup)
+    qh = wl.queries_heads
+    print(f"# step {ms:.4f} ms (host wall {wall_ms:.4f} ms/step)", file=sys.stderr, flush=True)
+
+    # attention only (forward + backward kernels, no RoPE)
+    if args.eager:
+        attn_run = lambda i: attn_one(F, sets[i % nsets])  # noqa: E731
+    else:
+        ag = [capture(lambda st=st: attn_one(F, st)) for st in sets]
+        attn_run = lambda i: ag[i % nsets].replay()  # noqa: E731
+    ms_attn, _ = timed(attn_run, args.steps, args.warmup)
+
+    # per-kernel mean durations (eager steps, library HIP events on the launch stream)
+    kt = {}
+    for kname in ("forward", "bwd_dq", "bwd_dkdv", "rope"):
+        per = 4 if kname == "rope" else 1
+        kms, n = kernel_time(F, sets, kname, args.steps, per)
+        kt[kname] = {"mean_ms": kms, "launches": n}
+    per_step = {k: v["mean_ms"] * (4 if k == "rope" else 1) for k, v in kt.items()}
+    dom = max(per_step, key=per_step.get)
+    units = qh  # query-heads per launch (RoPE: rows of one tensor per launch)
+    achieved = alg_bytes(dom, wl.D, s) * units / (kt[dom]["mean_ms"] * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+                "bytes_per_launch": alg_bytes(dom, wl.D, s) * units,
+                "mean_launch_ms": kt[dom]["mean_ms"]}
+
+    result = {
+        "metric": METRIC,
+        "value": qh / (ms * 1e-3),
+        "unit": "queries·heads/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "T": wl.T, "d_head": wl.D,
+                   "W": call.W, "base": call.base_name, "alpha": float(call.alpha),
+                   "step": "rope(q,k) + forward + backward + rope^T(dq,dk)",
+                   "launch": "eager" if args.eager else "hip_graph", "buffer_sets": nsets},
+        "roofline": roofline,
+        "attention_only": {"ms_per_step": ms_attn, "value": qh / (ms_attn * 1e-3),
+                           "alg_GBs": alg_bytes("fwd+bwd", wl.D, s) * qh / (ms_attn * 1e-3) / 1e9},
+        "kernels": kt,
+    }
+    if not args.no_t4096:
+        result["t4096"] = t4096_figure(max(5, args.steps // 4), 2, args.eager)
+    if args.copy_probe_mb:
+        a = torch.empty(args.copy_probe_mb * 2**20, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        result["copy_probe_bytes"] = a.numel()
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, call, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+def attn_one(F, st):
+    c = st.call
+    F.fibattn_forward(st.qr, st.kr, st.v, c.W, c.base, c.alpha, o=st.o, lse=st.lse)
+    F.fibattn_backward(st.qr, st.kr, st.v, st.o, st.lse, st.dO, c.W, c.base, c.alpha,
+                       dq=st.dq, dk=st.dk, dv=st.dv, dalpha=st.da, workspace=st.ws)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,149 @@
+/*
+ * fibattn.h - C ABI of libfibattn.so: Fibonacci-offset sparse attention on AMD
+ * Instinct MI355X (gfx950).
+ *
+ * Operation (Section 2 of "Depth-Staggered Fibonacci Spacing for Sparse Attention",
+ * paragraphs "Attended set" and "Implementation note"):
+ *   query i of each (batch b, head h) attends to
+ *     - the dense local window, distances delta = 0..W (truncated at position 0);
+ *     - K rung distances d_k = alpha * f_k shared by every query, f being an offset
+ *       base table (the Fibonacci base 1,2,3,5,...,987 or a power-of-2 control).
+ *   A rung is read at the continuous position i - d_k: its key and value are the
+ *   linear blend (1 - w_k) * row[i - floor(d_k)] + w_k * row[i - floor(d_k) - 1],
+ *   w_k = d_k - floor(d_k).  Logits are tau * <q_i, key>, tau = 1/sqrt(d_head);
+ *   the output is the softmax-weighted sum of the (blended) values.
+ *   RoPE is applied to q and k at their true positions before the gather
+ *   (fibattn_rope; Section 2 "Attended set", Section 3 "Model and training").
+ *
+ * Conventions where the paper is silent (the oracle follows the same ones):
+ *   - d_k = fl32(alpha * f_k): one IEEE float32 multiply, round to nearest even;
+ *   - rungs with d_k <= W coincide with window distances (the attended set is a
+ *     union) and are dropped; equal rung distances are kept once;
+ *   - a rung with d_k > i reaches before position 0 and is masked for query i;
+ *   - the rows are i - floor(d) and i - floor(d) - 1; row -1 (reached only when
+ *     w == 0) is a zero vector, which matters only for dalpha.
+ *
+ * Memory and ownership:
+ *   - every tensor pointer is DEVICE memory owned by the caller, contiguous,
+ *     16-byte aligned, layout [B, H, T, d_head] (row = one position of one head);
+ *   - lse is float32 [B, H, T]; dalpha is one float32 on the device;
+ *   - `base` is a HOST array of K strictly increasing int32 values >= 1; it is
+ *     read during the call and not retained;
+ *   - the library allocates no device memory; the backward's scratch space is the
+ *     caller's `workspace` buffer.
+ *
+ * Execution: each call validates its arguments on the host, then enqueues kernels
+ * on `stream` (0 = the null stream) and returns without synchronising.  Faults
+ * inside kernels surface at the caller's next synchronisation.  Results are
+ * bitwise deterministic from run to run (no atomics; fixed-order reductions).
+ *
+ * Errors: a call with invalid arguments returns a status code and enqueues
+ * nothing; it never aborts or throws.
+ */
+#ifndef FIBATTN_H
+#define FIBATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FIBATTN_OK = 0,
+    FIBATTN_ERR_INVALID_ARG = 1,  /* null/misaligned pointer, bad size, bad base table, bad alpha */
+    FIBATTN_ERR_UNSUPPORTED = 2,  /* valid but not implemented: d_head, W or K beyond the limits */
+    FIBATTN_ERR_WORKSPACE = 3,    /* backward workspace missing or too small */
+    FIBATTN_ERR_HIP = 4           /* a kernel launch failed (hipGetLastError) */
+} fibattn_status_t;
+
+typedef enum {
+    FIBATTN_FP32 = 0,             /* float32 storage and arithmetic */
+    FIBATTN_BF16 = 1              /* bfloat16 storage, float32 arithmetic, one rounding per output */
+} fibattn_dtype_t;
+
+#define FIBATTN_MAX_RUNGS 32      /* K <= 32 */
+#define FIBATTN_MAX_WINDOW 128    /* W <= 128 */
+
+/*
+ * Rung table (host only, no GPU needed): the offsets every query shares.
+ * Writes, in increasing distance, floor(d_k) to d0[], w_k to w[] and f_k to f[]
+ * for the rungs kept after the inclusion and dedupe rules above, and their count
+ * to *n.  Arrays must hold FIBATTN_MAX_RUNGS entries.
+ * Returns FIBATTN_ERR_INVALID_ARG for a bad base table, K or alpha.
+ */
+fibattn_status_t fibattn_rung_table(float alpha, const int32_t *base, int K, int W,
+                                    int32_t *d0, float *w, int32_t *f, int *n);
+
+/*
+ * Forward (Section 2 "Attended set").
+ *   q, k : post-RoPE queries and keys, dtype, [B,H,T,d_head]
+ *   v    : values, dtype, [B,H,T,d_head]
+ *   o    : output, dtype, [B,H,T,d_head] (written)
+ *   lse  : float32 [B,H,T] (written): natural-log log-sum-exp of the tau-scaled
+ *          logits of each query, saved for the backward
+ * Limits: d_head in {32, 64}; 0 <= W <= FIBATTN_MAX_WINDOW; 0 <= K <= FIBATTN_MAX_RUNGS;
+ * alpha finite and > 0; B*H <= 65535.
+ */
+fibattn_status_t fibattn_forward(const void *q, const void *k, const void *v,
+                                 void *o, float *lse,
+                                 int B, int H, int T, int d_head, int W,
+                                 const int32_t *base, int K, float alpha,
+                                 fibattn_dtype_t dtype, hipStream_t stream);
+
+/* Bytes of device workspace fibattn_backward needs for these sizes (0 for bad sizes). */
+size_t fibattn_backward_workspace_bytes(int B, int H, int T, int d_head, int W, int K);
+
+/*
+ * Backward: exact gradient of the forward, the inclusion masks held constant
+ * (a hard mask carries no gradient to alpha; Section 2 "Implementation note").
+ *   q, k, v, o, lse : as passed to / returned by fibattn_forward
+ *   dO   : upstream gradient of o, dtype, [B,H,T,d_head]
+ *   dq, dk, dv : gradients (written), dtype; accumulated in float32, rounded once
+ *   dalpha : device float32 (overwritten): sum over b, h, i and rung entries of
+ *            f_k * dL/dw_k (dw_k/dalpha = f_k); reduced in float64 in fixed order
+ *   workspace : device buffer of at least fibattn_backward_workspace_bytes(...)
+ * Same limits as the forward.
+ */
+fibattn_status_t fibattn_backward(const void *q, const void *k, const void *v,
+                                  const void *o, const float *lse, const void *dO,
+                                  void *dq, void *dk, void *dv, float *dalpha,
+                                  void *workspace, size_t workspace_bytes,
+                                  int B, int H, int T, int d_head, int W,
+                                  const int32_t *base, int K, float alpha,
+                                  fibattn_dtype_t dtype, hipStream_t stream);
+
+/*
+ * RoPE at the true positions t = 0..T-1 (Section 2 "Attended set"; base 1e4 in
+ * Section 3).  Rotate-half pairing: (x_j, x_{j+D/2}) rotates by the angle
+ * t * rope_base^(-2j/D), j < D/2; angles are evaluated in float64 and their cosine
+ * and sine rounded to float32.  transpose != 0 applies the inverse rotation R^T,
+ * which carries gradients of rotated tensors back to the unrotated ones.
+ *   x : input, dtype, [B,H,T,d_head];  y : output (may equal x), same layout.
+ * Limits: d_head in {32, 64}; rope_base finite and > 1.
+ */
+fibattn_status_t fibattn_rope(const void *x, void *y, int B, int H, int T, int d_head,
+                              float rope_base, int transpose,
+                              fibattn_dtype_t dtype, hipStream_t stream);
+
+/* Human-readable name of a status code (static storage). */
+const char *fibattn_status_string(fibattn_status_t status);
+
+/*
+ * Kernel timing (instrumentation for benchmarks; not thread-safe).
+ * fibattn_timing_begin(id, capacity) makes the library record a HIP event pair
+ * on the launch stream around each of the next `capacity` launches of kernel `id`
+ * (0 rope, 1 forward, 2 backward dq+dalpha, 3 backward dk/dv, 4 dalpha reduce).
+ * fibattn_timing_end(&avg_ms, &count) synchronises on the last event, returns
+ * the mean launch duration and the number of launches timed, and stops timing.
+ */
+fibattn_status_t fibattn_timing_begin(int kernel_id, int capacity);
+fibattn_status_t fibattn_timing_end(float *avg_ms, int *count);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FIBATTN_H */

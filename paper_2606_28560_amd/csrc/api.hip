@@ -1,0 +1,210 @@
+// C ABI of libfibattn.so: argument validation, the host rung table, workspace
+// layout and kernel timing.  The declarations and their contracts are in
+// include/fibattn.h.
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <vector>
+
+#include "../../include/fibattn.h"
+#include "launch.h"
+
+using namespace fibattn;
+
+namespace {
+
+// d_k = fl32(alpha * f_k) as one float32 multiply (volatile keeps the product a
+// separately rounded float even under aggressive host optimisation).
+fibattn_status_t build_table(float alpha, const int32_t *base, int K, int W, RungTable *rt) {
+    if (K < 0 || K > FIBATTN_MAX_RUNGS || (K > 0 && base == nullptr)) return FIBATTN_ERR_INVALID_ARG;
+    if (!(alpha > 0.f) || !isfinite(alpha)) return FIBATTN_ERR_INVALID_ARG;
+    int n = 0;
+    float last = -1.f;
+    for (int a = 0; a < K; ++a) {
+        if (base[a] < 1) return FIBATTN_ERR_INVALID_ARG;
+        if (a > 0 && base[a] <= base[a - 1]) return FIBATTN_ERR_INVALID_ARG;
+        volatile float fa = (float)base[a];
+        volatile float d = alpha * fa;
+        const float dd = d;
+        if (!isfinite(dd) || dd > 2147483520.f) return FIBATTN_ERR_INVALID_ARG;
+        if (!(dd > (float)W)) continue;   // coincides with the window: union, not counted twice
+        if (n > 0 && dd == last) continue;  // equal distances are one entry
+        const float fl = floorf(dd);
+        rt->d0[n] = (int)fl;
+        rt->w[n] = dd - fl;               // exact in float32
+        rt->f[n] = base[a];
+        last = dd;
+        ++n;
+    }
+    rt->n = n;
+    return FIBATTN_OK;
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+fibattn_status_t check_common(int B, int H, int T, int d_head, int W, int K, fibattn_dtype_t dtype) {
+    if (B < 1 || H < 1 || T < 1 || W < 0 || K < 0) return FIBATTN_ERR_INVALID_ARG;
+    if (dtype != FIBATTN_FP32 && dtype != FIBATTN_BF16) return FIBATTN_ERR_INVALID_ARG;
+    if ((long long)B * H > 65535) return FIBATTN_ERR_UNSUPPORTED;
+    if ((long long)B * H * T * d_head > (1ll << 40)) return FIBATTN_ERR_UNSUPPORTED;
+    if (d_head != 32 && d_head != 64) return FIBATTN_ERR_UNSUPPORTED;
+    if (W > FIBATTN_MAX_WINDOW || K > FIBATTN_MAX_RUNGS) return FIBATTN_ERR_UNSUPPORTED;
+    return FIBATTN_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// ---- kernel timing -------------------------------------------------------
+struct Timing {
+    int id = -1;
+    int capacity = 0;
+    std::vector<hipEvent_t> ev;  // start/stop pairs
+    int used = 0;
+    bool open = false;
+} g_timing;
+
+}  // namespace
+
+namespace fibattn {
+
+void timing_before(int id, hipStream_t s) {
+    if (id != g_timing.id || g_timing.used >= g_timing.capacity) return;
+    (void)hipEventRecord(g_timing.ev[2 * g_timing.used], s);
+    g_timing.open = true;
+}
+
+void timing_after(int id, hipStream_t s) {
+    if (id != g_timing.id || !g_timing.open) return;
+    (void)hipEventRecord(g_timing.ev[2 * g_timing.used + 1], s);
+    g_timing.open = false;
+    ++g_timing.used;
+}
+
+}  // namespace fibattn
+
+extern "C" {
+
+fibattn_status_t fibattn_rung_table(float alpha, const int32_t *base, int K, int W, int32_t *d0,
+                                    float *w, int32_t *f, int *n) {
+    if (!d0 || !w || !f || !n || W < 0) return FIBATTN_ERR_INVALID_ARG;
+    RungTable rt;
+    fibattn_status_t st = build_table(alpha, base, K, W, &rt);
+    if (st != FIBATTN_OK) return st;
+    for (int a = 0; a < rt.n; ++a) { d0[a] = rt.d0[a]; w[a] = rt.w[a]; f[a] = rt.f[a]; }
+    *n = rt.n;
+    return FIBATTN_OK;
+}
+
+fibattn_status_t fibattn_forward(const void *q, const void *k, const void *v, void *o, float *lse,
+                                 int B, int H, int T, int d_head, int W, const int32_t *base,
+                                 int K, float alpha, fibattn_dtype_t dtype, hipStream_t stream) {
+    fibattn_status_t st = check_common(B, H, T, d_head, W, K, dtype);
+    if (st != FIBATTN_OK) return st;
+    if (!q || !k || !v || !o || !lse) return FIBATTN_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse))
+        return FIBATTN_ERR_INVALID_ARG;
+    RungTable rt;
+    st = build_table(alpha, base, K, W, &rt);
+    if (st != FIBATTN_OK) return st;
+    hipError_t e = launch_forward((int)dtype, d_head, q, k, v, o, lse, B * H, T, W, rt, stream);
+    return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
+size_t fibattn_backward_workspace_bytes(int B, int H, int T, int d_head, int W, int K) {
+    if (check_common(B, H, T, d_head, W, K, FIBATTN_FP32) != FIBATTN_OK) return 0;
+    // Delta (float32 [B,H,T]) then the per-workgroup dalpha partials (float64);
+    // sized for the larger of the two dtypes' partial counts.
+    size_t np = bwd_num_partials(0, d_head, B * H, T);
+    size_t np1 = bwd_num_partials(1, d_head, B * H, T);
+    if (np1 > np) np = np1;
+    return align256(sizeof(float) * (size_t)B * H * T) + align256(sizeof(double) * np);
+}
+
+fibattn_status_t fibattn_backward(const void *q, const void *k, const void *v, const void *o,
+                                  const float *lse, const void *dO, void *dq, void *dk, void *dv,
+                                  float *dalpha, void *workspace, size_t workspace_bytes, int B,
+                                  int H, int T, int d_head, int W, const int32_t *base, int K,
+                                  float alpha, fibattn_dtype_t dtype, hipStream_t stream) {
+    fibattn_status_t st = check_common(B, H, T, d_head, W, K, dtype);
+    if (st != FIBATTN_OK) return st;
+    if (!q || !k || !v || !o || !lse || !dO || !dq || !dk || !dv || !dalpha)
+        return FIBATTN_ERR_INVALID_ARG;
+    const void *ptrs[] = {q, k, v, o, lse, dO, dq, dk, dv};
+    for (const void *p : ptrs)
+        if (!aligned16(p)) return FIBATTN_ERR_INVALID_ARG;
+    if (!workspace || !aligned16(workspace) ||
+        workspace_bytes < fibattn_backward_workspace_bytes(B, H, T, d_head, W, K))
+        return FIBATTN_ERR_WORKSPACE;
+    RungTable rt;
+    st = build_table(alpha, base, K, W, &rt);
+    if (st != FIBATTN_OK) return st;
+    float *delta_ws = (float *)workspace;
+    double *partials = (double *)((char *)workspace + align256(sizeof(float) * (size_t)B * H * T));
+    hipError_t e = launch_backward((int)dtype, d_head, q, k, v, o, lse, dO, dq, dk, dv, dalpha,
+                                   delta_ws, partials, B * H, T, W, rt, stream);
+    return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
+fibattn_status_t fibattn_rope(const void *x, void *y, int B, int H, int T, int d_head,
+                              float rope_base, int transpose, fibattn_dtype_t dtype,
+                              hipStream_t stream) {
+    if (B < 1 || H < 1 || T < 1 || !x || !y) return FIBATTN_ERR_INVALID_ARG;
+    if (dtype != FIBATTN_FP32 && dtype != FIBATTN_BF16) return FIBATTN_ERR_INVALID_ARG;
+    if (!(rope_base > 1.f) || !isfinite(rope_base)) return FIBATTN_ERR_INVALID_ARG;
+    if (d_head != 32 && d_head != 64) return FIBATTN_ERR_UNSUPPORTED;
+    if ((long long)B * H > 65535ll * 16) return FIBATTN_ERR_UNSUPPORTED;
+    hipError_t e = launch_rope((int)dtype, d_head, x, y, B * H, T, rope_base, transpose, stream);
+    return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
+const char *fibattn_status_string(fibattn_status_t s) {
+    switch (s) {
+        case FIBATTN_OK: return "ok";
+        case FIBATTN_ERR_INVALID_ARG: return "invalid argument";
+        case FIBATTN_ERR_UNSUPPORTED: return "unsupported size or configuration";
+        case FIBATTN_ERR_WORKSPACE: return "workspace missing or too small";
+        case FIBATTN_ERR_HIP: return "HIP launch error";
+    }
+    return "unknown status";
+}
+
+fibattn_status_t fibattn_timing_begin(int kernel_id, int capacity) {
+    if (kernel_id < 0 || kernel_id >= kNumKernels || capacity < 1 || capacity > 1 << 16)
+        return FIBATTN_ERR_INVALID_ARG;
+    for (hipEvent_t e : g_timing.ev) (void)hipEventDestroy(e);
+    g_timing.ev.assign(2 * (size_t)capacity, nullptr);
+    for (auto &e : g_timing.ev)
+        if (hipEventCreate(&e) != hipSuccess) return FIBATTN_ERR_HIP;
+    g_timing.id = kernel_id;
+    g_timing.capacity = capacity;
+    g_timing.used = 0;
+    g_timing.open = false;
+    return FIBATTN_OK;
+}
+
+fibattn_status_t fibattn_timing_end(float *avg_ms, int *count) {
+    if (!avg_ms || !count) return FIBATTN_ERR_INVALID_ARG;
+    *avg_ms = 0.f;
+    *count = g_timing.used;
+    fibattn_status_t st = FIBATTN_OK;
+    if (g_timing.used > 0) {
+        if (hipEventSynchronize(g_timing.ev[2 * g_timing.used - 1]) != hipSuccess) st = FIBATTN_ERR_HIP;
+        double tot = 0.0;
+        for (int a = 0; a < g_timing.used && st == FIBATTN_OK; ++a) {
+            float ms = 0.f;
+            if (hipEventElapsedTime(&ms, g_timing.ev[2 * a], g_timing.ev[2 * a + 1]) != hipSuccess)
+                st = FIBATTN_ERR_HIP;
+            tot += ms;
+        }
+        *avg_ms = (float)(tot / g_timing.used);
+    }
+    for (hipEvent_t e : g_timing.ev) (void)hipEventDestroy(e);
+    g_timing.ev.clear();
+    g_timing.id = -1;
+    g_timing.capacity = 0;
+    g_timing.used = 0;
+    return st;
+}
+
+}  // extern "C"

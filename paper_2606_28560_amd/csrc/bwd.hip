@@ -1,0 +1,294 @@
+// Backward kernels: dq + dalpha (query-stationary), dk/dv (key-stationary, no
+// atomics), and the fixed-order dalpha reduction.
+//
+// The gradient is that of the forward in fwd.hip with the inclusion masks held
+// constant (Section 2 "Implementation note": a hard mask carries no gradient to
+// alpha, so alpha acts only through the blend weights, dw_k/dalpha = f_k).
+// With p_e = exp(s_e - lse_i), Delta_i = <dO_i, o_i>, dP_e = <dO_i, vhat_e> and
+// dS_e = p_e (dP_e - Delta_i):
+//   dq_i   = tau sum_e dS_e khat_e
+//   dk_j   = sum over entries e that read row j of  weight_e(j) tau dS_e q_i
+//   dv_j   = sum over entries e that read row j of  weight_e(j) p_e dO_i
+//   dL/dw  = tau dS_e <q_i, k[r1] - k[r0]> + p_e <dO_i, v[r1] - v[r0]>  (rung entries)
+//   dalpha = sum_{b,h,i,rungs} f_k dL/dw
+// The row -1 (reached only when w == 0) is a zero vector.
+//
+// Because every rung offset is shared, the queries that read key row j are again a
+// fixed set of shifted positions: j .. j+W through the window, and j + floor(d_k)
+// (as the row r0, weight 1-w) and j + floor(d_k) + 1 (as r1, weight w) through rung k.
+// The dk/dv kernel therefore owns one key row per lane group and gathers its
+// contributions, so every dk/dv row is written once, without atomics.
+#include "launch.h"
+
+namespace fibattn {
+
+// ---------------------------------------------------------------------------
+// dq, Delta and per-workgroup dalpha partials.
+// ---------------------------------------------------------------------------
+template <typename S, int D>
+__global__ __launch_bounds__(256) void bwd_dq_kernel(
+    const S *__restrict__ q, const S *__restrict__ k, const S *__restrict__ v,
+    const S *__restrict__ o, const float *__restrict__ lse, const S *__restrict__ dO,
+    S *__restrict__ dq, float *__restrict__ delta_out, double *__restrict__ partials, int T,
+    int W, RungTable rt, float tau) {
+    constexpr int VN = Vec<S>::N;
+    constexpr int LPQ = D / VN;
+    constexpr int QPB = 256 / LPQ;
+    __shared__ double red[256];
+
+    const int g = threadIdx.x / LPQ;
+    const int sub = threadIdx.x % LPQ;
+    const int i = blockIdx.x * QPB + g;
+    const size_t off = (size_t)blockIdx.y * T * D;
+    const S *Q = q + off;
+    const S *K = k + off;
+    const S *V = v + off;
+    const int col = sub * VN;
+    const float sl2 = tau * kLog2e;
+
+    double dal = 0.0;
+    if (i < T) {
+        float qv[VN], gv[VN], kv[VN], vv[VN], acc[VN];
+        Vec<S>::load(Q + (size_t)i * D + col, qv);
+        Vec<S>::load(dO + off + (size_t)i * D + col, gv);
+        Vec<S>::load(o + off + (size_t)i * D + col, kv);
+        const float delta = group_sum<LPQ>(dot<VN>(gv, kv));
+        if (sub == 0) delta_out[(size_t)blockIdx.y * T + i] = delta;
+        const float lse2 = lse[(size_t)blockIdx.y * T + i] * kLog2e;
+#pragma unroll
+        for (int c = 0; c < VN; ++c) acc[c] = 0.f;
+
+        const int wmax = min(W, i);
+        for (int d = 0; d <= wmax; ++d) {
+            const size_t row = (size_t)(i - d) * D + col;
+            Vec<S>::load(K + row, kv);
+            Vec<S>::load(V + row, vv);
+            const float s = group_sum<LPQ>(dot<VN>(qv, kv));
+            const float dP = group_sum<LPQ>(dot<VN>(gv, vv));
+            const float p = exp2f(s * sl2 - lse2);
+            const float c = tau * p * (dP - delta);
+#pragma unroll
+            for (int x = 0; x < VN; ++x) acc[x] = fmaf(c, kv[x], acc[x]);
+        }
+        for (int r = 0; r < rt.n; ++r) {
+            const int d0 = rt.d0[r];
+            const float w = rt.w[r];
+            if (!(d0 < i || (d0 == i && w == 0.f))) break;
+            const int r0 = i - d0;
+            float k1[VN], v1[VN];
+            Vec<S>::load(K + (size_t)r0 * D + col, kv);
+            Vec<S>::load(V + (size_t)r0 * D + col, vv);
+            if (r0 >= 1) {
+                Vec<S>::load(K + (size_t)(r0 - 1) * D + col, k1);
+                Vec<S>::load(V + (size_t)(r0 - 1) * D + col, v1);
+            } else {
+#pragma unroll
+                for (int x = 0; x < VN; ++x) { k1[x] = 0.f; v1[x] = 0.f; }
+            }
+            const float s0 = group_sum<LPQ>(dot<VN>(qv, kv));
+            const float s1 = group_sum<LPQ>(dot<VN>(qv, k1));
+            const float dP0 = group_sum<LPQ>(dot<VN>(gv, vv));
+            const float dP1 = group_sum<LPQ>(dot<VN>(gv, v1));
+            const float s = (1.f - w) * s0 + w * s1;
+            const float dP = (1.f - w) * dP0 + w * dP1;
+            const float p = exp2f(s * sl2 - lse2);
+            const float dS = p * (dP - delta);
+            const float c = tau * dS;
+            const float c0 = c * (1.f - w);
+            const float c1 = c * w;
+#pragma unroll
+            for (int x = 0; x < VN; ++x) acc[x] = fmaf(c0, kv[x], fmaf(c1, k1[x], acc[x]));
+            const float gw = c * (s1 - s0) + p * (dP1 - dP0);
+            dal += (double)rt.f[r] * (double)gw;
+        }
+        Vec<S>::store(dq + off + (size_t)i * D + col, acc);
+    }
+    red[threadIdx.x] = (sub == 0 && i < T) ? dal : 0.0;
+    __syncthreads();
+#pragma unroll
+    for (int st = 128; st >= 1; st >>= 1) {
+        if (threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) partials[(size_t)blockIdx.y * gridDim.x + blockIdx.x] = red[0];
+}
+
+// ---------------------------------------------------------------------------
+// dk, dv: one key row per lane group.
+// ---------------------------------------------------------------------------
+template <typename S, int D>
+__global__ __launch_bounds__(256) void bwd_dkdv_kernel(
+    const S *__restrict__ q, const S *__restrict__ k, const S *__restrict__ v,
+    const float *__restrict__ lse, const S *__restrict__ dO, const float *__restrict__ delta_in,
+    S *__restrict__ dk, S *__restrict__ dv, int T, int W, RungTable rt, float tau) {
+    constexpr int VN = Vec<S>::N;
+    constexpr int LPQ = D / VN;
+    constexpr int QPB = 256 / LPQ;
+
+    const int g = threadIdx.x / LPQ;
+    const int sub = threadIdx.x % LPQ;
+    const int j = blockIdx.x * QPB + g;
+    if (j >= T) return;  // whole lane groups leave together; no block barrier below
+    const size_t off = (size_t)blockIdx.y * T * D;
+    const S *Q = q + off;
+    const S *K = k + off;
+    const S *V = v + off;
+    const S *G = dO + off;
+    const float *L = lse + (size_t)blockIdx.y * T;
+    const float *Dl = delta_in + (size_t)blockIdx.y * T;
+    const int col = sub * VN;
+    const float sl2 = tau * kLog2e;
+
+    float kj[VN], vj[VN], adk[VN], adv[VN], qv[VN], gv[VN];
+    Vec<S>::load(K + (size_t)j * D + col, kj);
+    Vec<S>::load(V + (size_t)j * D + col, vj);
+#pragma unroll
+    for (int c = 0; c < VN; ++c) { adk[c] = 0.f; adv[c] = 0.f; }
+
+    // window: queries i = j .. j+W read row j with weight 1
+    const int imax = min(T - 1, j + W);
+    for (int i = j; i <= imax; ++i) {
+        Vec<S>::load(Q + (size_t)i * D + col, qv);
+        Vec<S>::load(G + (size_t)i * D + col, gv);
+        const float s = group_sum<LPQ>(dot<VN>(qv, kj));
+        const float dP = group_sum<LPQ>(dot<VN>(gv, vj));
+        const float p = exp2f(s * sl2 - L[i] * kLog2e);
+        const float c = tau * p * (dP - Dl[i]);
+#pragma unroll
+        for (int x = 0; x < VN; ++x) {
+            adk[x] = fmaf(c, qv[x], adk[x]);
+            adv[x] = fmaf(p, gv[x], adv[x]);
+        }
+    }
+    // rungs
+    for (int r = 0; r < rt.n; ++r) {
+        const int d0 = rt.d0[r];
+        const float w = rt.w[r];
+        const int i0 = j + d0;
+        if (i0 >= T) break;  // d0 increases with r
+        float kn[VN], vn[VN];
+        // query i0 reads row j as r0 (weight 1-w) and row j-1 as r1; included iff w <= j
+        if (w == 0.f || j >= 1) {
+            Vec<S>::load(Q + (size_t)i0 * D + col, qv);
+            Vec<S>::load(G + (size_t)i0 * D + col, gv);
+            float s = (1.f - w) * dot<VN>(qv, kj);
+            float dP = (1.f - w) * dot<VN>(gv, vj);
+            if (w != 0.f) {
+                Vec<S>::load(K + (size_t)(j - 1) * D + col, kn);
+                Vec<S>::load(V + (size_t)(j - 1) * D + col, vn);
+                s = fmaf(w, dot<VN>(qv, kn), s);
+                dP = fmaf(w, dot<VN>(gv, vn), dP);
+            }
+            s = group_sum<LPQ>(s);
+            dP = group_sum<LPQ>(dP);
+            const float p = exp2f(s * sl2 - L[i0] * kLog2e);
+            const float c = tau * p * (dP - Dl[i0]) * (1.f - w);
+            const float pw = p * (1.f - w);
+#pragma unroll
+            for (int x = 0; x < VN; ++x) {
+                adk[x] = fmaf(c, qv[x], adk[x]);
+                adv[x] = fmaf(pw, gv[x], adv[x]);
+            }
+        }
+        // query i0+1 reads row j+1 as r0 and row j as r1 (weight w); always included
+        const int i1 = i0 + 1;
+        if (w != 0.f && i1 < T) {
+            Vec<S>::load(Q + (size_t)i1 * D + col, qv);
+            Vec<S>::load(G + (size_t)i1 * D + col, gv);
+            Vec<S>::load(K + (size_t)(j + 1) * D + col, kn);
+            Vec<S>::load(V + (size_t)(j + 1) * D + col, vn);
+            float s = fmaf(1.f - w, dot<VN>(qv, kn), w * dot<VN>(qv, kj));
+            float dP = fmaf(1.f - w, dot<VN>(gv, vn), w * dot<VN>(gv, vj));
+            s = group_sum<LPQ>(s);
+            dP = group_sum<LPQ>(dP);
+            const float p = exp2f(s * sl2 - L[i1] * kLog2e);
+            const float c = tau * p * (dP - Dl[i1]) * w;
+            const float pw = p * w;
+#pragma unroll
+            for (int x = 0; x < VN; ++x) {
+                adk[x] = fmaf(c, qv[x], adk[x]);
+                adv[x] = fmaf(pw, gv[x], adv[x]);
+            }
+        }
+    }
+    Vec<S>::store(dk + off + (size_t)j * D + col, adk);
+    Vec<S>::store(dv + off + (size_t)j * D + col, adv);
+}
+
+// ---------------------------------------------------------------------------
+// dalpha: one workgroup sums the partials in a fixed order, in float64.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void dalpha_reduce_kernel(const double *__restrict__ partials,
+                                                            size_t n, float *__restrict__ dalpha) {
+    __shared__ double red[256];
+    double s = 0.0;
+    for (size_t t = threadIdx.x; t < n; t += 256) s += partials[t];
+    red[threadIdx.x] = s;
+    __syncthreads();
+#pragma unroll
+    for (int st = 128; st >= 1; st >>= 1) {
+        if (threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *dalpha = (float)red[0];
+}
+
+template <typename S, int D>
+static size_t num_partials_t(int BH, int T) {
+    constexpr int QPB = 256 / (D / Vec<S>::N);
+    return (size_t)((T + QPB - 1) / QPB) * (size_t)BH;
+}
+
+size_t bwd_num_partials(int dtype, int D, int BH, int T) {
+    if (dtype == 0 && D == 32) return num_partials_t<float, 32>(BH, T);
+    if (dtype == 0 && D == 64) return num_partials_t<float, 64>(BH, T);
+    if (dtype == 1 && D == 32) return num_partials_t<uint16_t, 32>(BH, T);
+    if (dtype == 1 && D == 64) return num_partials_t<uint16_t, 64>(BH, T);
+    return 0;
+}
+
+template <typename S, int D>
+static hipError_t launch_bwd_t(const void *q, const void *k, const void *v, const void *o,
+                               const float *lse, const void *dO, void *dq, void *dk, void *dv,
+                               float *dalpha, float *delta_ws, double *partials, int BH, int T,
+                               int W, const RungTable &rt, hipStream_t s) {
+    constexpr int QPB = 256 / (D / Vec<S>::N);
+    const float tau = 1.f / sqrtf((float)D);
+    dim3 grid((T + QPB - 1) / QPB, BH);
+    timing_before(kBwdDq, s);
+    hipLaunchKernelGGL((bwd_dq_kernel<S, D>), grid, dim3(256), 0, s, (const S *)q, (const S *)k,
+                       (const S *)v, (const S *)o, lse, (const S *)dO, (S *)dq, delta_ws,
+                       partials, T, W, rt, tau);
+    timing_after(kBwdDq, s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    timing_before(kBwdDkDv, s);
+    hipLaunchKernelGGL((bwd_dkdv_kernel<S, D>), grid, dim3(256), 0, s, (const S *)q,
+                       (const S *)k, (const S *)v, lse, (const S *)dO, delta_ws, (S *)dk,
+                       (S *)dv, T, W, rt, tau);
+    timing_after(kBwdDkDv, s);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    timing_before(kDalphaReduce, s);
+    hipLaunchKernelGGL(dalpha_reduce_kernel, dim3(1), dim3(256), 0, s, partials,
+                       (size_t)grid.x * grid.y, dalpha);
+    timing_after(kDalphaReduce, s);
+    return hipGetLastError();
+}
+
+hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const void *v,
+                           const void *o, const float *lse, const void *dO, void *dq, void *dk,
+                           void *dv, float *dalpha, float *delta_ws, double *partials, int BH,
+                           int T, int W, const RungTable &rt, hipStream_t s) {
+#define FIBATTN_BWD(S_, D_)                                                                  \
+    return launch_bwd_t<S_, D_>(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials, \
+                                BH, T, W, rt, s)
+    if (dtype == 0 && D == 32) FIBATTN_BWD(float, 32);
+    if (dtype == 0 && D == 64) FIBATTN_BWD(float, 64);
+    if (dtype == 1 && D == 32) FIBATTN_BWD(uint16_t, 32);
+    if (dtype == 1 && D == 64) FIBATTN_BWD(uint16_t, 64);
+#undef FIBATTN_BWD
+    return hipErrorInvalidValue;
+}
+
+}  // namespace fibattn

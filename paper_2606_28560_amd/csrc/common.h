@@ -1,0 +1,83 @@
+// Device-side helpers shared by the fibattn kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fibattn {
+
+constexpr int kMaxRungs = 32;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// Rung table passed by value in the kernel arguments: the offsets every query of a
+// launch shares (floor of the distance, blend weight, base value), increasing d.
+struct RungTable {
+    int n;
+    int d0[kMaxRungs];
+    float w[kMaxRungs];
+    int f[kMaxRungs];
+};
+
+// ---- storage types -------------------------------------------------------
+// A lane moves 16 bytes of a row at a time: 4 float32 or 8 bfloat16 values.
+__device__ __forceinline__ float bf16_lo(uint32_t x) { return __uint_as_float(x << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t x) { return __uint_as_float(x & 0xffff0000u); }
+
+// float32 -> bfloat16 bits, round to nearest even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+template <typename S> struct Vec;
+
+template <> struct Vec<float> {
+    static constexpr int N = 4;
+    __device__ __forceinline__ static void load(const float *p, float *x) {
+        float4 t = *reinterpret_cast<const float4 *>(p);
+        x[0] = t.x; x[1] = t.y; x[2] = t.z; x[3] = t.w;
+    }
+    __device__ __forceinline__ static void store(float *p, const float *x) {
+        *reinterpret_cast<float4 *>(p) = make_float4(x[0], x[1], x[2], x[3]);
+    }
+};
+
+template <> struct Vec<uint16_t> {
+    static constexpr int N = 8;
+    __device__ __forceinline__ static void load(const uint16_t *p, float *x) {
+        uint4 t = *reinterpret_cast<const uint4 *>(p);
+        x[0] = bf16_lo(t.x); x[1] = bf16_hi(t.x);
+        x[2] = bf16_lo(t.y); x[3] = bf16_hi(t.y);
+        x[4] = bf16_lo(t.z); x[5] = bf16_hi(t.z);
+        x[6] = bf16_lo(t.w); x[7] = bf16_hi(t.w);
+    }
+    __device__ __forceinline__ static void store(uint16_t *p, const float *x) {
+        uint4 t;
+        t.x = f32_to_bf16(x[0]) | (f32_to_bf16(x[1]) << 16);
+        t.y = f32_to_bf16(x[2]) | (f32_to_bf16(x[3]) << 16);
+        t.z = f32_to_bf16(x[4]) | (f32_to_bf16(x[5]) << 16);
+        t.w = f32_to_bf16(x[6]) | (f32_to_bf16(x[7]) << 16);
+        *reinterpret_cast<uint4 *>(p) = t;
+    }
+};
+
+// Sum over the G lanes of an aligned lane group (G a power of two, G <= 64).
+template <int G>
+__device__ __forceinline__ float group_sum(float x) {
+#pragma unroll
+    for (int m = G / 2; m >= 1; m >>= 1) x += __shfl_xor(x, m, 64);
+    return x;
+}
+
+template <int N>
+__device__ __forceinline__ float dot(const float *a, const float *b) {
+    float s = 0.f;
+#pragma unroll
+    for (int c = 0; c < N; ++c) s = fmaf(a[c], b[c], s);
+    return s;
+}
+
+}  // namespace fibattn

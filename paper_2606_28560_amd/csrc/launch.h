@@ -1,0 +1,32 @@
+// Host-side launchers of the fibattn kernels (internal to libfibattn.so).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace fibattn {
+
+enum KernelId { kRope = 0, kForward = 1, kBwdDq = 2, kBwdDkDv = 3, kDalphaReduce = 4, kNumKernels = 5 };
+
+// Records a HIP event before / after a launch when kernel timing is active for `id`.
+void timing_before(int id, hipStream_t s);
+void timing_after(int id, hipStream_t s);
+
+// dtype: 0 float32, 1 bfloat16.  All launchers return hipGetLastError() of their launches.
+hipError_t launch_forward(int dtype, int D, const void *q, const void *k, const void *v, void *o,
+                          float *lse, int BH, int T, int W, const RungTable &rt, hipStream_t s);
+
+// Number of dalpha partials the dq kernel writes (one per workgroup).
+size_t bwd_num_partials(int dtype, int D, int BH, int T);
+
+hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const void *v,
+                           const void *o, const float *lse, const void *dO, void *dq, void *dk,
+                           void *dv, float *dalpha, float *delta_ws, double *partials, int BH,
+                           int T, int W, const RungTable &rt, hipStream_t s);
+
+hipError_t launch_rope(int dtype, int D, const void *x, void *y, int BH, int T, float rope_base,
+                       int transpose, hipStream_t s);
+
+}  // namespace fibattn

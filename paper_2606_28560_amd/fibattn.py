@@ -1,0 +1,201 @@
+"""Python binding of libfibattn.so (argument marshalling only).
+
+Every function has the name of the C entry point it calls (include/fibattn.h).
+Tensors are torch CUDA (HIP) tensors used only as device memory; every step of the
+attention runs in the library's HIP kernels, launched on torch's current stream.
+There is no fallback: if the library is missing or a call fails, these functions
+raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfibattn.so")
+
+FIBATTN_FP32, FIBATTN_BF16 = 0, 1
+MAX_RUNGS = 32
+MAX_WINDOW = 128
+KERNEL_IDS = {"rope": 0, "forward": 1, "bwd_dq": 2, "bwd_dkdv": 3, "dalpha_reduce": 4}
+EXPORTED = ("fibattn_rung_table", "fibattn_forward", "fibattn_backward_workspace_bytes",
+            "fibattn_backward", "fibattn_rope", "fibattn_status_string",
+            "fibattn_timing_begin", "fibattn_timing_end")
+
+
+class FibattnError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn} failed: status {status} ({status_string(status)})")
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libfibattn.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                          "(or python -m paper_2606_28560_amd.build)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i, f, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    ip = ctypes.POINTER(ctypes.c_int32)
+    fp = ctypes.POINTER(ctypes.c_float)
+    L.fibattn_rung_table.argtypes = [f, ip, i, i, ip, fp, ip, ctypes.POINTER(ctypes.c_int)]
+    L.fibattn_rung_table.restype = i
+    L.fibattn_forward.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, ip, i, f, i, vp]
+    L.fibattn_forward.restype = i
+    L.fibattn_backward_workspace_bytes.argtypes = [i, i, i, i, i, i]
+    L.fibattn_backward_workspace_bytes.restype = sz
+    L.fibattn_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+                                   i, i, i, i, i, ip, i, f, i, vp]
+    L.fibattn_backward.restype = i
+    L.fibattn_rope.argtypes = [vp, vp, i, i, i, i, f, i, i, vp]
+    L.fibattn_rope.restype = i
+    L.fibattn_status_string.argtypes = [i]
+    L.fibattn_status_string.restype = ctypes.c_char_p
+    L.fibattn_timing_begin.argtypes = [i, i]
+    L.fibattn_timing_begin.restype = i
+    L.fibattn_timing_end.argtypes = [fp, ctypes.POINTER(ctypes.c_int)]
+    L.fibattn_timing_end.restype = i
+    _lib = L
+    return L
+
+
+def status_string(status: int) -> str:
+    return lib().fibattn_status_string(int(status)).decode()
+
+
+def _check(fn: str, status: int):
+    if status != 0:
+        raise FibattnError(fn, status)
+
+
+def _base_array(base):
+    b = np.ascontiguousarray(np.asarray(list(base), dtype=np.int32))
+    return b, b.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def _dtype_code(t) -> int:
+    import torch
+
+    if t.dtype == torch.float32:
+        return FIBATTN_FP32
+    if t.dtype == torch.bfloat16:
+        return FIBATTN_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; expected float32 or bfloat16")
+
+
+def _stream(stream):
+    import torch
+
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check_tensor(name, t, shape, dtype):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+
+
+def fibattn_rung_table(alpha: float, base, W: int):
+    """Host rung table: list of (floor(d_k), w_k, f_k) in increasing distance."""
+    b, bp = _base_array(base)
+    d0 = (ctypes.c_int32 * MAX_RUNGS)()
+    w = (ctypes.c_float * MAX_RUNGS)()
+    f = (ctypes.c_int32 * MAX_RUNGS)()
+    n = ctypes.c_int(0)
+    st = lib().fibattn_rung_table(ctypes.c_float(alpha), bp, b.size, int(W), d0, w, f, ctypes.byref(n))
+    _check("fibattn_rung_table", st)
+    return [(int(d0[a]), np.float32(w[a]), int(f[a])) for a in range(n.value)]
+
+
+def fibattn_forward(q, k, v, W: int, base, alpha: float, *, o=None, lse=None, stream=None):
+    """o, lse = forward of post-RoPE q, k and v ([B,H,T,D], float32 or bfloat16)."""
+    import torch
+
+    B, H, T, D = q.shape
+    for n_, t in (("q", q), ("k", k), ("v", v)):
+        _check_tensor(n_, t, q.shape, q.dtype)
+    if o is None:
+        o = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, H, T), device=q.device, dtype=torch.float32)
+    _check_tensor("o", o, q.shape, q.dtype)
+    _check_tensor("lse", lse, (B, H, T), torch.float32)
+    b, bp = _base_array(base)
+    st = lib().fibattn_forward(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
+                               B, H, T, D, int(W), bp, b.size, ctypes.c_float(alpha),
+                               _dtype_code(q), _stream(stream))
+    _check("fibattn_forward", st)
+    return o, lse
+
+
+def fibattn_backward_workspace_bytes(B: int, H: int, T: int, d_head: int, W: int, K: int) -> int:
+    return int(lib().fibattn_backward_workspace_bytes(B, H, T, d_head, int(W), int(K)))
+
+
+def fibattn_backward(q, k, v, o, lse, dO, W: int, base, alpha: float, *, dq=None, dk=None, dv=None,
+                     dalpha=None, workspace=None, stream=None):
+    """dq, dk, dv, dalpha (a 1-element float32 device tensor)."""
+    import torch
+
+    B, H, T, D = q.shape
+    for n_, t in (("q", q), ("k", k), ("v", v), ("o", o), ("dO", dO)):
+        _check_tensor(n_, t, q.shape, q.dtype)
+    _check_tensor("lse", lse, (B, H, T), torch.float32)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    for n_, t in (("dq", dq), ("dk", dk), ("dv", dv)):
+        _check_tensor(n_, t, q.shape, q.dtype)
+    if dalpha is None:
+        dalpha = torch.empty(1, device=q.device, dtype=torch.float32)
+    b, bp = _base_array(base)
+    need = fibattn_backward_workspace_bytes(B, H, T, D, W, b.size)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), device=q.device, dtype=torch.uint8)
+    st = lib().fibattn_backward(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
+                                dO.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                                dalpha.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                                B, H, T, D, int(W), bp, b.size, ctypes.c_float(alpha),
+                                _dtype_code(q), _stream(stream))
+    _check("fibattn_backward", st)
+    return dq, dk, dv, dalpha
+
+
+def fibattn_rope(x, rope_base: float = 10000.0, transpose: bool = False, *, out=None, stream=None):
+    """RoPE at true positions (out may be x itself); transpose applies R^T."""
+    import torch
+
+    B, H, T, D = x.shape
+    _check_tensor("x", x, x.shape, x.dtype)
+    out = torch.empty_like(x) if out is None else out
+    _check_tensor("out", out, x.shape, x.dtype)
+    st = lib().fibattn_rope(x.data_ptr(), out.data_ptr(), B, H, T, D, ctypes.c_float(rope_base),
+                            int(bool(transpose)), _dtype_code(x), _stream(stream))
+    _check("fibattn_rope", st)
+    return out
+
+
+def fibattn_timing_begin(kernel: str, capacity: int):
+    _check("fibattn_timing_begin", lib().fibattn_timing_begin(KERNEL_IDS[kernel], int(capacity)))
+
+
+def fibattn_timing_end():
+    """(mean launch duration in ms, number of launches timed)."""
+    ms = ctypes.c_float(0.0)
+    n = ctypes.c_int(0)
+    _check("fibattn_timing_end", lib().fibattn_timing_end(ctypes.byref(ms), ctypes.byref(n)))
+    return float(ms.value), int(n.value)

@@ -1,0 +1,90 @@
+"""Host-only checks of the C ABI (no GPU): the library loads, exports every entry
+point include/fibattn.h declares, builds the same rung table as the oracle's
+independent code, and rejects invalid arguments before touching the device."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_28560_amd import fibattn as F
+from paper_2606_28560_amd import schedules, workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "fibattn.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(fibattn_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = header_functions()
+    assert len(names) >= 8
+    L = F.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(F.EXPORTED)
+
+
+def _all_alphas():
+    al = [1.0, 0.5, 1.5, 0.7310586, 0.01, 3.7]
+    for w in workloads.all_workloads():
+        al += [float(c.alpha) for c in w.calls]
+    return sorted(set(al))
+
+
+@pytest.mark.parametrize("W", [0, 6, 8, 10, 12])
+def test_rung_table_matches_oracle(W):
+    for base in (schedules.FIB15, schedules.POW2_11, (3, 7, 11, 1000)):
+        for a in _all_alphas():
+            lib_tab = F.fibattn_rung_table(a, base, W)
+            orc_tab = [(d0, w, f) for (d0, w, f, _) in oracle.rungs(a, base, W)]
+            assert lib_tab == orc_tab, (a, base, W)
+
+
+def test_stagger_float32_floor_cases():
+    # float32 products that round up to an integer where the float64 product does not
+    lin = schedules.alpha_linear_stagger(16)
+    hits = []
+    for l, a in enumerate(lin):
+        for f in schedules.FIB15:
+            if np.floor(np.float32(a) * np.float32(f)) != np.floor(float(a) * f):
+                hits.append((l, f))
+    assert hits == [(3, 610), (5, 144), (6, 610), (10, 144), (12, 610)]
+    tab = {f: (d0, w) for d0, w, f in F.fibattn_rung_table(lin[3], schedules.FIB15, 8)}
+    assert tab[610] == (427, 0.0)
+
+
+def test_rung_table_rejects_bad_input():
+    for alpha, base in ((0.0, [1, 2]), (-1.0, [1]), (float("nan"), [1]), (1.0, [2, 2]),
+                        (1.0, [0, 3]), (1.0, list(range(1, 40)))):
+        with pytest.raises(F.FibattnError):
+            F.fibattn_rung_table(alpha, base, 8)
+
+
+def test_invalid_arguments_return_codes_without_gpu():
+    L = F.lib()
+    b = (ctypes.c_int32 * 15)(*schedules.FIB15)
+    one = ctypes.c_float(1.0)
+    # null pointers
+    assert L.fibattn_forward(None, None, None, None, None, 1, 1, 8, 64, 8, b, 15, one, 1, None) == 1
+    # bad sizes
+    assert L.fibattn_forward(16, 16, 16, 16, 16, 0, 1, 8, 64, 8, b, 15, one, 1, None) == 1
+    assert L.fibattn_forward(16, 16, 16, 16, 16, 1, 1, 8, 128, 8, b, 15, one, 1, None) == 2
+    assert L.fibattn_forward(16, 16, 16, 16, 16, 1, 1, 8, 64, 129, b, 15, one, 1, None) == 2
+    assert L.fibattn_forward(16, 16, 16, 16, 16, 1, 1, 8, 64, 8, b, 15, one, 9, None) == 1
+    # workspace
+    assert L.fibattn_backward(16, 16, 16, 16, 16, 16, 16, 16, 16, 16, None, 0,
+                              1, 1, 8, 64, 8, b, 15, one, 1, None) == 3
+    assert L.fibattn_backward_workspace_bytes(1, 1, 8, 48, 8, 15) == 0
+    assert L.fibattn_backward_workspace_bytes(8, 8, 1024, 64, 8, 15) > 8 * 8 * 1024 * 4
+    # rope
+    assert L.fibattn_rope(None, None, 1, 1, 8, 64, ctypes.c_float(1e4), 0, 1, None) == 1
+    assert L.fibattn_rope(16, 16, 1, 1, 8, 64, ctypes.c_float(1.0), 0, 1, None) == 1
+    assert L.fibattn_rope(16, 16, 1, 1, 8, 96, ctypes.c_float(1e4), 0, 1, None) == 2
+    for s in range(5):
+        assert F.status_string(s)
