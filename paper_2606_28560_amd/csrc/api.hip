@@ -19,6 +19,7 @@ namespace {
 fibattn_status_t build_table(float alpha, const int32_t *base, int K, int W, RungTable *rt) {
     if (K < 0 || K > FIBATTN_MAX_RUNGS || (K > 0 && base == nullptr)) return FIBATTN_ERR_INVALID_ARG;
     if (!(alpha > 0.f) || !isfinite(alpha)) return FIBATTN_ERR_INVALID_ARG;
+    memset(rt, 0, sizeof(*rt));  // unused entries are read (and masked) by batched kernels
     int n = 0;
     float last = -1.f;
     for (int a = 0; a < K; ++a) {
@@ -117,7 +118,9 @@ size_t fibattn_backward_workspace_bytes(int B, int H, int T, int d_head, int W, 
     // sized for the larger of the two dtypes' partial counts.
     size_t np = bwd_num_partials(0, d_head, B * H, T);
     size_t np1 = bwd_num_partials(1, d_head, B * H, T);
+    size_t np2 = bwd_mfma_num_partials(B * H, T);
     if (np1 > np) np = np1;
+    if (np2 > np) np = np2;
     return align256(sizeof(float) * (size_t)B * H * T) + align256(sizeof(double) * np);
 }
 

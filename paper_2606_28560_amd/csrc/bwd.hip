@@ -280,6 +280,9 @@ hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const
                            const void *o, const float *lse, const void *dO, void *dq, void *dk,
                            void *dv, float *dalpha, float *delta_ws, double *partials, int BH,
                            int T, int W, const RungTable &rt, hipStream_t s) {
+    if (backward_mfma_supported(dtype, D, W))
+        return launch_backward_mfma(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials, BH,
+                                    T, W, rt, s);
 #define FIBATTN_BWD(S_, D_)                                                                  \
     return launch_bwd_t<S_, D_>(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials, \
                                 BH, T, W, rt, s)

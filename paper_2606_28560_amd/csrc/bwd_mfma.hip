@@ -1,0 +1,381 @@
+// Backward for bfloat16, d_head = 64, W <= 16 on gfx950 matrix cores + VALU.
+//
+// Same gradient as bwd.hip (the forward's exact gradient with the inclusion masks
+// held constant, Section 2 "Implementation note"), organised like fwd_mfma.hip:
+//
+// dq kernel (query-stationary, 64 queries per workgroup, 16 per wave):
+//   band:  S^T = K.Q^T and dP^T = V.dO^T on the matrix cores (16x32 tiles),
+//          dS = P (dP - Delta), dq^T += K^T (tau dS)^T with K^T staged in LDS;
+//   rungs: per-row bf16 dot2 products for <q, k[r0]>, <q, k[r1]>, <dO, v[r0]>,
+//          <dO, v[r1]> (the r1 terms are needed for dalpha even when w = 0),
+//          dq += tau dS ((1-w) k[r0] + w k[r1]) on the VALU,
+//          dalpha partial += f (tau dS <q, k[r1]-k[r0]> + p <dO, v[r1]-v[r0]>);
+//   writes dq, Delta_i = <dO_i, o_i> and one float64 dalpha partial per workgroup.
+// dk/dv kernel (key-stationary, 64 keys per workgroup, 16 per wave): the queries
+// that read key row j are j..j+W (window) and, for rung k, j+floor(d_k) (as row r0,
+// weight 1-w) and j+floor(d_k)+1 (as row r1, weight w):
+//   band:  S = Q.K^T and dP = dO.V^T tiles, dk^T += Q^T (tau dS), dv^T += dO^T P with
+//          Q^T, dO^T staged in LDS;
+//   rungs: per-row dot2 products on the VALU;
+//   each dk/dv row is written once; no atomics.  Workgroup 0 also sums the dalpha
+//   partials in a fixed order (float64), after the dq kernel has finished.
+#include "launch.h"
+#include "mfma.h"
+
+namespace fibattn {
+
+constexpr int kBwdB = 64;                // rows per workgroup
+constexpr int kStage = kBwdB + 16;       // staged rows
+constexpr int kRowStride = 72;           // bf16 per staged row (row-major)
+constexpr int kTStride = 132;            // bf16 per dim row of a staged transpose
+
+// A operand of a transposed-operand MFMA: dim out_dim(c, n) of the staged rows
+// base + 4g .. +4 and base + 16 + 4g .. +4 (k index 8g+j <-> block j/4, row 4g+j%4).
+__device__ __forceinline__ bf16x8 staged_operand(const uint16_t *st, int c, int n, int base, int g) {
+    const uint16_t *src = st + out_dim(c, n) * kTStride + base + 4 * g;
+    const uint2 a0 = *reinterpret_cast<const uint2 *>(src);
+    const uint2 a1 = *reinterpret_cast<const uint2 *>(src + 16);
+    return as_bf8(make_uint4(a0.x, a0.y, a1.x, a1.y));
+}
+
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void bwd_dq_bf16_d64_kernel(
+    const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
+    const uint16_t *__restrict__ o, const float *__restrict__ lse, const uint16_t *__restrict__ dO,
+    uint16_t *__restrict__ dq, float *__restrict__ delta_out, double *__restrict__ partials, int T,
+    int W, RungTable rt, float tau, int tiles) {
+    __shared__ __align__(16) uint16_t kr[kStage * kRowStride];
+    __shared__ __align__(16) uint16_t vr[kStage * kRowStride];
+    __shared__ __align__(16) uint16_t kt[kD * kTStride];
+    __shared__ double red[4];
+
+    const int lane = threadIdx.x & 63;
+    const int wv = threadIdx.x >> 6;
+    const int nm = lane & 15, gm = lane >> 4;  // MFMA layout
+    const int nq = lane >> 2, gq = lane & 3;   // quad layout
+    const int blk = xcd_remap(blockIdx.x, gridDim.x);
+    const int bh = blk / tiles;
+    const int T0 = (blk % tiles) * kBwdB;
+    const size_t off = (size_t)bh * T * kD;
+    const uint16_t *Q = q + off;
+    const uint16_t *K = k + off;
+    const uint16_t *V = v + off;
+    const uint16_t *G = dO + off;
+    const float *L = lse + (size_t)bh * T;
+    const float sl2 = tau * kLog2e;
+
+    const int t0 = T0 + 16 * wv;
+    const int im = t0 + nm, imc = min(im, T - 1);  // MFMA layout query
+    const int i = t0 + nq, ic = min(i, T - 1);     // quad layout query
+    const Slice qm = load_row(Q, imc, gm);
+    const Slice gmm = load_row(G, imc, gm);
+    const Slice qq = load_row(Q, ic, gq);
+    const Slice gqq = load_row(G, ic, gq);
+    const float delta = quad_sum(dot_slice(gqq, load_slice(o + off + (size_t)ic * kD, gq)));
+    const float delta_m = __shfl(delta, 4 * nm, 64);
+    const float lse2 = L[ic] * kLog2e;
+    const float lse2_m = L[imc] * kLog2e;
+
+    stage_rows(kr, kRowStride, K, T0 - 16, kStage, T);
+    stage_rows(vr, kRowStride, V, T0 - 16, kStage, T);
+    stage_transpose(kt, kTStride, K, T0 - 16, kStage, T);
+    __syncthreads();
+
+    // band (MFMA layout): keys [t0-16, t0+16)
+    uint32_t cw[4];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const int sr = 16 * wv + 16 * b + nm;  // staged row
+        const f32x4 s = mfma_dot64(load_slice(kr + sr * kRowStride, gm), qm, f32x4{0.f, 0.f, 0.f, 0.f});
+        const f32x4 dp = mfma_dot64(load_slice(vr + sr * kRowStride, gm), gmm, f32x4{0.f, 0.f, 0.f, 0.f});
+        float c[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int key = t0 - 16 + 16 * b + 4 * gm + e;
+            const bool ok = key >= 0 && key <= im && im - key <= W;
+            const float p = ok ? fast_exp2(s[e] * sl2 - lse2_m) : 0.f;
+            c[e] = tau * p * (dp[e] - delta_m);
+        }
+        cw[2 * b] = pack_bf16(c[0], c[1]);
+        cw[2 * b + 1] = pack_bf16(c[2], c[3]);
+    }
+    const bf16x8 C = as_bf8(make_uint4(cw[0], cw[1], cw[2], cw[3]));
+    Acc16 acc;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+        acc.c[c] = mfma(staged_operand(kt, c, nm, 16 * wv, gm), C, f32x4{0.f, 0.f, 0.f, 0.f});
+    acc_to_quad(acc, lane);
+
+    // rungs (quad layout), two at a time: the four rows of each (k, v at r0 and r1)
+    // of a batch are loaded together; r1 = -1 is the zero row
+    double dal = 0.0;
+    const int last = t0 + 15;
+    int nact = 0;
+#pragma unroll
+    for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && rt.d0[r] <= last) ? 1 : 0;
+#pragma unroll
+    for (int rb = 0; rb < kMaxRungs; rb += 2) {
+        if (rb < nact) {
+            Slice k0[2], v0[2], k1[2], v1[2];
+#pragma unroll
+            for (int x = 0; x < 2; ++x) {
+                const int R0 = min(max(i - rt.d0[rb + x], 0), T - 1);
+                const int R1 = max(R0 - 1, 0);
+                k0[x] = load_row(K, R0, gq);
+                v0[x] = load_row(V, R0, gq);
+                k1[x] = load_row(K, R1, gq);
+                v1[x] = load_row(V, R1, gq);
+            }
+#pragma unroll
+            for (int x = 0; x < 2; ++x) {
+                const int r = rb + x;
+                const int d0 = rt.d0[r];
+                const float w = rt.w[r];
+                const bool incl = r < nact && i < T && (d0 < i || (d0 == i && w == 0.f));
+                const bool has1 = i - d0 - 1 >= 0;  // row r1 exists (else the zero row)
+                const float s0 = quad_sum(dot_slice(qq, k0[x]));
+                const float s1r = quad_sum(dot_slice(qq, k1[x]));
+                const float p0 = quad_sum(dot_slice(gqq, v0[x]));
+                const float p1r = quad_sum(dot_slice(gqq, v1[x]));
+                const float s1 = has1 ? s1r : 0.f;
+                const float p1 = has1 ? p1r : 0.f;
+                const float s = (1.f - w) * s0 + w * s1;
+                const float dP = (1.f - w) * p0 + w * p1;
+                const float p = incl ? fast_exp2(s * sl2 - lse2) : 0.f;
+                const float cc = tau * p * (dP - delta);
+                acc_axpy2(acc, cc * (1.f - w), k0[x], cc * w, k1[x]);
+                if (gq == 0 && incl) dal += (double)rt.f[r] * (double)(cc * (s1 - s0) + p * (p1 - p0));
+            }
+        }
+    }
+
+    if (i < T) {
+        store_acc(dq + off + (size_t)i * kD, gq, acc, 1.f);
+        if (gq == 0) delta_out[(size_t)bh * T + i] = delta;
+    }
+    // workgroup dalpha partial: wave sums, then the four waves in order
+#pragma unroll
+    for (int st = 32; st >= 1; st >>= 1) dal += __shfl_xor(dal, st, 64);
+    if (lane == 0) red[wv] = dal;
+    __syncthreads();
+    if (threadIdx.x == 0) partials[blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
+}
+
+// ---------------------------------------------------------------------------
+template <bool INTERP>
+__global__ __launch_bounds__(256) void bwd_dkdv_bf16_d64_kernel(
+    const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
+    const float *__restrict__ lse, const uint16_t *__restrict__ dO, const float *__restrict__ delta_in,
+    uint16_t *__restrict__ dk, uint16_t *__restrict__ dv, const double *__restrict__ partials,
+    int n_partials, float *__restrict__ dalpha, int T, int W, RungTable rt, float tau, int tiles) {
+    __shared__ __align__(16) uint16_t qr[kStage * kRowStride];
+    __shared__ __align__(16) uint16_t gr[kStage * kRowStride];
+    __shared__ __align__(16) uint16_t qt[kD * kTStride];
+    __shared__ __align__(16) uint16_t gt[kD * kTStride];
+    __shared__ float sl[kStage], sd[kStage];
+    __shared__ double red[256];
+
+    const int lane = threadIdx.x & 63;
+    const int wv = threadIdx.x >> 6;
+    const int nm = lane & 15, gm = lane >> 4;  // MFMA layout
+    const int nq = lane >> 2, gq = lane & 3;   // quad layout
+    const int blk = xcd_remap(blockIdx.x, gridDim.x);
+    const int bh = blk / tiles;
+    const int T0 = (blk % tiles) * kBwdB;
+    const size_t off = (size_t)bh * T * kD;
+    const uint16_t *Q = q + off;
+    const uint16_t *K = k + off;
+    const uint16_t *V = v + off;
+    const uint16_t *G = dO + off;
+    const float *L = lse + (size_t)bh * T;
+    const float *Dl = delta_in + (size_t)bh * T;
+    const float sl2 = tau * kLog2e;
+
+    // final dalpha: the dq kernel has completed on this stream
+    if (blockIdx.x == 0) {
+        double s = 0.0;
+        for (int t = threadIdx.x; t < n_partials; t += 256) s += partials[t];
+        red[threadIdx.x] = s;
+        __syncthreads();
+        for (int st = 128; st >= 1; st >>= 1) {
+            if (threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+            __syncthreads();
+        }
+        if (threadIdx.x == 0) *dalpha = (float)red[0];
+    }
+
+    const int t0 = T0 + 16 * wv;
+    const int jm = t0 + nm, jmc = min(jm, T - 1);  // MFMA layout key
+    const int j = t0 + nq, jc = min(j, T - 1);     // quad layout key
+    const Slice km = load_row(K, jmc, gm);
+    const Slice vm = load_row(V, jmc, gm);
+    const Slice ks = load_row(K, jc, gq);
+    const Slice vs = load_row(V, jc, gq);
+
+    // stage q, dO rows (row-major and transposed), lse, Delta for queries [T0, T0+80)
+    stage_rows(qr, kRowStride, Q, T0, kStage, T);
+    stage_rows(gr, kRowStride, G, T0, kStage, T);
+    stage_transpose(qt, kTStride, Q, T0, kStage, T);
+    stage_transpose(gt, kTStride, G, T0, kStage, T);
+    for (int c = threadIdx.x; c < kStage; c += 256) {
+        const int row = T0 + c;
+        sl[c] = row < T ? L[row] * kLog2e : 0.f;
+        sd[c] = row < T ? Dl[row] : 0.f;
+    }
+    __syncthreads();
+
+    // band (MFMA layout): queries [t0, t0 + 32) in two blocks
+    uint32_t cw[4], pw[4];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const int sr = 16 * wv + 16 * b + nm;  // staged query row
+        const f32x4 s = mfma_dot64(load_slice(qr + sr * kRowStride, gm), km, f32x4{0.f, 0.f, 0.f, 0.f});
+        const f32x4 dp = mfma_dot64(load_slice(gr + sr * kRowStride, gm), vm, f32x4{0.f, 0.f, 0.f, 0.f});
+        float c[4], p[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int si = 16 * wv + 16 * b + 4 * gm + e;  // staged index of the query
+            const int qi = T0 + si;
+            const bool ok = qi < T && jm < T && qi >= jm && qi - jm <= W;
+            p[e] = ok ? fast_exp2(s[e] * sl2 - sl[si]) : 0.f;
+            c[e] = tau * p[e] * (dp[e] - sd[si]);
+        }
+        cw[2 * b] = pack_bf16(c[0], c[1]);
+        cw[2 * b + 1] = pack_bf16(c[2], c[3]);
+        pw[2 * b] = pack_bf16(p[0], p[1]);
+        pw[2 * b + 1] = pack_bf16(p[2], p[3]);
+    }
+    const bf16x8 Cb = as_bf8(make_uint4(cw[0], cw[1], cw[2], cw[3]));
+    const bf16x8 Pb = as_bf8(make_uint4(pw[0], pw[1], pw[2], pw[3]));
+    Acc16 adk, adv;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        adk.c[c] = mfma(staged_operand(qt, c, nm, 16 * wv, gm), Cb, f32x4{0.f, 0.f, 0.f, 0.f});
+        adv.c[c] = mfma(staged_operand(gt, c, nm, 16 * wv, gm), Pb, f32x4{0.f, 0.f, 0.f, 0.f});
+    }
+    acc_to_quad(adk, lane);
+    acc_to_quad(adv, lane);
+
+    // rungs (quad layout): some key of this wave has j + floor(d) < T for a prefix
+    int nact = 0;
+#pragma unroll
+    for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && t0 + rt.d0[r] < T) ? 1 : 0;
+    if (!INTERP) {
+        // every w == 0: query j + d0 reads this row with weight 1; four rungs per batch
+#pragma unroll
+        for (int rb = 0; rb < kMaxRungs; rb += 4) {
+            if (rb < nact) {
+                Slice q0[4], g0[4];
+                int icq[4];
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    icq[x] = min(j + rt.d0[rb + x], T - 1);
+                    q0[x] = load_row(Q, icq[x], gq);
+                    g0[x] = load_row(G, icq[x], gq);
+                }
+                float cc[4], pp[4];
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    const int i0 = j + rt.d0[rb + x];
+                    const bool in0 = rb + x < nact && j < T && i0 < T;
+                    const float s = quad_sum(dot_slice(q0[x], ks));
+                    const float dp = quad_sum(dot_slice(g0[x], vs));
+                    pp[x] = in0 ? fast_exp2(s * sl2 - L[icq[x]] * kLog2e) : 0.f;
+                    cc[x] = tau * pp[x] * (dp - Dl[icq[x]]);
+                }
+                acc_axpy2(adk, cc[0], q0[0], cc[1], q0[1]);
+                acc_axpy2(adk, cc[2], q0[2], cc[3], q0[3]);
+                acc_axpy2(adv, pp[0], g0[0], pp[1], g0[1]);
+                acc_axpy2(adv, pp[2], g0[2], pp[3], g0[3]);
+            }
+        }
+    } else {
+        // neighbours j-1 and j+1 are shared by every rung
+        const int jmn = min(max(j - 1, 0), T - 1);
+        const int jpn = min(j + 1, T - 1);
+        const Slice kmn = load_row(K, jmn, gq);
+        const Slice vmn = load_row(V, jmn, gq);
+        const Slice kpn = load_row(K, jpn, gq);
+        const Slice vpn = load_row(V, jpn, gq);
+#pragma unroll
+        for (int rb = 0; rb < kMaxRungs; rb += 2) {
+            if (rb < nact) {
+                Slice q0[2], g0[2], q1[2], g1[2];
+#pragma unroll
+                for (int x = 0; x < 2; ++x) {
+                    const int i0c = min(j + rt.d0[rb + x], T - 1);
+                    const int i1c = min(j + rt.d0[rb + x] + 1, T - 1);
+                    q0[x] = load_row(Q, i0c, gq);
+                    g0[x] = load_row(G, i0c, gq);
+                    q1[x] = load_row(Q, i1c, gq);
+                    g1[x] = load_row(G, i1c, gq);
+                }
+#pragma unroll
+                for (int x = 0; x < 2; ++x) {
+                    const int r = rb + x;
+                    const float w = rt.w[r];
+                    // query i0 = j + d0 reads this row as r0 (weight 1 - w) and j-1 as r1
+                    const int i0 = j + rt.d0[r];
+                    const bool in0 = r < nact && j < T && i0 < T && (w == 0.f || j >= 1);
+                    const int i0c = min(i0, T - 1);
+                    const float sa = quad_sum((1.f - w) * dot_slice(q0[x], ks) + w * dot_slice(q0[x], kmn));
+                    const float da = quad_sum((1.f - w) * dot_slice(g0[x], vs) + w * dot_slice(g0[x], vmn));
+                    const float pa = in0 ? fast_exp2(sa * sl2 - L[i0c] * kLog2e) : 0.f;
+                    const float ca = tau * pa * (da - Dl[i0c]);
+                    // query i1 = i0 + 1 reads row j+1 as r0 and this row as r1 (weight w)
+                    const int i1 = i0 + 1;
+                    const bool in1 = r < nact && j < T && i1 < T && w != 0.f;
+                    const int i1c = min(i1, T - 1);
+                    const float sb = quad_sum((1.f - w) * dot_slice(q1[x], kpn) + w * dot_slice(q1[x], ks));
+                    const float db = quad_sum((1.f - w) * dot_slice(g1[x], vpn) + w * dot_slice(g1[x], vs));
+                    const float pb = in1 ? fast_exp2(sb * sl2 - L[i1c] * kLog2e) : 0.f;
+                    const float cb = tau * pb * (db - Dl[i1c]);
+                    acc_axpy2(adk, (1.f - w) * ca, q0[x], w * cb, q1[x]);
+                    acc_axpy2(adv, (1.f - w) * pa, g0[x], w * pb, g1[x]);
+                }
+            }
+        }
+    }
+
+    if (j < T) {
+        store_acc(dk + off + (size_t)j * kD, gq, adk, 1.f);
+        store_acc(dv + off + (size_t)j * kD, gq, adv, 1.f);
+    }
+}
+
+bool backward_mfma_supported(int dtype, int D, int W) { return dtype == 1 && D == 64 && W <= 16; }
+
+size_t bwd_mfma_num_partials(int BH, int T) { return (size_t)((T + kBwdB - 1) / kBwdB) * (size_t)BH; }
+
+hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, const void *o,
+                                const float *lse, const void *dO, void *dq, void *dk, void *dv,
+                                float *dalpha, float *delta_ws, double *partials, int BH, int T,
+                                int W, const RungTable &rt, hipStream_t s) {
+    const int tiles = (T + kBwdB - 1) / kBwdB;
+    const float tau = 1.f / sqrtf(64.f);
+    const int nb = tiles * BH;
+    timing_before(kBwdDq, s);
+    hipLaunchKernelGGL(bwd_dq_bf16_d64_kernel, dim3(nb), dim3(256), 0, s, (const uint16_t *)q,
+                       (const uint16_t *)k, (const uint16_t *)v, (const uint16_t *)o, lse,
+                       (const uint16_t *)dO, (uint16_t *)dq, delta_ws, partials, T, W, rt, tau, tiles);
+    timing_after(kBwdDq, s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    timing_before(kBwdDkDv, s);
+    bool interp = false;
+    for (int r = 0; r < rt.n; ++r) interp = interp || rt.w[r] != 0.f;
+    if (interp)
+        hipLaunchKernelGGL(bwd_dkdv_bf16_d64_kernel<true>, dim3(nb), dim3(256), 0, s,
+                           (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v, lse,
+                           (const uint16_t *)dO, delta_ws, (uint16_t *)dk, (uint16_t *)dv, partials,
+                           nb, dalpha, T, W, rt, tau, tiles);
+    else
+        hipLaunchKernelGGL(bwd_dkdv_bf16_d64_kernel<false>, dim3(nb), dim3(256), 0, s,
+                           (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v, lse,
+                           (const uint16_t *)dO, delta_ws, (uint16_t *)dk, (uint16_t *)dv, partials,
+                           nb, dalpha, T, W, rt, tau, tiles);
+    timing_after(kBwdDkDv, s);
+    return hipGetLastError();
+}
+
+}  // namespace fibattn

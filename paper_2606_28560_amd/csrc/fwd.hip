@@ -123,6 +123,7 @@ static hipError_t launch_fwd_t(const void *q, const void *k, const void *v, void
 
 hipError_t launch_forward(int dtype, int D, const void *q, const void *k, const void *v, void *o,
                           float *lse, int BH, int T, int W, const RungTable &rt, hipStream_t s) {
+    if (forward_mfma_supported(dtype, D, W)) return launch_forward_mfma(q, k, v, o, lse, BH, T, W, rt, s);
     if (dtype == 0 && D == 32) return launch_fwd_t<float, 32>(q, k, v, o, lse, BH, T, W, rt, s);
     if (dtype == 0 && D == 64) return launch_fwd_t<float, 64>(q, k, v, o, lse, BH, T, W, rt, s);
     if (dtype == 1 && D == 32) return launch_fwd_t<uint16_t, 32>(q, k, v, o, lse, BH, T, W, rt, s);

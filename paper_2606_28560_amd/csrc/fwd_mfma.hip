@@ -1,0 +1,197 @@
+// Forward for bfloat16, d_head = 64, W <= 16 on gfx950 matrix cores + VALU.
+//
+// Section 2 "Attended set": query i attends distances 0..W and the rung distances
+// d_k = alpha f_k, shared by all queries.  A workgroup owns 64 consecutive queries of
+// one (batch, head) (four waves of 16).  For a wave's queries [t0, t0+16):
+//   - the window band lies in the 32 key rows [t0-16, t0+16).  Its logits are one
+//     16x32 tile of Q.K^T on the matrix cores, masked to 0 <= i - j <= W; the
+//     probability-weighted values are (V^T P^T) on the matrix cores, with V^T staged
+//     in LDS once per workgroup;
+//   - every rung is a contiguous shifted block: query t0+n reads rows t0+n-floor(d)
+//     and t0+n-floor(d)-1.  Those logits are per-row dot products (bf16 dot2, four
+//     lanes per row) blended in score space; the blended values are accumulated on
+//     the VALU in the same register layout as the matrix-core output.
+// Softmax runs in base 2: the band sets the first running maximum, then rungs are
+// taken a batch at a time (their key and value rows loaded together), rescaling the
+// running sum and weighted values when the maximum grows.
+#include "launch.h"
+#include "mfma.h"
+
+namespace fibattn {
+
+constexpr int kFwdBQ = 64;                 // queries per workgroup
+constexpr int kBandRows = kFwdBQ + 16;     // staged band rows [T0-16, T0+64)
+constexpr int kRowStride = 72;             // bf16 per staged K row (row-major)
+constexpr int kVtStride = 132;             // bf16 per dim row of the staged V^T
+
+// INTERP: some rung has w != 0, so the second row r1 is read.
+template <bool INTERP>
+__global__ __launch_bounds__(256) void fwd_bf16_d64_kernel(
+    const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
+    uint16_t *__restrict__ o, float *__restrict__ lse, int T, int W, RungTable rt, float sl2,
+    int tiles) {
+    constexpr int kFwdRB = INTERP ? 2 : 4;  // rungs per load batch (register budget)
+    __shared__ __align__(16) uint16_t kr[kBandRows * kRowStride];
+    __shared__ __align__(16) uint16_t vt[kD * kVtStride];
+
+    const int lane = threadIdx.x & 63;
+    const int wv = threadIdx.x >> 6;
+    const int nm = lane & 15, gm = lane >> 4;  // MFMA layout
+    const int nq = lane >> 2, gq = lane & 3;   // quad layout
+    const int blk = xcd_remap(blockIdx.x, gridDim.x);
+    const int bh = blk / tiles;
+    const int T0 = (blk % tiles) * kFwdBQ;
+    const size_t off = (size_t)bh * T * kD;
+    const uint16_t *Q = q + off;
+    const uint16_t *K = k + off;
+    const uint16_t *V = v + off;
+
+    const int t0 = T0 + 16 * wv;
+    const int last = t0 + 15;  // the wave's last query
+    // rungs some query of this wave includes: a prefix of the table (sorted by d)
+    int nact = 0;
+#pragma unroll
+    for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && rt.d0[r] <= last) ? 1 : 0;
+
+    const int im = t0 + nm;  // query of this lane in the MFMA layout
+    const int i = t0 + nq;   // ... in the quad layout
+    const Slice qm = load_row(Q, min(im, T - 1), gm);
+    const Slice qq = load_row(Q, min(i, T - 1), gq);
+
+    // band rows [T0-16, T0+64): K row-major, V transposed (zero outside [0, T))
+    stage_rows(kr, kRowStride, K, T0 - 16, kBandRows, T);
+    stage_transpose(vt, kVtStride, V, T0 - 16, kBandRows, T);
+    __syncthreads();
+
+    // ---- window band (MFMA layout): logits (log2 units), maximum, probabilities ----
+    float m = -INFINITY;
+    f32x4 sb[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const Slice kb = load_slice(kr + (16 * wv + 16 * b + nm) * kRowStride, gm);
+        sb[b] = mfma_dot64(kb, qm, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int key = t0 - 16 + 16 * b + 4 * gm + e;
+            const bool ok = key >= 0 && key <= im && im - key <= W;
+            sb[b][e] = ok ? sb[b][e] * sl2 : -INFINITY;
+            m = fmaxf(m, sb[b][e]);
+        }
+    }
+    m = max4(m);
+    if (m == -INFINITY) m = 0.f;  // only rows past the end of the sequence
+    float lb = 0.f;
+    uint32_t pw[4];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        float p[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            p[e] = fast_exp2(sb[b][e] - m);
+            lb += p[e];
+        }
+        pw[2 * b] = pack_bf16(p[0], p[1]);
+        pw[2 * b + 1] = pack_bf16(p[2], p[3]);
+    }
+    float l = sum4(lb);
+    const bf16x8 P = as_bf8(make_uint4(pw[0], pw[1], pw[2], pw[3]));
+    Acc16 acc;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const uint16_t *src = vt + out_dim(c, nm) * kVtStride + 16 * wv + 4 * gm;
+        const uint2 a0 = *reinterpret_cast<const uint2 *>(src);
+        const uint2 a1 = *reinterpret_cast<const uint2 *>(src + 16);
+        acc.c[c] = mfma(as_bf8(make_uint4(a0.x, a0.y, a1.x, a1.y)), P, f32x4{0.f, 0.f, 0.f, 0.f});
+    }
+    // hand the band results to the quad layout
+    acc_to_quad(acc, lane);
+    m = to_quad(m, lane);
+    l = to_quad(l, lane);
+
+    // ---- rungs (quad layout), kFwdRB at a time: all rows of a batch are loaded
+    // together, then the running maximum, sum and weighted values are updated ----
+#pragma unroll
+    for (int rb = 0; rb < kMaxRungs; rb += kFwdRB) {
+        if (rb < nact) {
+            Slice k0[kFwdRB], v0[kFwdRB], k1[kFwdRB], v1[kFwdRB];
+#pragma unroll
+            for (int x = 0; x < kFwdRB; ++x) {
+                const int R0 = min(max(i - rt.d0[rb + x], 0), T - 1);
+                k0[x] = load_row(K, R0, gq);
+                v0[x] = load_row(V, R0, gq);
+                if (INTERP) {
+                    const int R1 = max(R0 - 1, 0);
+                    k1[x] = load_row(K, R1, gq);
+                    v1[x] = load_row(V, R1, gq);
+                }
+            }
+            float s[kFwdRB];
+            float mb = m;
+#pragma unroll
+            for (int x = 0; x < kFwdRB; ++x) {
+                const int r = rb + x;
+                const int d0 = rt.d0[r];
+                const float w = rt.w[r];
+                const bool incl = r < nact && (d0 < i || (d0 == i && w == 0.f));
+                float part = dot_slice(qq, k0[x]);
+                if (INTERP) part = (1.f - w) * part + w * dot_slice(qq, k1[x]);
+                part = quad_sum(part) * sl2;
+                s[x] = incl ? part : -INFINITY;
+                mb = fmaxf(mb, s[x]);
+            }
+            const float scale = fast_exp2(m - mb);
+            m = mb;
+            l *= scale;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) acc.c[c] *= scale;
+            float p[kFwdRB];
+#pragma unroll
+            for (int x = 0; x < kFwdRB; ++x) {
+                p[x] = fast_exp2(s[x] - m);
+                l += p[x];
+            }
+            if (INTERP) {
+#pragma unroll
+                for (int x = 0; x < kFwdRB; ++x) {
+                    const float w = rt.w[rb + x];
+                    acc_axpy2(acc, p[x] * (1.f - w), v0[x], p[x] * w, v1[x]);
+                }
+            } else {
+#pragma unroll
+                for (int x = 0; x < kFwdRB; x += 2) acc_axpy2(acc, p[x], v0[x], p[x + 1], v0[x + 1]);
+            }
+        }
+    }
+
+    if (i < T) {
+        store_acc(o + off + (size_t)i * kD, gq, acc, 1.f / l);
+        if (gq == 0) lse[(size_t)bh * T + i] = (m + log2f(l)) * kLn2;
+    }
+}
+
+static bool any_interp(const RungTable &rt) {
+    for (int r = 0; r < rt.n; ++r)
+        if (rt.w[r] != 0.f) return true;
+    return false;
+}
+
+bool forward_mfma_supported(int dtype, int D, int W) { return dtype == 1 && D == 64 && W <= 16; }
+
+hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void *o, float *lse,
+                               int BH, int T, int W, const RungTable &rt, hipStream_t s) {
+    const int tiles = (T + kFwdBQ - 1) / kFwdBQ;
+    const float sl2 = kLog2e / sqrtf(64.f);
+    timing_before(kForward, s);
+    if (any_interp(rt))
+        hipLaunchKernelGGL(fwd_bf16_d64_kernel<true>, dim3(tiles * BH), dim3(256), 0, s,
+                           (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v,
+                           (uint16_t *)o, lse, T, W, rt, sl2, tiles);
+    else
+        hipLaunchKernelGGL(fwd_bf16_d64_kernel<false>, dim3(tiles * BH), dim3(256), 0, s,
+                           (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v,
+                           (uint16_t *)o, lse, T, W, rt, sl2, tiles);
+    timing_after(kForward, s);
+    return hipGetLastError();
+}
+
+}  // namespace fibattn

@@ -26,6 +26,17 @@ hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const
                            void *dv, float *dalpha, float *delta_ws, double *partials, int BH,
                            int T, int W, const RungTable &rt, hipStream_t s);
 
+// bfloat16, d_head = 64, W <= 16: matrix-core band + VALU rungs (fwd_mfma.hip, bwd_mfma.hip).
+bool forward_mfma_supported(int dtype, int D, int W);
+hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void *o, float *lse,
+                               int BH, int T, int W, const RungTable &rt, hipStream_t s);
+bool backward_mfma_supported(int dtype, int D, int W);
+size_t bwd_mfma_num_partials(int BH, int T);
+hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, const void *o,
+                                const float *lse, const void *dO, void *dq, void *dk, void *dv,
+                                float *dalpha, float *delta_ws, double *partials, int BH, int T,
+                                int W, const RungTable &rt, hipStream_t s);
+
 hipError_t launch_rope(int dtype, int D, const void *x, void *y, int BH, int T, float rope_base,
                        int transpose, hipStream_t s);
 

@@ -1,0 +1,238 @@
+// Helpers for the bfloat16, d_head = 64 kernels built on gfx950 matrix cores.
+//
+// Lane layout shared by these kernels: a wave owns 16 consecutive rows (queries in
+// the forward and dq kernels, keys in the dk/dv kernel).  Lane l serves row
+// n = l % 16 and, with g = l / 16, the head dims [8g, 8g+8) and [32+8g, 32+8g+8)
+// (its "slice"), so a row is spread over the four lanes n, n+16, n+32, n+48 and
+// each 16-byte load instruction reads 64 contiguous bytes of each of 16 rows.
+//
+// This is also the layout of v_mfma_f32_16x16x32_bf16 (A: lane -> row l%16,
+// k = 8(l/16)+j; B: lane -> column l%16, same k; C: lane -> column l%16, rows
+// 4(l/16)+i).  The head-dim contraction of Q.K^T is two MFMAs whose k index 8g+j
+// stands for dim 32s + 8g + j (s = 0, 1): each operand is half of the lane's slice.
+// For products that sum over key/query rows, the output row m = 4g+i of dim block c
+// stands for slice position 4c + i of lane group g (out_dim below), so lane (n, g)
+// ends up holding exactly its own slice of the output row.
+#pragma once
+
+#include "common.h"
+
+namespace fibattn {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kD = 64;
+
+// 16 bfloat16 values of one row slice: a = dims [8g, 8g+8), b = [32+8g, 32+8g+8).
+// Slice position d (0..15) is word d/2, low half for even d; positions 0..7 are in
+// a, 8..15 in b.
+struct Slice {
+    uint4 a, b;
+};
+
+__device__ __forceinline__ Slice load_slice(const uint16_t *row, int g) {
+    Slice s;
+    s.a = *reinterpret_cast<const uint4 *>(row + 8 * g);
+    s.b = *reinterpret_cast<const uint4 *>(row + 32 + 8 * g);
+    return s;
+}
+
+// Slice g of row `row` of a [*, 64] bf16 matrix at a uniform base address: a 32-bit
+// byte offset from the base lets the loads use scalar-base addressing.
+__device__ __forceinline__ Slice load_row(const uint16_t *base, int row, int g) {
+    const uint32_t off = (uint32_t)row * 128u + (uint32_t)g * 16u;
+    const char *p = reinterpret_cast<const char *>(base);
+    Slice s;
+    s.a = *reinterpret_cast<const uint4 *>(p + off);
+    s.b = *reinterpret_cast<const uint4 *>(p + off + 64);
+    return s;
+}
+
+// 2^x with the hardware instruction (no denormal rescaling; x <= 0 here).
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ Slice zero_slice() {
+    Slice s;
+    s.a = make_uint4(0, 0, 0, 0);
+    s.b = make_uint4(0, 0, 0, 0);
+    return s;
+}
+
+__device__ __forceinline__ uint32_t word(const Slice &s, int w) {
+    switch (w) {
+        case 0: return s.a.x; case 1: return s.a.y; case 2: return s.a.z; case 3: return s.a.w;
+        case 4: return s.b.x; case 5: return s.b.y; case 6: return s.b.z; default: return s.b.w;
+    }
+}
+
+__device__ __forceinline__ bf16x2 as_bf2(uint32_t x) { return __builtin_bit_cast(bf16x2, x); }
+__device__ __forceinline__ bf16x8 as_bf8(uint4 x) { return __builtin_bit_cast(bf16x8, x); }
+
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+    f32x2 v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+// <x, y> over the 16 dims of the slice (float32 accumulation of exact bf16 products).
+__device__ __forceinline__ float dot_slice(const Slice &x, const Slice &y) {
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) s = __builtin_amdgcn_fdot2_f32_bf16(as_bf2(word(x, w)), as_bf2(word(y, w)), s, false);
+    return s;
+}
+
+// Sum / max over the four lanes that share a row in the MFMA layout (n, n+16, n+32, n+48).
+__device__ __forceinline__ float sum4(float x) {
+    x += __shfl_xor(x, 16, 64);
+    x += __shfl_xor(x, 32, 64);
+    return x;
+}
+__device__ __forceinline__ float max4(float x) {
+    x = fmaxf(x, __shfl_xor(x, 16, 64));
+    x = fmaxf(x, __shfl_xor(x, 32, 64));
+    return x;
+}
+
+// Quad layout (used where rows are read from global memory one per lane group):
+// lanes 4n .. 4n+3 share row n, lane 4n+g holding slice g of it, so the four lanes
+// of a row read 64 contiguous bytes per load instruction.  Sums over a quad use DPP
+// lane swaps (quad_perm [1,0,3,2] then [2,3,0,1]); every lane must be active.
+__device__ __forceinline__ float quad_sum(float x) {
+    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, false));
+    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xF, 0xF, false));
+    return x;
+}
+
+// acc.c[c][i] holds slice position 4c + i of the lane's row.
+struct Acc16 {
+    f32x4 c[4];
+};
+
+__device__ __forceinline__ void acc_zero(Acc16 &a) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) a.c[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+// acc += a * x (x one bf16 slice), float32 FMAs.
+__device__ __forceinline__ void acc_axpy(Acc16 &acc, float a, const Slice &x) {
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+        const uint32_t u = word(x, w);
+        const int d = 2 * w;
+        acc.c[d >> 2][d & 3] = fmaf(a, bf16_lo(u), acc.c[d >> 2][d & 3]);
+        acc.c[(d + 1) >> 2][(d + 1) & 3] = fmaf(a, bf16_hi(u), acc.c[(d + 1) >> 2][(d + 1) & 3]);
+    }
+}
+
+// acc += a * x + b * y with one bf16 dot2 per dim: the pair (x_d, y_d) is packed
+// with v_perm and the weights (a, b) are rounded to bf16.
+__device__ __forceinline__ void acc_axpy2(Acc16 &acc, float a, const Slice &x, float b, const Slice &y) {
+    const bf16x2 ab = as_bf2(pack_bf16(a, b));
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+        const uint32_t xu = word(x, w), yu = word(y, w);
+        const uint32_t lo = __builtin_amdgcn_perm(yu, xu, 0x05040100u);  // (x_lo, y_lo)
+        const uint32_t hi = __builtin_amdgcn_perm(yu, xu, 0x07060302u);  // (x_hi, y_hi)
+        const int d = 2 * w;
+        acc.c[d >> 2][d & 3] = __builtin_amdgcn_fdot2_f32_bf16(as_bf2(lo), ab, acc.c[d >> 2][d & 3], false);
+        acc.c[(d + 1) >> 2][(d + 1) & 3] =
+            __builtin_amdgcn_fdot2_f32_bf16(as_bf2(hi), ab, acc.c[(d + 1) >> 2][(d + 1) & 3], false);
+    }
+}
+
+// Scaled store of the lane's slice as bf16 (two 16-byte stores).
+__device__ __forceinline__ void store_acc(uint16_t *row, int g, const Acc16 &acc, float scale) {
+    uint4 a, b;
+    a.x = pack_bf16(acc.c[0][0] * scale, acc.c[0][1] * scale);
+    a.y = pack_bf16(acc.c[0][2] * scale, acc.c[0][3] * scale);
+    a.z = pack_bf16(acc.c[1][0] * scale, acc.c[1][1] * scale);
+    a.w = pack_bf16(acc.c[1][2] * scale, acc.c[1][3] * scale);
+    b.x = pack_bf16(acc.c[2][0] * scale, acc.c[2][1] * scale);
+    b.y = pack_bf16(acc.c[2][2] * scale, acc.c[2][3] * scale);
+    b.z = pack_bf16(acc.c[3][0] * scale, acc.c[3][1] * scale);
+    b.w = pack_bf16(acc.c[3][2] * scale, acc.c[3][3] * scale);
+    *reinterpret_cast<uint4 *>(row + 8 * g) = a;
+    *reinterpret_cast<uint4 *>(row + 32 + 8 * g) = b;
+}
+
+// Moves a value from the MFMA layout (row n on lanes n + 16g) to the quad layout
+// (row n on lanes 4n + g): lane 4n + g takes the value of lane n + 16g.
+__device__ __forceinline__ float to_quad(float x, int lane) {
+    return __shfl(x, (lane >> 2) + 16 * (lane & 3), 64);
+}
+__device__ __forceinline__ void acc_to_quad(Acc16 &a, int lane) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) a.c[c][e] = to_quad(a.c[c][e], lane);
+}
+
+// Row-major staging of rows [r_begin, r_begin + nrows) into dst[(row - r_begin) * stride]
+// (zero outside [0, T)); 16-byte coalesced loads and stores.
+__device__ __forceinline__ void stage_rows(uint16_t *dst, int stride, const uint16_t *X, int r_begin,
+                                           int nrows, int T) {
+    for (int c = threadIdx.x; c < nrows * 8; c += blockDim.x) {
+        const int kk = c >> 3, ch = c & 7;
+        const int row = r_begin + kk;
+        uint4 val = make_uint4(0, 0, 0, 0);
+        if (row >= 0 && row < T) val = *reinterpret_cast<const uint4 *>(X + (size_t)row * kD + ch * 8);
+        *reinterpret_cast<uint4 *>(dst + kk * stride + ch * 8) = val;
+    }
+}
+
+__device__ __forceinline__ f32x4 mfma(const bf16x8 &a, const bf16x8 &b, const f32x4 &c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// <row slices> over all 64 dims for 16 rows x 16 columns: A rows from `ar`, B
+// columns from `bc` (both the lane's own slices).
+__device__ __forceinline__ f32x4 mfma_dot64(const Slice &ar, const Slice &bc, f32x4 c) {
+    c = mfma(as_bf8(ar.a), as_bf8(bc.a), c);
+    c = mfma(as_bf8(ar.b), as_bf8(bc.b), c);
+    return c;
+}
+
+// Output dim of row m in dim block c of a transposed-operand MFMA: slice position
+// 4c + (m & 3) of lane group m / 4 (see top).
+__device__ __forceinline__ int out_dim(int c, int m) {
+    return (c < 2 ? 0 : 32) + 8 * (m >> 2) + 4 * (c & 1) + (m & 3);
+}
+
+// Transposed staging of rows [r_begin, r_begin + nrows) of a [*, 64] bf16 matrix into
+// dst[dim * stride + row - r_begin] (zero outside [0, T)).  Each work item reads one
+// 32-bit word (two dims) of four consecutive rows and writes two 8-byte runs.
+// nrows must be a multiple of 4; stride (in bf16) must be a multiple of 4 so that
+// the 8-byte runs are aligned (132 spreads 32 consecutive dim pairs over 16 bank
+// offsets).
+__device__ __forceinline__ void stage_transpose(uint16_t *dst, int stride, const uint16_t *X,
+                                                int r_begin, int nrows, int T) {
+    const int items = (nrows / 4) * 32;
+    for (int u = threadIdx.x; u < items; u += blockDim.x) {
+        const int dp = u & 31;      // dim pair
+        const int rg = u >> 5;      // group of four rows
+        uint32_t a[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int row = r_begin + 4 * rg + r;
+            a[r] = (row >= 0 && row < T) ? reinterpret_cast<const uint32_t *>(X + (size_t)row * kD)[dp] : 0u;
+        }
+        const uint2 lo = make_uint2(__builtin_amdgcn_perm(a[1], a[0], 0x05040100u),
+                                    __builtin_amdgcn_perm(a[3], a[2], 0x05040100u));
+        const uint2 hi = make_uint2(__builtin_amdgcn_perm(a[1], a[0], 0x07060302u),
+                                    __builtin_amdgcn_perm(a[3], a[2], 0x07060302u));
+        *reinterpret_cast<uint2 *>(dst + (2 * dp) * stride + 4 * rg) = lo;
+        *reinterpret_cast<uint2 *>(dst + (2 * dp + 1) * stride + 4 * rg) = hi;
+    }
+}
+
+// Block index -> work item, keeping consecutive work items (the tiles of one
+// (batch, head)) on one XCD: workgroups are dispatched round-robin over 8 XCDs.
+__device__ __forceinline__ int xcd_remap(int b, int nblocks) {
+    if (nblocks & 7) return b;
+    return (b & 7) * (nblocks >> 3) + (b >> 3);
+}
+
+}  // namespace fibattn

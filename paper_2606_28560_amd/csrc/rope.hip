@@ -2,15 +2,15 @@
 // at the true positions before gathering; Section 3: base 1e4).
 //
 // Rotate-half pairing: for j < D/2 the pair (x_j, x_{j+D/2}) of the row at position t
-// rotates by theta = t * base^(-2j/D).  A workgroup owns TP consecutive positions and
-// RB rows (b, h) at those positions; it evaluates cos/sin of its TP * D/2 angles once,
-// in float64, rounds them to float32 in LDS, and rotates every row with them.
+// rotates by theta = t * base^(-2j/D).  A workgroup owns a few consecutive positions
+// and a group of (b, h) rows at those positions; it evaluates cos/sin of its angles
+// once, in float64, rounds them to float32 in LDS, and rotates every row with them.
 #include "launch.h"
 
 namespace fibattn {
 
-constexpr int kRopeTP = 8;   // positions per workgroup
-constexpr int kRopeRB = 16;  // (b, h) rows per workgroup
+constexpr int kRopeTP = 8;   // positions per workgroup (generic kernel)
+constexpr int kRopeRB = 16;  // (b, h) rows per workgroup (generic kernel)
 
 template <typename S> __device__ __forceinline__ float ld1(const S *p);
 template <> __device__ __forceinline__ float ld1<float>(const float *p) { return *p; }
@@ -23,9 +23,9 @@ template <> __device__ __forceinline__ void st1<uint16_t>(uint16_t *p, float x) 
     *p = (uint16_t)f32_to_bf16(x);
 }
 
+// Generic kernel (float32 storage, d_head 32): one element pair per thread.
 template <typename S, int D>
-__global__ __launch_bounds__(256) void rope_kernel(const S *x, S *y,
-                                                   int BH, int T, double rope_base,
+__global__ __launch_bounds__(256) void rope_kernel(const S *x, S *y, int BH, int T, double rope_base,
                                                    int transpose) {
     constexpr int HALF = D / 2;
     __shared__ float cs[kRopeTP * HALF], sn[kRopeTP * HALF];
@@ -58,12 +58,62 @@ __global__ __launch_bounds__(256) void rope_kernel(const S *x, S *y,
     }
 }
 
+// bfloat16, d_head 64: a workgroup owns 4 positions of 16 (b, h) rows (64 rows).
+// Lane group g of a row's four lanes holds dims [8g, 8g+8) and [32+8g, 32+8g+8),
+// i.e. the eight rotate-half pairs (j, j+32), j in [8g, 8g+8): two 16-byte loads
+// and stores per lane, reading 64 contiguous bytes per row per instruction.
+constexpr int kRope64TP = 4;
+constexpr int kRope64RB = 16;
+
+__global__ __launch_bounds__(256) void rope_bf16_d64_kernel(const uint16_t *x, uint16_t *y, int BH,
+                                                            int T, double rope_base, int transpose) {
+    __shared__ float cs[kRope64TP * 32], sn[kRope64TP * 32];
+    const int t0 = blockIdx.x * kRope64TP;
+    if (threadIdx.x < kRope64TP * 32) {
+        const int t = t0 + (threadIdx.x >> 5);
+        const int jj = threadIdx.x & 31;
+        const double ang = (double)t * pow(rope_base, -2.0 * (double)jj / 64.0);
+        double sv, cv;
+        sincos(ang, &sv, &cv);
+        cs[threadIdx.x] = (float)cv;
+        sn[threadIdx.x] = transpose ? -(float)sv : (float)sv;
+    }
+    __syncthreads();
+    const int g = threadIdx.x & 3;
+    const int rr = threadIdx.x >> 2;          // 0..63
+    const int tt = rr & (kRope64TP - 1);
+    const int t = t0 + tt;
+    const int bh = blockIdx.y * kRope64RB + (rr >> 2);
+    if (t >= T || bh >= BH) return;
+    const size_t row = ((size_t)bh * T + t) * 64;
+    const uint4 a = *reinterpret_cast<const uint4 *>(x + row + 8 * g);
+    const uint4 b = *reinterpret_cast<const uint4 *>(x + row + 32 + 8 * g);
+    const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w};
+    uint32_t ow[4], pw[4];
+    const float *C = cs + tt * 32 + 8 * g;
+    const float *Sn = sn + tt * 32 + 8 * g;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        const float u0 = bf16_lo(aw[w]), u1 = bf16_hi(aw[w]);
+        const float v0 = bf16_lo(bw[w]), v1 = bf16_hi(bw[w]);
+        const float c0 = C[2 * w], c1 = C[2 * w + 1], s0 = Sn[2 * w], s1 = Sn[2 * w + 1];
+        ow[w] = f32_to_bf16(u0 * c0 - v0 * s0) | (f32_to_bf16(u1 * c1 - v1 * s1) << 16);
+        pw[w] = f32_to_bf16(v0 * c0 + u0 * s0) | (f32_to_bf16(v1 * c1 + u1 * s1) << 16);
+    }
+    *reinterpret_cast<uint4 *>(y + row + 8 * g) = make_uint4(ow[0], ow[1], ow[2], ow[3]);
+    *reinterpret_cast<uint4 *>(y + row + 32 + 8 * g) = make_uint4(pw[0], pw[1], pw[2], pw[3]);
+}
+
 hipError_t launch_rope(int dtype, int D, const void *x, void *y, int BH, int T, float rope_base,
                        int transpose, hipStream_t s) {
     dim3 grid((T + kRopeTP - 1) / kRopeTP, (BH + kRopeRB - 1) / kRopeRB);
     const double lb = (double)rope_base;
     timing_before(kRope, s);
-    if (dtype == 0 && D == 32)
+    if (dtype == 1 && D == 64)
+        hipLaunchKernelGGL(rope_bf16_d64_kernel,
+                           dim3((T + kRope64TP - 1) / kRope64TP, (BH + kRope64RB - 1) / kRope64RB),
+                           dim3(256), 0, s, (const uint16_t *)x, (uint16_t *)y, BH, T, lb, transpose);
+    else if (dtype == 0 && D == 32)
         hipLaunchKernelGGL((rope_kernel<float, 32>), grid, dim3(256), 0, s, (const float *)x,
                            (float *)y, BH, T, lb, transpose);
     else if (dtype == 0 && D == 64)
@@ -71,9 +121,6 @@ hipError_t launch_rope(int dtype, int D, const void *x, void *y, int BH, int T, 
                            (float *)y, BH, T, lb, transpose);
     else if (dtype == 1 && D == 32)
         hipLaunchKernelGGL((rope_kernel<uint16_t, 32>), grid, dim3(256), 0, s,
-                           (const uint16_t *)x, (uint16_t *)y, BH, T, lb, transpose);
-    else if (dtype == 1 && D == 64)
-        hipLaunchKernelGGL((rope_kernel<uint16_t, 64>), grid, dim3(256), 0, s,
                            (const uint16_t *)x, (uint16_t *)y, BH, T, lb, transpose);
     else
         return hipErrorInvalidValue;
