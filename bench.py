@@ -3,8 +3,8 @@
 
 One step = one layer of the 60M-model shape (B=8, H=8, T=1024, d_head=64, bf16,
 W=8, Fibonacci base K=15, alpha=1): RoPE of q and k at true positions, the forward
-(o, lse), the backward (dq, dk, dv, dalpha) and R^T carrying dq, dk back to the
-unrotated inputs, all in libfibattn.so's HIP kernels on one stream.  Inputs are
+(o, lse) and the backward (dq, dk, dv, dalpha, with R^T carrying dq, dk back to the
+unrotated inputs), all in libfibattn.so's HIP kernels on one stream.  Inputs are
 seeded N(0,1) tensors resident in HBM; several buffer sets rotate so that the
 256 MB last-level cache cannot hold a step's working set.  Steps are replayed from
 HIP graphs (one captured step per buffer set).
@@ -27,6 +27,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
+ROPE_BASE = 10000.0    # theta_rope of the 60M model (Section 3)
 METRIC = "fwd+bwd queries·heads/s at T=1024 and T=4096; achieved HBM GB/s vs peak"
 
 
@@ -52,7 +53,7 @@ def alg_bytes(kernel: str, D: int, s: int) -> int:
         "forward": 4 * D * s + 4,        # read q, k, v; write o, lse
         "bwd_dq": 6 * D * s + 8,         # read q, k, v, o, dO, lse; write dq, Delta
         "bwd_dkdv": 6 * D * s + 8,       # read q, k, v, dO, lse, Delta; write dk, dv
-        "rope": 2 * D * s,               # read x; write y (per rotated tensor)
+        "rope": 4 * D * s,               # read q, k; write R q, R k (one launch)
         "fwd+bwd": 12 * D * s + 8,       # forward + backward compulsory traffic
     }[kernel]
 
@@ -80,16 +81,15 @@ class Step:
 
     def forward(self):
         F, c = self.F, self.call
-        F.fibattn_rope(self.q, out=self.qr)
-        F.fibattn_rope(self.k, out=self.kr)
+        F.fibattn_rope_qk(self.q, self.k, ROPE_BASE, q_out=self.qr, k_out=self.kr)
         F.fibattn_forward(self.qr, self.kr, self.v, c.W, c.base, c.alpha, o=self.o, lse=self.lse)
 
     def backward(self):
+        # gradients w.r.t. the raw (unrotated) q, k: R^T is applied inside the backward
         F, c = self.F, self.call
         F.fibattn_backward(self.qr, self.kr, self.v, self.o, self.lse, self.dO, c.W, c.base, c.alpha,
-                           dq=self.dq, dk=self.dk, dv=self.dv, dalpha=self.da, workspace=self.ws)
-        F.fibattn_rope(self.dq, transpose=True, out=self.dq)
-        F.fibattn_rope(self.dk, transpose=True, out=self.dk)
+                           dq=self.dq, dk=self.dk, dv=self.dv, dalpha=self.da, workspace=self.ws,
+                           rope_base=ROPE_BASE)
 
     def __call__(self):
         self.forward()
@@ -133,12 +133,15 @@ def timed(run, steps: int, warmup: int):
 
 def kernel_time(F, sets, kernel: str, steps: int, per_step: int):
     """Mean launch duration (ms) of one library kernel over `steps` eager steps, from
-    HIP events the library records around each launch on the launch stream."""
+    HIP events the library records around each launch on the launch stream.  A spin
+    kernel (no memory traffic) ahead of each step keeps the queue non-empty, so that
+    the host's launch latency does not fall between an event pair and its kernel."""
     import torch
 
     torch.cuda.synchronize()
     F.fibattn_timing_begin(kernel, steps * per_step)
     for i in range(steps):
+        torch.cuda._sleep(400_000)
         sets[i % len(sets)]()
     ms, n = F.fibattn_timing_end()
     return ms, n
@@ -242,12 +245,11 @@ def main():
     # per-kernel mean durations (eager steps, library HIP events on the launch stream)
     kt = {}
     for kname in ("forward", "bwd_dq", "bwd_dkdv", "rope"):
-        per = 4 if kname == "rope" else 1
-        kms, n = kernel_time(F, sets, kname, args.steps, per)
+        kms, n = kernel_time(F, sets, kname, args.steps, 1)
         kt[kname] = {"mean_ms": kms, "launches": n}
-    per_step = {k: v["mean_ms"] * (4 if k == "rope" else 1) for k, v in kt.items()}
+    per_step = {k: v["mean_ms"] for k, v in kt.items()}
     dom = max(per_step, key=per_step.get)
-    units = qh  # query-heads per launch (RoPE: rows of one tensor per launch)
+    units = qh  # query-heads per launch
     achieved = alg_bytes(dom, wl.D, s) * units / (kt[dom]["mean_ms"] * 1e-3) / 1e9
     roofline = {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": None,
@@ -269,7 +271,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "T": wl.T, "d_head": wl.D,
                    "W": call.W, "base": call.base_name, "alpha": float(call.alpha),
-                   "step": "rope(q,k) + forward + backward + rope^T(dq,dk)",
+                   "step": "rope(q,k) + forward + backward (dq, dk w.r.t. unrotated q, k)",
                    "launch": "eager" if args.eager else "hip_graph", "buffer_sets": nsets},
         "roofline": roofline,
         "attention_only": {"ms_per_step": ms_attn, "value": qh / (ms_attn * 1e-3),

@@ -105,6 +105,10 @@ size_t fibattn_backward_workspace_bytes(int B, int H, int T, int d_head, int W, 
  *   dalpha : device float32 (overwritten): sum over b, h, i and rung entries of
  *            f_k * dL/dw_k (dw_k/dalpha = f_k); reduced in float64 in fixed order
  *   workspace : device buffer of at least fibattn_backward_workspace_bytes(...)
+ *   rope_base : 0 -> dq, dk are gradients w.r.t. the rotated q, k passed in;
+ *               > 1 -> the inverse rotation R^T at true positions (same pairing and
+ *               angles as fibattn_rope) is applied before the single rounding, so
+ *               dq, dk are gradients w.r.t. the unrotated inputs of the RoPE step.
  * Same limits as the forward.
  */
 fibattn_status_t fibattn_backward(const void *q, const void *k, const void *v,
@@ -112,7 +116,7 @@ fibattn_status_t fibattn_backward(const void *q, const void *k, const void *v,
                                   void *dq, void *dk, void *dv, float *dalpha,
                                   void *workspace, size_t workspace_bytes,
                                   int B, int H, int T, int d_head, int W,
-                                  const int32_t *base, int K, float alpha,
+                                  const int32_t *base, int K, float alpha, float rope_base,
                                   fibattn_dtype_t dtype, hipStream_t stream);
 
 /*
@@ -127,6 +131,14 @@ fibattn_status_t fibattn_backward(const void *q, const void *k, const void *v,
 fibattn_status_t fibattn_rope(const void *x, void *y, int B, int H, int T, int d_head,
                               float rope_base, int transpose,
                               fibattn_dtype_t dtype, hipStream_t stream);
+
+/*
+ * RoPE of q and k in one launch: q_out = R q, k_out = R k (same rotation as
+ * fibattn_rope with transpose = 0; outputs may alias their inputs).
+ */
+fibattn_status_t fibattn_rope_qk(const void *q, const void *k, void *q_out, void *k_out,
+                                 int B, int H, int T, int d_head, float rope_base,
+                                 fibattn_dtype_t dtype, hipStream_t stream);
 
 /* Human-readable name of a status code (static storage). */
 const char *fibattn_status_string(fibattn_status_t status);

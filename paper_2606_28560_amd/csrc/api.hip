@@ -128,7 +128,8 @@ fibattn_status_t fibattn_backward(const void *q, const void *k, const void *v, c
                                   const float *lse, const void *dO, void *dq, void *dk, void *dv,
                                   float *dalpha, void *workspace, size_t workspace_bytes, int B,
                                   int H, int T, int d_head, int W, const int32_t *base, int K,
-                                  float alpha, fibattn_dtype_t dtype, hipStream_t stream) {
+                                  float alpha, float rope_base, fibattn_dtype_t dtype,
+                                  hipStream_t stream) {
     fibattn_status_t st = check_common(B, H, T, d_head, W, K, dtype);
     if (st != FIBATTN_OK) return st;
     if (!q || !k || !v || !o || !lse || !dO || !dq || !dk || !dv || !dalpha)
@@ -136,6 +137,7 @@ fibattn_status_t fibattn_backward(const void *q, const void *k, const void *v, c
     const void *ptrs[] = {q, k, v, o, lse, dO, dq, dk, dv};
     for (const void *p : ptrs)
         if (!aligned16(p)) return FIBATTN_ERR_INVALID_ARG;
+    if (!(rope_base == 0.f || (rope_base > 1.f && isfinite(rope_base)))) return FIBATTN_ERR_INVALID_ARG;
     if (!workspace || !aligned16(workspace) ||
         workspace_bytes < fibattn_backward_workspace_bytes(B, H, T, d_head, W, K))
         return FIBATTN_ERR_WORKSPACE;
@@ -144,8 +146,9 @@ fibattn_status_t fibattn_backward(const void *q, const void *k, const void *v, c
     if (st != FIBATTN_OK) return st;
     float *delta_ws = (float *)workspace;
     double *partials = (double *)((char *)workspace + align256(sizeof(float) * (size_t)B * H * T));
+    const RopeFreq rf = make_rope_freq((double)rope_base, d_head);
     hipError_t e = launch_backward((int)dtype, d_head, q, k, v, o, lse, dO, dq, dk, dv, dalpha,
-                                   delta_ws, partials, B * H, T, W, rt, stream);
+                                   delta_ws, partials, B * H, T, W, rt, rf, rope_base, stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
 }
 
@@ -153,11 +156,27 @@ fibattn_status_t fibattn_rope(const void *x, void *y, int B, int H, int T, int d
                               float rope_base, int transpose, fibattn_dtype_t dtype,
                               hipStream_t stream) {
     if (B < 1 || H < 1 || T < 1 || !x || !y) return FIBATTN_ERR_INVALID_ARG;
+    if (!aligned16(x) || !aligned16(y)) return FIBATTN_ERR_INVALID_ARG;
     if (dtype != FIBATTN_FP32 && dtype != FIBATTN_BF16) return FIBATTN_ERR_INVALID_ARG;
     if (!(rope_base > 1.f) || !isfinite(rope_base)) return FIBATTN_ERR_INVALID_ARG;
     if (d_head != 32 && d_head != 64) return FIBATTN_ERR_UNSUPPORTED;
     if ((long long)B * H > 65535ll * 16) return FIBATTN_ERR_UNSUPPORTED;
-    hipError_t e = launch_rope((int)dtype, d_head, x, y, B * H, T, rope_base, transpose, stream);
+    hipError_t e = launch_rope((int)dtype, d_head, x, y, nullptr, nullptr, B * H, T, rope_base,
+                               transpose, stream);
+    return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
+fibattn_status_t fibattn_rope_qk(const void *q, const void *k, void *q_out, void *k_out, int B, int H,
+                                 int T, int d_head, float rope_base, fibattn_dtype_t dtype,
+                                 hipStream_t stream) {
+    if (B < 1 || H < 1 || T < 1 || !q || !k || !q_out || !k_out) return FIBATTN_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(q_out) || !aligned16(k_out))
+        return FIBATTN_ERR_INVALID_ARG;
+    if (dtype != FIBATTN_FP32 && dtype != FIBATTN_BF16) return FIBATTN_ERR_INVALID_ARG;
+    if (!(rope_base > 1.f) || !isfinite(rope_base)) return FIBATTN_ERR_INVALID_ARG;
+    if (d_head != 32 && d_head != 64) return FIBATTN_ERR_UNSUPPORTED;
+    if ((long long)B * H > 65535ll * 16) return FIBATTN_ERR_UNSUPPORTED;
+    hipError_t e = launch_rope((int)dtype, d_head, q, q_out, k, k_out, B * H, T, rope_base, 0, stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
 }
 

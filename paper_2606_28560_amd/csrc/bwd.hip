@@ -276,13 +276,11 @@ static hipError_t launch_bwd_t(const void *q, const void *k, const void *v, cons
     return hipGetLastError();
 }
 
-hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const void *v,
-                           const void *o, const float *lse, const void *dO, void *dq, void *dk,
-                           void *dv, float *dalpha, float *delta_ws, double *partials, int BH,
-                           int T, int W, const RungTable &rt, hipStream_t s) {
-    if (backward_mfma_supported(dtype, D, W))
-        return launch_backward_mfma(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials, BH,
-                                    T, W, rt, s);
+static hipError_t launch_backward_generic(int dtype, int D, const void *q, const void *k, const void *v,
+                                          const void *o, const float *lse, const void *dO, void *dq,
+                                          void *dk, void *dv, float *dalpha, float *delta_ws,
+                                          double *partials, int BH, int T, int W, const RungTable &rt,
+                                          hipStream_t s) {
 #define FIBATTN_BWD(S_, D_)                                                                  \
     return launch_bwd_t<S_, D_>(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials, \
                                 BH, T, W, rt, s)
@@ -292,6 +290,22 @@ hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const
     if (dtype == 1 && D == 64) FIBATTN_BWD(uint16_t, 64);
 #undef FIBATTN_BWD
     return hipErrorInvalidValue;
+}
+
+
+hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const void *v,
+                           const void *o, const float *lse, const void *dO, void *dq, void *dk,
+                           void *dv, float *dalpha, float *delta_ws, double *partials, int BH,
+                           int T, int W, const RungTable &rt, const RopeFreq &rf, float rope_base,
+                           hipStream_t s) {
+    if (backward_mfma_supported(dtype, D, W))
+        return launch_backward_mfma(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials, BH,
+                                    T, W, rt, rf, s);
+    hipError_t e = launch_backward_generic(dtype, D, q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws,
+                                           partials, BH, T, W, rt, s);
+    // R^T on dq and dk in place: gradients w.r.t. the unrotated q, k
+    if (e == hipSuccess && rf.on) e = launch_rope(dtype, D, dq, dq, dk, dk, BH, T, rope_base, 1, s);
+    return e;
 }
 
 }  // namespace fibattn

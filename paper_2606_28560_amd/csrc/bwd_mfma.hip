@@ -43,8 +43,9 @@ __global__ __launch_bounds__(256) void bwd_dq_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const uint16_t *__restrict__ o, const float *__restrict__ lse, const uint16_t *__restrict__ dO,
     uint16_t *__restrict__ dq, float *__restrict__ delta_out, double *__restrict__ partials, int T,
-    int W, RungTable rt, float tau, int tiles) {
+    int W, RungTable rt, RopeFreq rf, float tau, int tiles) {
     __shared__ __align__(16) uint16_t kr[kStage * kRowStride];
+    __shared__ double sfreq[32];
     __shared__ __align__(16) uint16_t vr[kStage * kRowStride];
     __shared__ __align__(16) uint16_t kt[kD * kTStride];
     __shared__ double red[4];
@@ -76,9 +77,25 @@ __global__ __launch_bounds__(256) void bwd_dq_bf16_d64_kernel(
     const float lse2 = L[ic] * kLog2e;
     const float lse2_m = L[imc] * kLog2e;
 
+    const int last = t0 + 15;
+    int nact = 0;
+#pragma unroll
+    for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && rt.d0[r] <= last) ? 1 : 0;
+    auto load_rung = [&](int r, Slice *x) {
+        const int R0 = min(max(i - rt.d0[r], 0), T - 1);
+        const int R1 = max(R0 - 1, 0);
+        x[0] = load_row(K, R0, gq);
+        x[1] = load_row(V, R0, gq);
+        x[2] = load_row(K, R1, gq);
+        x[3] = load_row(V, R1, gq);
+    };
+    Slice xA[4], xB[4];
+    if (0 < nact) load_rung(0, xA);  // in flight during the band phase
+
     stage_rows(kr, kRowStride, K, T0 - 16, kStage, T);
     stage_rows(vr, kRowStride, V, T0 - 16, kStage, T);
     stage_transpose(kt, kTStride, K, T0 - 16, kStage, T);
+    stage_freq(sfreq, rf);
     __syncthreads();
 
     // band (MFMA layout): keys [t0-16, t0+16)
@@ -106,49 +123,40 @@ __global__ __launch_bounds__(256) void bwd_dq_bf16_d64_kernel(
         acc.c[c] = mfma(staged_operand(kt, c, nm, 16 * wv, gm), C, f32x4{0.f, 0.f, 0.f, 0.f});
     acc_to_quad(acc, lane);
 
-    // rungs (quad layout), two at a time: the four rows of each (k, v at r0 and r1)
-    // of a batch are loaded together; r1 = -1 is the zero row
+    // rungs (quad layout), one per batch with two batches in flight: the four rows
+    // (k, v at r0 and r1) of a rung are loaded together; r1 = -1 is the zero row
     double dal = 0.0;
-    const int last = t0 + 15;
-    int nact = 0;
-#pragma unroll
-    for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && rt.d0[r] <= last) ? 1 : 0;
+    auto compute_rung = [&](int r, const Slice *x) {  // x = {k0, v0, k1, v1}
+        const int d0 = rt.d0[r];
+        const float w = rt.w[r];
+        const bool incl = r < nact && i < T && (d0 < i || (d0 == i && w == 0.f));
+        const bool has1 = i - d0 - 1 >= 0;  // row r1 exists (else the zero row)
+        const float s0 = quad_sum(dot_slice(qq, x[0]));
+        const float s1r = quad_sum(dot_slice(qq, x[2]));
+        const float p0 = quad_sum(dot_slice(gqq, x[1]));
+        const float p1r = quad_sum(dot_slice(gqq, x[3]));
+        const float s1 = has1 ? s1r : 0.f;
+        const float p1 = has1 ? p1r : 0.f;
+        const float sc = (1.f - w) * s0 + w * s1;
+        const float dP = (1.f - w) * p0 + w * p1;
+        const float p = incl ? fast_exp2(sc * sl2 - lse2) : 0.f;
+        const float cc = tau * p * (dP - delta);
+        acc_axpy2(acc, cc * (1.f - w), x[0], cc * w, x[2]);
+        if (gq == 0 && incl) dal += (double)rt.f[r] * (double)(cc * (s1 - s0) + p * (p1 - p0));
+    };
 #pragma unroll
     for (int rb = 0; rb < kMaxRungs; rb += 2) {
         if (rb < nact) {
-            Slice k0[2], v0[2], k1[2], v1[2];
-#pragma unroll
-            for (int x = 0; x < 2; ++x) {
-                const int R0 = min(max(i - rt.d0[rb + x], 0), T - 1);
-                const int R1 = max(R0 - 1, 0);
-                k0[x] = load_row(K, R0, gq);
-                v0[x] = load_row(V, R0, gq);
-                k1[x] = load_row(K, R1, gq);
-                v1[x] = load_row(V, R1, gq);
-            }
-#pragma unroll
-            for (int x = 0; x < 2; ++x) {
-                const int r = rb + x;
-                const int d0 = rt.d0[r];
-                const float w = rt.w[r];
-                const bool incl = r < nact && i < T && (d0 < i || (d0 == i && w == 0.f));
-                const bool has1 = i - d0 - 1 >= 0;  // row r1 exists (else the zero row)
-                const float s0 = quad_sum(dot_slice(qq, k0[x]));
-                const float s1r = quad_sum(dot_slice(qq, k1[x]));
-                const float p0 = quad_sum(dot_slice(gqq, v0[x]));
-                const float p1r = quad_sum(dot_slice(gqq, v1[x]));
-                const float s1 = has1 ? s1r : 0.f;
-                const float p1 = has1 ? p1r : 0.f;
-                const float s = (1.f - w) * s0 + w * s1;
-                const float dP = (1.f - w) * p0 + w * p1;
-                const float p = incl ? fast_exp2(s * sl2 - lse2) : 0.f;
-                const float cc = tau * p * (dP - delta);
-                acc_axpy2(acc, cc * (1.f - w), k0[x], cc * w, k1[x]);
-                if (gq == 0 && incl) dal += (double)rt.f[r] * (double)(cc * (s1 - s0) + p * (p1 - p0));
+            if (rb + 1 < nact) load_rung(rb + 1, xB);
+            compute_rung(rb, xA);
+            if (rb + 1 < nact) {
+                if (rb + 2 < nact) load_rung(rb + 2, xA);
+                compute_rung(rb + 1, xB);
             }
         }
     }
 
+    if (rf.on) acc_rope_t(acc, i, sfreq + 8 * gq);  // gradient w.r.t. the unrotated q
     if (i < T) {
         store_acc(dq + off + (size_t)i * kD, gq, acc, 1.f);
         if (gq == 0) delta_out[(size_t)bh * T + i] = delta;
@@ -167,8 +175,10 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const float *__restrict__ lse, const uint16_t *__restrict__ dO, const float *__restrict__ delta_in,
     uint16_t *__restrict__ dk, uint16_t *__restrict__ dv, const double *__restrict__ partials,
-    int n_partials, float *__restrict__ dalpha, int T, int W, RungTable rt, float tau, int tiles) {
+    int n_partials, float *__restrict__ dalpha, int T, int W, RungTable rt, RopeFreq rf, float tau,
+    int tiles) {
     __shared__ __align__(16) uint16_t qr[kStage * kRowStride];
+    __shared__ double sfreq[32];
     __shared__ __align__(16) uint16_t gr[kStage * kRowStride];
     __shared__ __align__(16) uint16_t qt[kD * kTStride];
     __shared__ __align__(16) uint16_t gt[kD * kTStride];
@@ -212,6 +222,33 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_d64_kernel(
     const Slice ks = load_row(K, jc, gq);
     const Slice vs = load_row(V, jc, gq);
 
+    // rungs: some key of this wave has j + floor(d) < T for a prefix of the table
+    int nact = 0;
+#pragma unroll
+    for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && t0 + rt.d0[r] < T) ? 1 : 0;
+    // rows of query i0 = j + d0 (and i0 + 1 when interpolating) for a rung
+    auto load_rung = [&](int r, Slice *x) {
+        const int i0c = min(j + rt.d0[r], T - 1);
+        const int i1c = min(j + rt.d0[r] + 1, T - 1);
+        x[0] = load_row(Q, i0c, gq);
+        x[1] = load_row(G, i0c, gq);
+        x[2] = load_row(Q, i1c, gq);
+        x[3] = load_row(G, i1c, gq);
+    };
+    auto load_pair = [&](int rb, Slice *x) {
+        const int ia = min(j + rt.d0[rb], T - 1);
+        const int ib = min(j + rt.d0[rb + 1], T - 1);
+        x[0] = load_row(Q, ia, gq);
+        x[1] = load_row(G, ia, gq);
+        x[2] = load_row(Q, ib, gq);
+        x[3] = load_row(G, ib, gq);
+    };
+    Slice xA[4], xB[4];
+    if (0 < nact) {  // in flight during the band phase
+        if (INTERP) load_rung(0, xA);
+        else load_pair(0, xA);
+    }
+
     // stage q, dO rows (row-major and transposed), lse, Delta for queries [T0, T0+80)
     stage_rows(qr, kRowStride, Q, T0, kStage, T);
     stage_rows(gr, kRowStride, G, T0, kStage, T);
@@ -222,6 +259,7 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_d64_kernel(
         sl[c] = row < T ? L[row] * kLog2e : 0.f;
         sd[c] = row < T ? Dl[row] : 0.f;
     }
+    stage_freq(sfreq, rf);
     __syncthreads();
 
     // band (MFMA layout): queries [t0, t0 + 32) in two blocks
@@ -256,37 +294,33 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_d64_kernel(
     acc_to_quad(adk, lane);
     acc_to_quad(adv, lane);
 
-    // rungs (quad layout): some key of this wave has j + floor(d) < T for a prefix
-    int nact = 0;
-#pragma unroll
-    for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && t0 + rt.d0[r] < T) ? 1 : 0;
     if (!INTERP) {
-        // every w == 0: query j + d0 reads this row with weight 1; four rungs per batch
+        // every w == 0: query j + d0 reads this row with weight 1; two rungs per batch,
+        // two batches in flight
+        auto compute_pair = [&](int rb, const Slice *x) {  // x = {q0a, g0a, q0b, g0b}
+            float cc[2], pp[2];
+#pragma unroll
+            for (int y = 0; y < 2; ++y) {
+                const int i0 = j + rt.d0[rb + y];
+                const int i0c = min(i0, T - 1);
+                const bool in0 = rb + y < nact && j < T && i0 < T;
+                const float sc = quad_sum(dot_slice(x[2 * y], ks));
+                const float dp = quad_sum(dot_slice(x[2 * y + 1], vs));
+                pp[y] = in0 ? fast_exp2(sc * sl2 - L[i0c] * kLog2e) : 0.f;
+                cc[y] = tau * pp[y] * (dp - Dl[i0c]);
+            }
+            acc_axpy2(adk, cc[0], x[0], cc[1], x[2]);
+            acc_axpy2(adv, pp[0], x[1], pp[1], x[3]);
+        };
 #pragma unroll
         for (int rb = 0; rb < kMaxRungs; rb += 4) {
             if (rb < nact) {
-                Slice q0[4], g0[4];
-                int icq[4];
-#pragma unroll
-                for (int x = 0; x < 4; ++x) {
-                    icq[x] = min(j + rt.d0[rb + x], T - 1);
-                    q0[x] = load_row(Q, icq[x], gq);
-                    g0[x] = load_row(G, icq[x], gq);
+                if (rb + 2 < nact) load_pair(rb + 2, xB);
+                compute_pair(rb, xA);
+                if (rb + 2 < nact) {
+                    if (rb + 4 < nact) load_pair(rb + 4, xA);
+                    compute_pair(rb + 2, xB);
                 }
-                float cc[4], pp[4];
-#pragma unroll
-                for (int x = 0; x < 4; ++x) {
-                    const int i0 = j + rt.d0[rb + x];
-                    const bool in0 = rb + x < nact && j < T && i0 < T;
-                    const float s = quad_sum(dot_slice(q0[x], ks));
-                    const float dp = quad_sum(dot_slice(g0[x], vs));
-                    pp[x] = in0 ? fast_exp2(s * sl2 - L[icq[x]] * kLog2e) : 0.f;
-                    cc[x] = tau * pp[x] * (dp - Dl[icq[x]]);
-                }
-                acc_axpy2(adk, cc[0], q0[0], cc[1], q0[1]);
-                acc_axpy2(adk, cc[2], q0[2], cc[3], q0[3]);
-                acc_axpy2(adv, pp[0], g0[0], pp[1], g0[1]);
-                acc_axpy2(adv, pp[2], g0[2], pp[3], g0[3]);
             }
         }
     } else {
@@ -297,46 +331,41 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_d64_kernel(
         const Slice vmn = load_row(V, jmn, gq);
         const Slice kpn = load_row(K, jpn, gq);
         const Slice vpn = load_row(V, jpn, gq);
+        auto compute_rung = [&](int r, const Slice *x) {  // x = {q0, g0, q1, g1}
+            const float w = rt.w[r];
+            // query i0 = j + d0 reads this row as r0 (weight 1 - w) and j-1 as r1
+            const int i0 = j + rt.d0[r];
+            const bool in0 = r < nact && j < T && i0 < T && (w == 0.f || j >= 1);
+            const int i0c = min(i0, T - 1);
+            const float sa = quad_sum((1.f - w) * dot_slice(x[0], ks) + w * dot_slice(x[0], kmn));
+            const float da = quad_sum((1.f - w) * dot_slice(x[1], vs) + w * dot_slice(x[1], vmn));
+            const float pa = in0 ? fast_exp2(sa * sl2 - L[i0c] * kLog2e) : 0.f;
+            const float ca = tau * pa * (da - Dl[i0c]);
+            // query i1 = i0 + 1 reads row j+1 as r0 and this row as r1 (weight w)
+            const int i1 = i0 + 1;
+            const bool in1 = r < nact && j < T && i1 < T && w != 0.f;
+            const int i1c = min(i1, T - 1);
+            const float sb = quad_sum((1.f - w) * dot_slice(x[2], kpn) + w * dot_slice(x[2], ks));
+            const float db = quad_sum((1.f - w) * dot_slice(x[3], vpn) + w * dot_slice(x[3], vs));
+            const float pb = in1 ? fast_exp2(sb * sl2 - L[i1c] * kLog2e) : 0.f;
+            const float cb = tau * pb * (db - Dl[i1c]);
+            acc_axpy2(adk, (1.f - w) * ca, x[0], w * cb, x[2]);
+            acc_axpy2(adv, (1.f - w) * pa, x[1], w * pb, x[3]);
+        };
 #pragma unroll
         for (int rb = 0; rb < kMaxRungs; rb += 2) {
             if (rb < nact) {
-                Slice q0[2], g0[2], q1[2], g1[2];
-#pragma unroll
-                for (int x = 0; x < 2; ++x) {
-                    const int i0c = min(j + rt.d0[rb + x], T - 1);
-                    const int i1c = min(j + rt.d0[rb + x] + 1, T - 1);
-                    q0[x] = load_row(Q, i0c, gq);
-                    g0[x] = load_row(G, i0c, gq);
-                    q1[x] = load_row(Q, i1c, gq);
-                    g1[x] = load_row(G, i1c, gq);
-                }
-#pragma unroll
-                for (int x = 0; x < 2; ++x) {
-                    const int r = rb + x;
-                    const float w = rt.w[r];
-                    // query i0 = j + d0 reads this row as r0 (weight 1 - w) and j-1 as r1
-                    const int i0 = j + rt.d0[r];
-                    const bool in0 = r < nact && j < T && i0 < T && (w == 0.f || j >= 1);
-                    const int i0c = min(i0, T - 1);
-                    const float sa = quad_sum((1.f - w) * dot_slice(q0[x], ks) + w * dot_slice(q0[x], kmn));
-                    const float da = quad_sum((1.f - w) * dot_slice(g0[x], vs) + w * dot_slice(g0[x], vmn));
-                    const float pa = in0 ? fast_exp2(sa * sl2 - L[i0c] * kLog2e) : 0.f;
-                    const float ca = tau * pa * (da - Dl[i0c]);
-                    // query i1 = i0 + 1 reads row j+1 as r0 and this row as r1 (weight w)
-                    const int i1 = i0 + 1;
-                    const bool in1 = r < nact && j < T && i1 < T && w != 0.f;
-                    const int i1c = min(i1, T - 1);
-                    const float sb = quad_sum((1.f - w) * dot_slice(q1[x], kpn) + w * dot_slice(q1[x], ks));
-                    const float db = quad_sum((1.f - w) * dot_slice(g1[x], vpn) + w * dot_slice(g1[x], vs));
-                    const float pb = in1 ? fast_exp2(sb * sl2 - L[i1c] * kLog2e) : 0.f;
-                    const float cb = tau * pb * (db - Dl[i1c]);
-                    acc_axpy2(adk, (1.f - w) * ca, q0[x], w * cb, q1[x]);
-                    acc_axpy2(adv, (1.f - w) * pa, g0[x], w * pb, g1[x]);
+                if (rb + 1 < nact) load_rung(rb + 1, xB);
+                compute_rung(rb, xA);
+                if (rb + 1 < nact) {
+                    if (rb + 2 < nact) load_rung(rb + 2, xA);
+                    compute_rung(rb + 1, xB);
                 }
             }
         }
     }
 
+    if (rf.on) acc_rope_t(adk, j, sfreq + 8 * gq);  // gradient w.r.t. the unrotated k
     if (j < T) {
         store_acc(dk + off + (size_t)j * kD, gq, adk, 1.f);
         store_acc(dv + off + (size_t)j * kD, gq, adv, 1.f);
@@ -350,14 +379,15 @@ size_t bwd_mfma_num_partials(int BH, int T) { return (size_t)((T + kBwdB - 1) / 
 hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, const void *o,
                                 const float *lse, const void *dO, void *dq, void *dk, void *dv,
                                 float *dalpha, float *delta_ws, double *partials, int BH, int T,
-                                int W, const RungTable &rt, hipStream_t s) {
+                                int W, const RungTable &rt, const RopeFreq &rf, hipStream_t s) {
     const int tiles = (T + kBwdB - 1) / kBwdB;
     const float tau = 1.f / sqrtf(64.f);
     const int nb = tiles * BH;
     timing_before(kBwdDq, s);
     hipLaunchKernelGGL(bwd_dq_bf16_d64_kernel, dim3(nb), dim3(256), 0, s, (const uint16_t *)q,
                        (const uint16_t *)k, (const uint16_t *)v, (const uint16_t *)o, lse,
-                       (const uint16_t *)dO, (uint16_t *)dq, delta_ws, partials, T, W, rt, tau, tiles);
+                       (const uint16_t *)dO, (uint16_t *)dq, delta_ws, partials, T, W, rt, rf, tau,
+                       tiles);
     timing_after(kBwdDq, s);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -368,12 +398,12 @@ hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, con
         hipLaunchKernelGGL(bwd_dkdv_bf16_d64_kernel<true>, dim3(nb), dim3(256), 0, s,
                            (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v, lse,
                            (const uint16_t *)dO, delta_ws, (uint16_t *)dk, (uint16_t *)dv, partials,
-                           nb, dalpha, T, W, rt, tau, tiles);
+                           nb, dalpha, T, W, rt, rf, tau, tiles);
     else
         hipLaunchKernelGGL(bwd_dkdv_bf16_d64_kernel<false>, dim3(nb), dim3(256), 0, s,
                            (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v, lse,
                            (const uint16_t *)dO, delta_ws, (uint16_t *)dk, (uint16_t *)dv, partials,
-                           nb, dalpha, T, W, rt, tau, tiles);
+                           nb, dalpha, T, W, rt, rf, tau, tiles);
     timing_after(kBwdDkDv, s);
     return hipGetLastError();
 }

@@ -19,6 +19,22 @@ struct RungTable {
     int f[kMaxRungs];
 };
 
+// RoPE inverse frequencies base^(-2j/D) for j < D/2 <= 32, evaluated in float64 on
+// the host; `on` = 0 when no rotation is requested.
+struct RopeFreq {
+    double inv[32];
+    int on;
+};
+
+// cos/sin of t * inv_freq: the angle and its reduction to [-pi, pi] are float64, the
+// reduced angle is evaluated with float32 sincosf (error ~1e-7 absolute).
+__device__ __forceinline__ void rope_cs(int t, double inv_freq, float &c, float &s) {
+    const double a = (double)t * inv_freq;
+    const double two_pi = 6.283185307179586476925286766559;
+    const double r = a - two_pi * rint(a * (1.0 / two_pi));
+    sincosf((float)r, &s, &c);
+}
+
 // ---- storage types -------------------------------------------------------
 // A lane moves 16 bytes of a row at a time: 4 float32 or 8 bfloat16 values.
 __device__ __forceinline__ float bf16_lo(uint32_t x) { return __uint_as_float(x << 16); }

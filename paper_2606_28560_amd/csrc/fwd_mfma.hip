@@ -30,7 +30,8 @@ __global__ __launch_bounds__(256) void fwd_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     uint16_t *__restrict__ o, float *__restrict__ lse, int T, int W, RungTable rt, float sl2,
     int tiles) {
-    constexpr int kFwdRB = INTERP ? 2 : 4;  // rungs per load batch (register budget)
+    constexpr int RB = INTERP ? 1 : 2;  // rungs per load batch; two batches in flight
+    constexpr int NS = INTERP ? 2 : 1;  // rows per rung (r0, and r1 when interpolating)
     __shared__ __align__(16) uint16_t kr[kBandRows * kRowStride];
     __shared__ __align__(16) uint16_t vt[kD * kVtStride];
 
@@ -57,6 +58,22 @@ __global__ __launch_bounds__(256) void fwd_bf16_d64_kernel(
     const int i = t0 + nq;   // ... in the quad layout
     const Slice qm = load_row(Q, min(im, T - 1), gm);
     const Slice qq = load_row(Q, min(i, T - 1), gq);
+
+    // rung rows of a batch: kx[x*NS + s], vx[x*NS + s] = row r_s of rung rb + x
+    auto load_batch = [&](int rb, Slice *kx, Slice *vx) {
+#pragma unroll
+        for (int x = 0; x < RB; ++x) {
+            const int R0 = min(max(i - rt.d0[rb + x], 0), T - 1);
+#pragma unroll
+            for (int sidx = 0; sidx < NS; ++sidx) {
+                const int R = max(R0 - sidx, 0);
+                kx[x * NS + sidx] = load_row(K, R, gq);
+                vx[x * NS + sidx] = load_row(V, R, gq);
+            }
+        }
+    };
+    Slice kA[RB * NS], vA[RB * NS], kB[RB * NS], vB[RB * NS];
+    if (0 < nact) load_batch(0, kA, vA);  // in flight during the band phase
 
     // band rows [T0-16, T0+64): K row-major, V transposed (zero outside [0, T))
     stage_rows(kr, kRowStride, K, T0 - 16, kBandRows, T);
@@ -108,57 +125,50 @@ __global__ __launch_bounds__(256) void fwd_bf16_d64_kernel(
     m = to_quad(m, lane);
     l = to_quad(l, lane);
 
-    // ---- rungs (quad layout), kFwdRB at a time: all rows of a batch are loaded
-    // together, then the running maximum, sum and weighted values are updated ----
+    // ---- rungs (quad layout): logits of a batch, running maximum, rescale, values ----
+    auto compute_batch = [&](int rb, const Slice *kx, const Slice *vx) {
+        float s[RB];
+        float mb = m;
 #pragma unroll
-    for (int rb = 0; rb < kMaxRungs; rb += kFwdRB) {
+        for (int x = 0; x < RB; ++x) {
+            const int r = rb + x;
+            const int d0 = rt.d0[r];
+            const float w = rt.w[r];
+            const bool incl = r < nact && (d0 < i || (d0 == i && w == 0.f));
+            float part = dot_slice(qq, kx[x * NS]);
+            if (INTERP) part = (1.f - w) * part + w * dot_slice(qq, kx[x * NS + 1]);
+            part = quad_sum(part) * sl2;
+            s[x] = incl ? part : -INFINITY;
+            mb = fmaxf(mb, s[x]);
+        }
+        const float scale = fast_exp2(m - mb);
+        m = mb;
+        l *= scale;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc.c[c] *= scale;
+        float p[RB];
+#pragma unroll
+        for (int x = 0; x < RB; ++x) {
+            p[x] = fast_exp2(s[x] - m);
+            l += p[x];
+        }
+        if (INTERP) {
+            const float w = rt.w[rb];
+            acc_axpy2(acc, p[0] * (1.f - w), vx[0], p[0] * w, vx[1]);
+        } else {
+            acc_axpy2(acc, p[0], vx[0], p[1], vx[1]);
+        }
+    };
+
+    // two batches in flight: load the next while computing the current
+#pragma unroll
+    for (int rb = 0; rb < kMaxRungs; rb += 2 * RB) {
         if (rb < nact) {
-            Slice k0[kFwdRB], v0[kFwdRB], k1[kFwdRB], v1[kFwdRB];
-#pragma unroll
-            for (int x = 0; x < kFwdRB; ++x) {
-                const int R0 = min(max(i - rt.d0[rb + x], 0), T - 1);
-                k0[x] = load_row(K, R0, gq);
-                v0[x] = load_row(V, R0, gq);
-                if (INTERP) {
-                    const int R1 = max(R0 - 1, 0);
-                    k1[x] = load_row(K, R1, gq);
-                    v1[x] = load_row(V, R1, gq);
-                }
-            }
-            float s[kFwdRB];
-            float mb = m;
-#pragma unroll
-            for (int x = 0; x < kFwdRB; ++x) {
-                const int r = rb + x;
-                const int d0 = rt.d0[r];
-                const float w = rt.w[r];
-                const bool incl = r < nact && (d0 < i || (d0 == i && w == 0.f));
-                float part = dot_slice(qq, k0[x]);
-                if (INTERP) part = (1.f - w) * part + w * dot_slice(qq, k1[x]);
-                part = quad_sum(part) * sl2;
-                s[x] = incl ? part : -INFINITY;
-                mb = fmaxf(mb, s[x]);
-            }
-            const float scale = fast_exp2(m - mb);
-            m = mb;
-            l *= scale;
-#pragma unroll
-            for (int c = 0; c < 4; ++c) acc.c[c] *= scale;
-            float p[kFwdRB];
-#pragma unroll
-            for (int x = 0; x < kFwdRB; ++x) {
-                p[x] = fast_exp2(s[x] - m);
-                l += p[x];
-            }
-            if (INTERP) {
-#pragma unroll
-                for (int x = 0; x < kFwdRB; ++x) {
-                    const float w = rt.w[rb + x];
-                    acc_axpy2(acc, p[x] * (1.f - w), v0[x], p[x] * w, v1[x]);
-                }
-            } else {
-#pragma unroll
-                for (int x = 0; x < kFwdRB; x += 2) acc_axpy2(acc, p[x], v0[x], p[x + 1], v0[x + 1]);
+            if (rb + RB < nact) load_batch(rb + RB, kB, vB);
+            compute_batch(rb, kA, vA);
+            if (rb + RB < nact) {
+                if (rb + 2 * RB < nact) load_batch(rb + 2 * RB, kA, vA);
+                compute_batch(rb + RB, kB, vB);
             }
         }
     }

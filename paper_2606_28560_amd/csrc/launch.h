@@ -24,7 +24,8 @@ size_t bwd_num_partials(int dtype, int D, int BH, int T);
 hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const void *v,
                            const void *o, const float *lse, const void *dO, void *dq, void *dk,
                            void *dv, float *dalpha, float *delta_ws, double *partials, int BH,
-                           int T, int W, const RungTable &rt, hipStream_t s);
+                           int T, int W, const RungTable &rt, const RopeFreq &rf, float rope_base,
+                           hipStream_t s);
 
 // bfloat16, d_head = 64, W <= 16: matrix-core band + VALU rungs (fwd_mfma.hip, bwd_mfma.hip).
 bool forward_mfma_supported(int dtype, int D, int W);
@@ -35,9 +36,12 @@ size_t bwd_mfma_num_partials(int BH, int T);
 hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, const void *o,
                                 const float *lse, const void *dO, void *dq, void *dk, void *dv,
                                 float *dalpha, float *delta_ws, double *partials, int BH, int T,
-                                int W, const RungTable &rt, hipStream_t s);
+                                int W, const RungTable &rt, const RopeFreq &rf, hipStream_t s);
 
-hipError_t launch_rope(int dtype, int D, const void *x, void *y, int BH, int T, float rope_base,
-                       int transpose, hipStream_t s);
+RopeFreq make_rope_freq(double rope_base, int D);  // on = 0 when rope_base <= 0
+
+// RoPE of one tensor (x1 == nullptr) or of two same-shaped tensors in one launch.
+hipError_t launch_rope(int dtype, int D, const void *x0, void *y0, const void *x1, void *y1, int BH,
+                       int T, float rope_base, int transpose, hipStream_t s);
 
 }  // namespace fibattn

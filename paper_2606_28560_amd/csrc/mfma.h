@@ -158,6 +158,29 @@ __device__ __forceinline__ void store_acc(uint16_t *row, int g, const Acc16 &acc
     *reinterpret_cast<uint4 *>(row + 32 + 8 * g) = b;
 }
 
+// R^T (the inverse RoPE rotation) at position t on the lane's slice: slice positions
+// d and d + 8 hold the rotate-half pair (8g + d, 32 + 8g + d); inv8 points at the
+// eight inverse frequencies of lane group g.
+__device__ __forceinline__ void acc_rope_t(Acc16 &a, int t, const double *inv8) {
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+        float c, s;
+        rope_cs(t, inv8[d], c, s);
+        const float x = a.c[d >> 2][d & 3];
+        const float y = a.c[2 + (d >> 2)][d & 3];
+        a.c[d >> 2][d & 3] = x * c + y * s;
+        a.c[2 + (d >> 2)][d & 3] = y * c - x * s;
+    }
+}
+
+// Stage the RoPE inverse frequencies in LDS (read by acc_rope_t after a barrier).
+__device__ __forceinline__ void stage_freq(double *dst, const RopeFreq &rf) {
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int j = 0; j < 32; ++j) dst[j] = rf.inv[j];
+    }
+}
+
 // Moves a value from the MFMA layout (row n on lanes n + 16g) to the quad layout
 // (row n on lanes 4n + g): lane 4n + g takes the value of lane n + 16g.
 __device__ __forceinline__ float to_quad(float x, int lane) {

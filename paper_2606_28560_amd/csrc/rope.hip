@@ -61,33 +61,36 @@ __global__ __launch_bounds__(256) void rope_kernel(const S *x, S *y, int BH, int
 // bfloat16, d_head 64: a workgroup owns 4 positions of 16 (b, h) rows (64 rows).
 // Lane group g of a row's four lanes holds dims [8g, 8g+8) and [32+8g, 32+8g+8),
 // i.e. the eight rotate-half pairs (j, j+32), j in [8g, 8g+8): two 16-byte loads
-// and stores per lane, reading 64 contiguous bytes per row per instruction.
+// and stores per lane, reading 64 contiguous bytes per row per instruction.  The
+// loads are issued before the angles are evaluated.
 constexpr int kRope64TP = 4;
 constexpr int kRope64RB = 16;
 
-__global__ __launch_bounds__(256) void rope_bf16_d64_kernel(const uint16_t *x, uint16_t *y, int BH,
-                                                            int T, double rope_base, int transpose) {
+// blockIdx.z selects the tensor: (x0 -> y0) or (x1 -> y1).
+__global__ __launch_bounds__(256) void rope_bf16_d64_kernel(const uint16_t *x0, uint16_t *y0,
+                                                            const uint16_t *x1, uint16_t *y1, int BH,
+                                                            int T, RopeFreq rf, int transpose) {
     __shared__ float cs[kRope64TP * 32], sn[kRope64TP * 32];
+    const uint16_t *x = blockIdx.z ? x1 : x0;
+    uint16_t *y = blockIdx.z ? y1 : y0;
     const int t0 = blockIdx.x * kRope64TP;
-    if (threadIdx.x < kRope64TP * 32) {
-        const int t = t0 + (threadIdx.x >> 5);
-        const int jj = threadIdx.x & 31;
-        const double ang = (double)t * pow(rope_base, -2.0 * (double)jj / 64.0);
-        double sv, cv;
-        sincos(ang, &sv, &cv);
-        cs[threadIdx.x] = (float)cv;
-        sn[threadIdx.x] = transpose ? -(float)sv : (float)sv;
-    }
-    __syncthreads();
     const int g = threadIdx.x & 3;
-    const int rr = threadIdx.x >> 2;          // 0..63
+    const int rr = threadIdx.x >> 2;  // 0..63
     const int tt = rr & (kRope64TP - 1);
     const int t = t0 + tt;
     const int bh = blockIdx.y * kRope64RB + (rr >> 2);
-    if (t >= T || bh >= BH) return;
-    const size_t row = ((size_t)bh * T + t) * 64;
+    const bool live = t < T && bh < BH;
+    const size_t row = ((size_t)min(bh, BH - 1) * T + min(t, T - 1)) * 64;
     const uint4 a = *reinterpret_cast<const uint4 *>(x + row + 8 * g);
     const uint4 b = *reinterpret_cast<const uint4 *>(x + row + 32 + 8 * g);
+    if (threadIdx.x < kRope64TP * 32) {
+        float c, sv;
+        rope_cs(t0 + (threadIdx.x >> 5), rf.inv[threadIdx.x & 31], c, sv);
+        cs[threadIdx.x] = c;
+        sn[threadIdx.x] = transpose ? -sv : sv;
+    }
+    __syncthreads();
+    if (!live) return;
     const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w};
     uint32_t ow[4], pw[4];
     const float *C = cs + tt * 32 + 8 * g;
@@ -104,16 +107,17 @@ __global__ __launch_bounds__(256) void rope_bf16_d64_kernel(const uint16_t *x, u
     *reinterpret_cast<uint4 *>(y + row + 32 + 8 * g) = make_uint4(pw[0], pw[1], pw[2], pw[3]);
 }
 
-hipError_t launch_rope(int dtype, int D, const void *x, void *y, int BH, int T, float rope_base,
-                       int transpose, hipStream_t s) {
+RopeFreq make_rope_freq(double rope_base, int D) {
+    RopeFreq rf;
+    rf.on = rope_base > 0.0;
+    for (int j = 0; j < 32; ++j) rf.inv[j] = (j < D / 2 && rf.on) ? pow(rope_base, -2.0 * (double)j / (double)D) : 0.0;
+    return rf;
+}
+
+static hipError_t launch_rope_generic(int dtype, int D, const void *x, void *y, int BH, int T,
+                                      double lb, int transpose, hipStream_t s) {
     dim3 grid((T + kRopeTP - 1) / kRopeTP, (BH + kRopeRB - 1) / kRopeRB);
-    const double lb = (double)rope_base;
-    timing_before(kRope, s);
-    if (dtype == 1 && D == 64)
-        hipLaunchKernelGGL(rope_bf16_d64_kernel,
-                           dim3((T + kRope64TP - 1) / kRope64TP, (BH + kRope64RB - 1) / kRope64RB),
-                           dim3(256), 0, s, (const uint16_t *)x, (uint16_t *)y, BH, T, lb, transpose);
-    else if (dtype == 0 && D == 32)
+    if (dtype == 0 && D == 32)
         hipLaunchKernelGGL((rope_kernel<float, 32>), grid, dim3(256), 0, s, (const float *)x,
                            (float *)y, BH, T, lb, transpose);
     else if (dtype == 0 && D == 64)
@@ -122,10 +126,34 @@ hipError_t launch_rope(int dtype, int D, const void *x, void *y, int BH, int T, 
     else if (dtype == 1 && D == 32)
         hipLaunchKernelGGL((rope_kernel<uint16_t, 32>), grid, dim3(256), 0, s,
                            (const uint16_t *)x, (uint16_t *)y, BH, T, lb, transpose);
+    else if (dtype == 1 && D == 64)
+        hipLaunchKernelGGL((rope_kernel<uint16_t, 64>), grid, dim3(256), 0, s,
+                           (const uint16_t *)x, (uint16_t *)y, BH, T, lb, transpose);
     else
         return hipErrorInvalidValue;
-    timing_after(kRope, s);
     return hipGetLastError();
+}
+
+// One launch for one tensor (x1 == nullptr) or two tensors of the same shape.
+hipError_t launch_rope(int dtype, int D, const void *x0, void *y0, const void *x1, void *y1, int BH,
+                       int T, float rope_base, int transpose, hipStream_t s) {
+    const double lb = (double)rope_base;
+    timing_before(kRope, s);
+    hipError_t e = hipSuccess;
+    if (dtype == 1 && D == 64) {
+        const RopeFreq rf = make_rope_freq(lb, 64);
+        hipLaunchKernelGGL(rope_bf16_d64_kernel,
+                           dim3((T + kRope64TP - 1) / kRope64TP, (BH + kRope64RB - 1) / kRope64RB,
+                                x1 ? 2 : 1),
+                           dim3(256), 0, s, (const uint16_t *)x0, (uint16_t *)y0,
+                           (const uint16_t *)x1, (uint16_t *)y1, BH, T, rf, transpose);
+        e = hipGetLastError();
+    } else {
+        e = launch_rope_generic(dtype, D, x0, y0, BH, T, lb, transpose, s);
+        if (e == hipSuccess && x1) e = launch_rope_generic(dtype, D, x1, y1, BH, T, lb, transpose, s);
+    }
+    timing_after(kRope, s);
+    return e;
 }
 
 }  // namespace fibattn

@@ -21,7 +21,7 @@ MAX_RUNGS = 32
 MAX_WINDOW = 128
 KERNEL_IDS = {"rope": 0, "forward": 1, "bwd_dq": 2, "bwd_dkdv": 3, "dalpha_reduce": 4}
 EXPORTED = ("fibattn_rung_table", "fibattn_forward", "fibattn_backward_workspace_bytes",
-            "fibattn_backward", "fibattn_rope", "fibattn_status_string",
+            "fibattn_backward", "fibattn_rope", "fibattn_rope_qk", "fibattn_status_string",
             "fibattn_timing_begin", "fibattn_timing_end")
 
 
@@ -53,10 +53,12 @@ def lib():
     L.fibattn_backward_workspace_bytes.argtypes = [i, i, i, i, i, i]
     L.fibattn_backward_workspace_bytes.restype = sz
     L.fibattn_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
-                                   i, i, i, i, i, ip, i, f, i, vp]
+                                   i, i, i, i, i, ip, i, f, f, i, vp]
     L.fibattn_backward.restype = i
     L.fibattn_rope.argtypes = [vp, vp, i, i, i, i, f, i, i, vp]
     L.fibattn_rope.restype = i
+    L.fibattn_rope_qk.argtypes = [vp, vp, vp, vp, i, i, i, i, f, i, vp]
+    L.fibattn_rope_qk.restype = i
     L.fibattn_status_string.argtypes = [i]
     L.fibattn_status_string.restype = ctypes.c_char_p
     L.fibattn_timing_begin.argtypes = [i, i]
@@ -147,8 +149,10 @@ def fibattn_backward_workspace_bytes(B: int, H: int, T: int, d_head: int, W: int
 
 
 def fibattn_backward(q, k, v, o, lse, dO, W: int, base, alpha: float, *, dq=None, dk=None, dv=None,
-                     dalpha=None, workspace=None, stream=None):
-    """dq, dk, dv, dalpha (a 1-element float32 device tensor)."""
+                     dalpha=None, workspace=None, rope_base: float = 0.0, stream=None):
+    """dq, dk, dv, dalpha (a 1-element float32 device tensor).
+
+    rope_base > 0: dq, dk are returned w.r.t. the unrotated q, k (R^T applied)."""
     import torch
 
     B, H, T, D = q.shape
@@ -170,7 +174,7 @@ def fibattn_backward(q, k, v, o, lse, dO, W: int, base, alpha: float, *, dq=None
                                 dO.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
                                 dalpha.data_ptr(), workspace.data_ptr(), workspace.numel(),
                                 B, H, T, D, int(W), bp, b.size, ctypes.c_float(alpha),
-                                _dtype_code(q), _stream(stream))
+                                ctypes.c_float(rope_base), _dtype_code(q), _stream(stream))
     _check("fibattn_backward", st)
     return dq, dk, dv, dalpha
 
@@ -187,6 +191,23 @@ def fibattn_rope(x, rope_base: float = 10000.0, transpose: bool = False, *, out=
                             int(bool(transpose)), _dtype_code(x), _stream(stream))
     _check("fibattn_rope", st)
     return out
+
+
+def fibattn_rope_qk(q, k, rope_base: float = 10000.0, *, q_out=None, k_out=None, stream=None):
+    """R q and R k (RoPE at true positions) in one launch."""
+    import torch
+
+    B, H, T, D = q.shape
+    _check_tensor("q", q, q.shape, q.dtype)
+    _check_tensor("k", k, q.shape, q.dtype)
+    q_out = torch.empty_like(q) if q_out is None else q_out
+    k_out = torch.empty_like(k) if k_out is None else k_out
+    _check_tensor("q_out", q_out, q.shape, q.dtype)
+    _check_tensor("k_out", k_out, q.shape, q.dtype)
+    st = lib().fibattn_rope_qk(q.data_ptr(), k.data_ptr(), q_out.data_ptr(), k_out.data_ptr(), B, H, T,
+                               D, ctypes.c_float(rope_base), _dtype_code(q), _stream(stream))
+    _check("fibattn_rope_qk", st)
+    return q_out, k_out
 
 
 def fibattn_timing_begin(kernel: str, capacity: int):

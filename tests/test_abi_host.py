@@ -78,13 +78,21 @@ def test_invalid_arguments_return_codes_without_gpu():
     assert L.fibattn_forward(16, 16, 16, 16, 16, 1, 1, 8, 64, 129, b, 15, one, 1, None) == 2
     assert L.fibattn_forward(16, 16, 16, 16, 16, 1, 1, 8, 64, 8, b, 15, one, 9, None) == 1
     # workspace
+    zero = ctypes.c_float(0.0)
     assert L.fibattn_backward(16, 16, 16, 16, 16, 16, 16, 16, 16, 16, None, 0,
-                              1, 1, 8, 64, 8, b, 15, one, 1, None) == 3
+                              1, 1, 8, 64, 8, b, 15, one, zero, 1, None) == 3
+    # rope_base must be 0 (no rotation) or > 1
+    assert L.fibattn_backward(16, 16, 16, 16, 16, 16, 16, 16, 16, 16, 16, 1 << 30,
+                              1, 1, 8, 64, 8, b, 15, one, ctypes.c_float(0.5), 1, None) == 1
     assert L.fibattn_backward_workspace_bytes(1, 1, 8, 48, 8, 15) == 0
     assert L.fibattn_backward_workspace_bytes(8, 8, 1024, 64, 8, 15) > 8 * 8 * 1024 * 4
     # rope
     assert L.fibattn_rope(None, None, 1, 1, 8, 64, ctypes.c_float(1e4), 0, 1, None) == 1
     assert L.fibattn_rope(16, 16, 1, 1, 8, 64, ctypes.c_float(1.0), 0, 1, None) == 1
     assert L.fibattn_rope(16, 16, 1, 1, 8, 96, ctypes.c_float(1e4), 0, 1, None) == 2
+    assert L.fibattn_rope(18, 16, 1, 1, 8, 64, ctypes.c_float(1e4), 0, 1, None) == 1  # misaligned
+    assert L.fibattn_rope_qk(16, 16, 16, None, 1, 1, 8, 64, ctypes.c_float(1e4), 1, None) == 1
+    assert L.fibattn_rope_qk(16, 16, 16, 16, 1, 1, 8, 64, ctypes.c_float(1.0), 1, None) == 1
+    assert L.fibattn_rope_qk(16, 16, 16, 16, 1, 1, 8, 48, ctypes.c_float(1e4), 1, None) == 2
     for s in range(5):
         assert F.status_string(s)

@@ -110,23 +110,33 @@ def test_rope_in_place():
     assert torch.equal(x, y)
 
 
-@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
-def test_pipeline_with_rope(dtype):
-    # raw q, k -> RoPE -> attention forward/backward -> R^T on dq, dk, on both sides
-    B, H, T, D, W, alpha = 1, 2, 200, 64, 8, 0.85
-    x = _case_inputs(B, H, T, D, dtype, 60)
-    Q = F.fibattn_rope(x["q"].cuda(), 10000.0)
-    K = F.fibattn_rope(x["k"].cuda(), 10000.0)
+PIPE = [
+    # (dtype, D, W, alpha): bf16/64/W<=16 applies R^T in the backward kernels' epilogue;
+    # the others run the generic kernels followed by an R^T launch
+    ("bf16", 64, 8, 0.85),
+    ("bf16", 64, 8, 1.0),
+    ("fp32", 64, 8, 0.85),
+    ("fp32", 32, 6, 1.2),
+    ("bf16", 64, 20, 0.9),
+]
+
+
+@pytest.mark.parametrize("dtype,D,W,alpha", PIPE)
+def test_pipeline_with_rope(dtype, D, W, alpha):
+    # raw q, k -> RoPE -> attention forward -> backward returning gradients w.r.t. the
+    # raw q, k; the oracle runs the same chain (its rotated q, k rounded to the
+    # storage dtype, as the pipeline stores them)
+    B, H, T = 1, 2, 200
+    x = _case_inputs(B, H, T, D, dtype, 60 + PIPE.index((dtype, D, W, alpha)))
+    Q, K = F.fibattn_rope_qk(x["q"].cuda(), x["k"].cuda(), 10000.0)
     V, G = x["v"].cuda(), x["dO"].cuda()
     o, lse = F.fibattn_forward(Q, K, V, W, FIB, alpha)
-    dq, dk, dv, da = F.fibattn_backward(Q, K, V, o, lse, G, W, FIB, alpha)
-    dq = F.fibattn_rope(dq, 10000.0, True)
-    dk = F.fibattn_rope(dk, 10000.0, True)
+    dq, dk, dv, da = F.fibattn_backward(Q, K, V, o, lse, G, W, FIB, alpha, rope_base=10000.0)
     torch.cuda.synchronize()
     rq, rk = oracle.rope(x["q"]), oracle.rope(x["k"])
-    # the pipeline stores the rotated q, k in the workload dtype: round the oracle's
-    # rotated tensors the same way (torch's round-to-nearest-even conversion)
     rq, rk = (inputs.round_to(r.astype(np.float32), dtype).double().numpy() for r in (rq, rk))
+    np.testing.assert_allclose(Q.double().cpu().numpy(), rq, atol=1e-5 if dtype == "fp32" else 0,
+                               rtol=0 if dtype == "fp32" else 2 ** -7)
     ro, rl = oracle.forward(rq, rk, x["v"], W, FIB, alpha)
     rdq, rdk, rdv, rda, l1 = oracle.backward(rq, rk, x["v"], x["dO"], W, FIB, alpha)
     rdq, rdk = oracle.rope(rdq, transpose=True), oracle.rope(rdk, transpose=True)
@@ -134,7 +144,14 @@ def test_pipeline_with_rope(dtype):
     got = {kk: vv.double().cpu().numpy() for kk, vv in got.items()}
     got["dalpha"] = float(da.item())
     compare(got, {"o": ro, "lse": rl, "dq": rdq, "dk": rdk, "dv": rdv, "dalpha": rda, "l1": l1},
-            dtype if dtype == "bf16" else "fp32", f"pipeline {dtype}")
+            dtype, f"pipeline {dtype} D{D} W{W}")
+
+
+def test_rope_qk_matches_two_single_launches():
+    x = _case_inputs(2, 3, 333, 64, "bf16", 52)
+    q, k = x["q"].cuda(), x["k"].cuda()
+    qa, ka = F.fibattn_rope_qk(q, k, 10000.0)
+    assert torch.equal(qa, F.fibattn_rope(q, 10000.0)) and torch.equal(ka, F.fibattn_rope(k, 10000.0))
 
 
 def test_deterministic_and_stream_independent():
