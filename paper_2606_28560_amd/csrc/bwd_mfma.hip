@@ -7,7 +7,8 @@
 //   band:  S^T = K.Q^T and dP^T = V.dO^T on the matrix cores (16x32 tiles),
 //          dS = P (dP - Delta), dq^T += K^T (tau dS)^T with K^T staged in LDS;
 //   rungs: per-row bf16 dot2 products for <q, k[r0]>, <q, k[r1]>, <dO, v[r0]>,
-//          <dO, v[r1]> (the r1 terms are needed for dalpha even when w = 0),
+//          <dO, v[r1]> (the r1 terms are needed for dalpha even when w = 0; then row
+//          r1 of a query is row r0 of the previous query, taken from its lanes),
 //          dq += tau dS ((1-w) k[r0] + w k[r1]) on the VALU,
 //          dalpha partial += f (tau dS <q, k[r1]-k[r0]> + p <dO, v[r1]-v[r0]>);
 //   writes dq, Delta_i = <dO_i, o_i> and one float64 dalpha partial per workgroup.
@@ -39,6 +40,8 @@ __device__ __forceinline__ bf16x8 staged_operand(const uint16_t *st, int c, int 
 }
 
 // ---------------------------------------------------------------------------
+// INTERP: some rung has w != 0 (rows r0 and r1 both loaded per rung).
+template <bool INTERP>
 __global__ __launch_bounds__(256) void bwd_dq_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const uint16_t *__restrict__ o, const float *__restrict__ lse, const uint16_t *__restrict__ dO,
@@ -81,13 +84,17 @@ __global__ __launch_bounds__(256) void bwd_dq_bf16_d64_kernel(
     int nact = 0;
 #pragma unroll
     for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && rt.d0[r] <= last) ? 1 : 0;
+    // x = {k0, v0, k1, v1}: rows r0 and r1 = r0 - 1 of K and V (r1 filled by fill_r1
+    // below when every w == 0)
     auto load_rung = [&](int r, Slice *x) {
         const int R0 = min(max(i - rt.d0[r], 0), T - 1);
-        const int R1 = max(R0 - 1, 0);
         x[0] = load_row(K, R0, gq);
         x[1] = load_row(V, R0, gq);
-        x[2] = load_row(K, R1, gq);
-        x[3] = load_row(V, R1, gq);
+        if (INTERP) {
+            const int R1 = max(R0 - 1, 0);
+            x[2] = load_row(K, R1, gq);
+            x[3] = load_row(V, R1, gq);
+        }
     };
     Slice xA[4], xB[4];
     if (0 < nact) load_rung(0, xA);  // in flight during the band phase
@@ -123,8 +130,7 @@ __global__ __launch_bounds__(256) void bwd_dq_bf16_d64_kernel(
         acc.c[c] = mfma(staged_operand(kt, c, nm, 16 * wv, gm), C, f32x4{0.f, 0.f, 0.f, 0.f});
     acc_to_quad(acc, lane);
 
-    // rungs (quad layout), one per batch with two batches in flight: the four rows
-    // (k, v at r0 and r1) of a rung are loaded together; r1 = -1 is the zero row
+    // rungs (quad layout), two batches in flight; r1 = -1 is the zero row
     double dal = 0.0;
     auto compute_rung = [&](int r, const Slice *x) {  // x = {k0, v0, k1, v1}
         const int d0 = rt.d0[r];
@@ -141,16 +147,39 @@ __global__ __launch_bounds__(256) void bwd_dq_bf16_d64_kernel(
         const float dP = (1.f - w) * p0 + w * p1;
         const float p = incl ? fast_exp2(sc * sl2 - lse2) : 0.f;
         const float cc = tau * p * (dP - delta);
-        acc_axpy2(acc, cc * (1.f - w), x[0], cc * w, x[2]);
+        if (INTERP)
+            acc_axpy2(acc, cc * (1.f - w), x[0], cc * w, x[2]);
+        else
+            acc_axpy(acc, cc, x[0]);
         if (gq == 0 && incl) dal += (double)rt.f[r] * (double)(cc * (s1 - s0) + p * (p1 - p0));
+    };
+    // with every w == 0 only rows r0 are loaded for all queries: row r1 of query n is
+    // row r0 of query n - 1 (the quad below), and the tile's first query loads its own
+    auto fill_r1 = [&](int r, Slice *x) {
+        if (!INTERP) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                uint32_t *d = reinterpret_cast<uint32_t *>(&x[2 + h]);
+                const uint32_t *src = reinterpret_cast<const uint32_t *>(&x[h]);
+#pragma unroll
+                for (int u = 0; u < 8; ++u) d[u] = (uint32_t)__shfl((int)src[u], (lane - 4) & 63, 64);
+            }
+            if (nq == 0) {
+                const int R1 = min(max(i - rt.d0[r] - 1, 0), T - 1);
+                x[2] = load_row(K, R1, gq);
+                x[3] = load_row(V, R1, gq);
+            }
+        }
     };
 #pragma unroll
     for (int rb = 0; rb < kMaxRungs; rb += 2) {
         if (rb < nact) {
             if (rb + 1 < nact) load_rung(rb + 1, xB);
+            fill_r1(rb, xA);
             compute_rung(rb, xA);
             if (rb + 1 < nact) {
                 if (rb + 2 < nact) load_rung(rb + 2, xA);
+                fill_r1(rb + 1, xB);
                 compute_rung(rb + 1, xB);
             }
         }
@@ -177,9 +206,7 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_d64_kernel(
     uint16_t *__restrict__ dk, uint16_t *__restrict__ dv, const double *__restrict__ partials,
     int n_partials, float *__restrict__ dalpha, int T, int W, RungTable rt, RopeFreq rf, float tau,
     int tiles) {
-    __shared__ __align__(16) uint16_t qr[kStage * kRowStride];
     __shared__ double sfreq[32];
-    __shared__ __align__(16) uint16_t gr[kStage * kRowStride];
     __shared__ __align__(16) uint16_t qt[kD * kTStride];
     __shared__ __align__(16) uint16_t gt[kD * kTStride];
     __shared__ float sl[kStage], sd[kStage];
@@ -249,9 +276,7 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_d64_kernel(
         else load_pair(0, xA);
     }
 
-    // stage q, dO rows (row-major and transposed), lse, Delta for queries [T0, T0+80)
-    stage_rows(qr, kRowStride, Q, T0, kStage, T);
-    stage_rows(gr, kRowStride, G, T0, kStage, T);
+    // stage q, dO rows (transposed), lse, Delta for queries [T0, T0+80)
     stage_transpose(qt, kTStride, Q, T0, kStage, T);
     stage_transpose(gt, kTStride, G, T0, kStage, T);
     for (int c = threadIdx.x; c < kStage; c += 256) {
@@ -266,9 +291,9 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_d64_kernel(
     uint32_t cw[4], pw[4];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
-        const int sr = 16 * wv + 16 * b + nm;  // staged query row
-        const f32x4 s = mfma_dot64(load_slice(qr + sr * kRowStride, gm), km, f32x4{0.f, 0.f, 0.f, 0.f});
-        const f32x4 dp = mfma_dot64(load_slice(gr + sr * kRowStride, gm), vm, f32x4{0.f, 0.f, 0.f, 0.f});
+        const int qrow = min(t0 + 16 * b + nm, T - 1);  // query row of this lane's A operand
+        const f32x4 s = mfma_dot64(load_row(Q, qrow, gm), km, f32x4{0.f, 0.f, 0.f, 0.f});
+        const f32x4 dp = mfma_dot64(load_row(G, qrow, gm), vm, f32x4{0.f, 0.f, 0.f, 0.f});
         float c[4], p[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -312,15 +337,12 @@ __global__ __launch_bounds__(256) void bwd_dkdv_bf16_d64_kernel(
             acc_axpy2(adk, cc[0], x[0], cc[1], x[2]);
             acc_axpy2(adv, pp[0], x[1], pp[1], x[3]);
         };
+        // one batch in flight: the register budget keeps four waves per SIMD resident
 #pragma unroll
-        for (int rb = 0; rb < kMaxRungs; rb += 4) {
+        for (int rb = 0; rb < kMaxRungs; rb += 2) {
             if (rb < nact) {
-                if (rb + 2 < nact) load_pair(rb + 2, xB);
+                if (rb > 0) load_pair(rb, xA);
                 compute_pair(rb, xA);
-                if (rb + 2 < nact) {
-                    if (rb + 4 < nact) load_pair(rb + 4, xA);
-                    compute_pair(rb + 2, xB);
-                }
             }
         }
     } else {
@@ -383,17 +405,23 @@ hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, con
     const int tiles = (T + kBwdB - 1) / kBwdB;
     const float tau = 1.f / sqrtf(64.f);
     const int nb = tiles * BH;
+    bool interp = false;
+    for (int r = 0; r < rt.n; ++r) interp = interp || rt.w[r] != 0.f;
     timing_before(kBwdDq, s);
-    hipLaunchKernelGGL(bwd_dq_bf16_d64_kernel, dim3(nb), dim3(256), 0, s, (const uint16_t *)q,
-                       (const uint16_t *)k, (const uint16_t *)v, (const uint16_t *)o, lse,
-                       (const uint16_t *)dO, (uint16_t *)dq, delta_ws, partials, T, W, rt, rf, tau,
-                       tiles);
+    if (interp)
+        hipLaunchKernelGGL(bwd_dq_bf16_d64_kernel<true>, dim3(nb), dim3(256), 0, s,
+                           (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v,
+                           (const uint16_t *)o, lse, (const uint16_t *)dO, (uint16_t *)dq, delta_ws,
+                           partials, T, W, rt, rf, tau, tiles);
+    else
+        hipLaunchKernelGGL(bwd_dq_bf16_d64_kernel<false>, dim3(nb), dim3(256), 0, s,
+                           (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v,
+                           (const uint16_t *)o, lse, (const uint16_t *)dO, (uint16_t *)dq, delta_ws,
+                           partials, T, W, rt, rf, tau, tiles);
     timing_after(kBwdDq, s);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     timing_before(kBwdDkDv, s);
-    bool interp = false;
-    for (int r = 0; r < rt.n; ++r) interp = interp || rt.w[r] != 0.f;
     if (interp)
         hipLaunchKernelGGL(bwd_dkdv_bf16_d64_kernel<true>, dim3(nb), dim3(256), 0, s,
                            (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v, lse,
