@@ -17,6 +17,7 @@ a reported baseline.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -45,6 +46,42 @@ def parse_args():
     p.add_argument("--copy-probe-mb", type=int, default=0,
                    help="also run one plain device copy of this many MiB (counter calibration)")
     return p.parse_args()
+
+
+# HBM traffic per launch of the layer_60m_fixed_T1024 kernels, from two rocprofv3 --pmc
+# passes (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) over
+#   bench.py --eager --steps 10 --warmup 2 --no-cpu-baseline --no-t4096 --copy-probe-mb 256
+# each scaled by what the same counter reads for the plain 256 MiB device copy of that run.
+# They hold only for the kernel sources they were taken on (COUNTER_SOURCES_SHA).
+COUNTER_SOURCES_SHA = "6ed9aa1b7097cf75350ec0e557b525d1bece916cd755925459842a6fb30b9dca"
+COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
+COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
+    "forward": (12376.2, 8448.0),
+    "bwd_dq": (20774.0, 8480.4),
+    "bwd_dkdv": (16787.8, 16384.0),
+    "rope": (8212.2, 16384.0),
+}
+COPY_PROBE_KIB = (262144.0, 131093.2, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
+
+
+def kernel_sources_sha() -> str:
+    d = os.path.join(ROOT, "paper_2606_28560_amd", "csrc")
+    h = hashlib.sha256()
+    for n in sorted(os.listdir(d)):
+        if n.endswith((".hip", ".h")):
+            h.update(n.encode())
+            with open(os.path.join(d, n), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def hbm_traffic(kernel: str, workload: str):
+    """Calibrated HBM bytes per launch, or None when the counters do not apply."""
+    if workload != COUNTER_WORKLOAD or kernel not in COUNTER_KIB or kernel_sources_sha() != COUNTER_SOURCES_SHA:
+        return None
+    fetch, write = COUNTER_KIB[kernel]
+    moved, copy_fetch, copy_write = COPY_PROBE_KIB
+    return (fetch * moved / copy_fetch + write * moved / copy_write) * 1024.0
 
 
 # algorithmic bytes per query-head (s = bytes per element, D = d_head)
@@ -132,10 +169,11 @@ def timed(run, steps: int, warmup: int):
 
 
 def kernel_time(F, sets, kernel: str, steps: int, per_step: int):
-    """Mean launch duration (ms) of one library kernel over `steps` eager steps, from
-    HIP events the library records around each launch on the launch stream.  A spin
-    kernel (no memory traffic) ahead of each step keeps the queue non-empty, so that
-    the host's launch latency does not fall between an event pair and its kernel."""
+    """Mean launch duration (ms) of one library kernel over `steps` eager steps.  The
+    library launches that kernel with a HIP event pair that takes the dispatch's own
+    start and end timestamps (hipExtLaunchKernel on the launch stream), the interval a
+    kernel-trace profile reports.  A spin kernel (no memory traffic) ahead of each step
+    keeps the queue busy, as in the graph-replayed steps."""
     import torch
 
     torch.cuda.synchronize()
@@ -252,7 +290,7 @@ def main():
     units = qh  # query-heads per launch
     achieved = alg_bytes(dom, wl.D, s) * units / (kt[dom]["mean_ms"] * 1e-3) / 1e9
     roofline = {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+                "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": hbm_traffic(dom, wl.name),
                 "bytes_per_launch": alg_bytes(dom, wl.D, s) * units,
                 "mean_launch_ms": kt[dom]["mean_ms"]}
 

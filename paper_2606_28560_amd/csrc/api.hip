@@ -62,24 +62,18 @@ struct Timing {
     int capacity = 0;
     std::vector<hipEvent_t> ev;  // start/stop pairs
     int used = 0;
-    bool open = false;
 } g_timing;
 
 }  // namespace
 
 namespace fibattn {
 
-void timing_before(int id, hipStream_t s) {
-    if (id != g_timing.id || g_timing.used >= g_timing.capacity) return;
-    (void)hipEventRecord(g_timing.ev[2 * g_timing.used], s);
-    g_timing.open = true;
-}
-
-void timing_after(int id, hipStream_t s) {
-    if (id != g_timing.id || !g_timing.open) return;
-    (void)hipEventRecord(g_timing.ev[2 * g_timing.used + 1], s);
-    g_timing.open = false;
+bool timing_events(int id, hipEvent_t *start, hipEvent_t *stop) {
+    if (id != g_timing.id || g_timing.used >= g_timing.capacity) return false;
+    *start = g_timing.ev[2 * g_timing.used];
+    *stop = g_timing.ev[2 * g_timing.used + 1];
     ++g_timing.used;
+    return true;
 }
 
 }  // namespace fibattn
@@ -201,7 +195,6 @@ fibattn_status_t fibattn_timing_begin(int kernel_id, int capacity) {
     g_timing.id = kernel_id;
     g_timing.capacity = capacity;
     g_timing.used = 0;
-    g_timing.open = false;
     return FIBATTN_OK;
 }
 

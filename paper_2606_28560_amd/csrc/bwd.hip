@@ -255,25 +255,15 @@ static hipError_t launch_bwd_t(const void *q, const void *k, const void *v, cons
     constexpr int QPB = 256 / (D / Vec<S>::N);
     const float tau = 1.f / sqrtf((float)D);
     dim3 grid((T + QPB - 1) / QPB, BH);
-    timing_before(kBwdDq, s);
-    hipLaunchKernelGGL((bwd_dq_kernel<S, D>), grid, dim3(256), 0, s, (const S *)q, (const S *)k,
-                       (const S *)v, (const S *)o, lse, (const S *)dO, (S *)dq, delta_ws,
-                       partials, T, W, rt, tau);
-    timing_after(kBwdDq, s);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch(kBwdDq, bwd_dq_kernel<S, D>, grid, dim3(256), 0, s, (const S *)q,
+                          (const S *)k, (const S *)v, (const S *)o, lse, (const S *)dO, (S *)dq,
+                          delta_ws, partials, T, W, rt, tau);
     if (e != hipSuccess) return e;
-    timing_before(kBwdDkDv, s);
-    hipLaunchKernelGGL((bwd_dkdv_kernel<S, D>), grid, dim3(256), 0, s, (const S *)q,
-                       (const S *)k, (const S *)v, lse, (const S *)dO, delta_ws, (S *)dk,
-                       (S *)dv, T, W, rt, tau);
-    timing_after(kBwdDkDv, s);
-    e = hipGetLastError();
+    e = launch(kBwdDkDv, bwd_dkdv_kernel<S, D>, grid, dim3(256), 0, s, (const S *)q, (const S *)k,
+               (const S *)v, lse, (const S *)dO, delta_ws, (S *)dk, (S *)dv, T, W, rt, tau);
     if (e != hipSuccess) return e;
-    timing_before(kDalphaReduce, s);
-    hipLaunchKernelGGL(dalpha_reduce_kernel, dim3(1), dim3(256), 0, s, partials,
-                       (size_t)grid.x * grid.y, dalpha);
-    timing_after(kDalphaReduce, s);
-    return hipGetLastError();
+    return launch(kDalphaReduce, dalpha_reduce_kernel, dim3(1), dim3(256), 0, s, partials,
+                  (size_t)grid.x * grid.y, dalpha);
 }
 
 static hipError_t launch_backward_generic(int dtype, int D, const void *q, const void *k, const void *v,

@@ -407,33 +407,13 @@ hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, con
     const int nb = tiles * BH;
     bool interp = false;
     for (int r = 0; r < rt.n; ++r) interp = interp || rt.w[r] != 0.f;
-    timing_before(kBwdDq, s);
-    if (interp)
-        hipLaunchKernelGGL(bwd_dq_bf16_d64_kernel<true>, dim3(nb), dim3(256), 0, s,
-                           (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v,
-                           (const uint16_t *)o, lse, (const uint16_t *)dO, (uint16_t *)dq, delta_ws,
-                           partials, T, W, rt, rf, tau, tiles);
-    else
-        hipLaunchKernelGGL(bwd_dq_bf16_d64_kernel<false>, dim3(nb), dim3(256), 0, s,
-                           (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v,
-                           (const uint16_t *)o, lse, (const uint16_t *)dO, (uint16_t *)dq, delta_ws,
-                           partials, T, W, rt, rf, tau, tiles);
-    timing_after(kBwdDq, s);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch(kBwdDq, interp ? bwd_dq_bf16_d64_kernel<true> : bwd_dq_bf16_d64_kernel<false>,
+                          dim3(nb), dim3(256), 0, s, q, k, v, o, lse, dO, dq, delta_ws, partials,
+                          T, W, rt, rf, tau, tiles);
     if (e != hipSuccess) return e;
-    timing_before(kBwdDkDv, s);
-    if (interp)
-        hipLaunchKernelGGL(bwd_dkdv_bf16_d64_kernel<true>, dim3(nb), dim3(256), 0, s,
-                           (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v, lse,
-                           (const uint16_t *)dO, delta_ws, (uint16_t *)dk, (uint16_t *)dv, partials,
-                           nb, dalpha, T, W, rt, rf, tau, tiles);
-    else
-        hipLaunchKernelGGL(bwd_dkdv_bf16_d64_kernel<false>, dim3(nb), dim3(256), 0, s,
-                           (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v, lse,
-                           (const uint16_t *)dO, delta_ws, (uint16_t *)dk, (uint16_t *)dv, partials,
-                           nb, dalpha, T, W, rt, rf, tau, tiles);
-    timing_after(kBwdDkDv, s);
-    return hipGetLastError();
+    return launch(kBwdDkDv, interp ? bwd_dkdv_bf16_d64_kernel<true> : bwd_dkdv_bf16_d64_kernel<false>,
+                  dim3(nb), dim3(256), 0, s, q, k, v, lse, dO, delta_ws, dk, dv, partials, nb,
+                  dalpha, T, W, rt, rf, tau, tiles);
 }
 
 }  // namespace fibattn

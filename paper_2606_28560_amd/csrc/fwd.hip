@@ -114,11 +114,8 @@ static hipError_t launch_fwd_t(const void *q, const void *k, const void *v, void
     dim3 grid((T + QPB - 1) / QPB, BH);
     const size_t lds = sizeof(float) * QPB * (size_t)(W + 1 + rt.n);
     const float scale_log2 = kLog2e / sqrtf((float)D);
-    timing_before(kForward, s);
-    hipLaunchKernelGGL((fwd_kernel<S, D>), grid, dim3(256), lds, s, (const S *)q, (const S *)k,
-                       (const S *)v, (S *)o, lse, T, W, rt, scale_log2);
-    timing_after(kForward, s);
-    return hipGetLastError();
+    return launch(kForward, fwd_kernel<S, D>, grid, dim3(256), (unsigned)lds, s, (const S *)q,
+                  (const S *)k, (const S *)v, (S *)o, lse, T, W, rt, scale_log2);
 }
 
 hipError_t launch_forward(int dtype, int D, const void *q, const void *k, const void *v, void *o,

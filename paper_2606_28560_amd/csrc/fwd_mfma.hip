@@ -191,17 +191,8 @@ hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void
                                int BH, int T, int W, const RungTable &rt, hipStream_t s) {
     const int tiles = (T + kFwdBQ - 1) / kFwdBQ;
     const float sl2 = kLog2e / sqrtf(64.f);
-    timing_before(kForward, s);
-    if (any_interp(rt))
-        hipLaunchKernelGGL(fwd_bf16_d64_kernel<true>, dim3(tiles * BH), dim3(256), 0, s,
-                           (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v,
-                           (uint16_t *)o, lse, T, W, rt, sl2, tiles);
-    else
-        hipLaunchKernelGGL(fwd_bf16_d64_kernel<false>, dim3(tiles * BH), dim3(256), 0, s,
-                           (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v,
-                           (uint16_t *)o, lse, T, W, rt, sl2, tiles);
-    timing_after(kForward, s);
-    return hipGetLastError();
+    return launch(kForward, any_interp(rt) ? fwd_bf16_d64_kernel<true> : fwd_bf16_d64_kernel<false>,
+                  dim3(tiles * BH), dim3(256), 0, s, q, k, v, o, lse, T, W, rt, sl2, tiles);
 }
 
 }  // namespace fibattn

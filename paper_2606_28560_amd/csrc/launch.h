@@ -1,6 +1,7 @@
 // Host-side launchers of the fibattn kernels (internal to libfibattn.so).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -10,9 +11,23 @@ namespace fibattn {
 
 enum KernelId { kRope = 0, kForward = 1, kBwdDq = 2, kBwdDkDv = 3, kDalphaReduce = 4, kNumKernels = 5 };
 
-// Records a HIP event before / after a launch when kernel timing is active for `id`.
-void timing_before(int id, hipStream_t s);
-void timing_after(int id, hipStream_t s);
+// The start/stop event pair for the next launch of kernel `id` while kernel timing is
+// active for it; false otherwise.
+bool timing_events(int id, hipEvent_t *start, hipEvent_t *stop);
+
+// Launches `kernel`; while timing is active for `id` the launch carries an event pair that
+// takes the dispatch's own start and end timestamps (hipExtLaunchKernel), so the pair
+// measures this kernel alone, free of marker packets and launch gaps.
+template <typename... P, typename... A>
+hipError_t launch(int id, void (*kernel)(P...), dim3 grid, dim3 block, unsigned lds, hipStream_t s,
+                  A... args) {
+    hipEvent_t e0, e1;
+    if (timing_events(id, &e0, &e1))
+        hipExtLaunchKernelGGL(kernel, grid, block, lds, s, e0, e1, 0u, static_cast<P>(args)...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, lds, s, static_cast<P>(args)...);
+    return hipGetLastError();
+}
 
 // dtype: 0 float32, 1 bfloat16.  All launchers return hipGetLastError() of their launches.
 hipError_t launch_forward(int dtype, int D, const void *q, const void *k, const void *v, void *o,

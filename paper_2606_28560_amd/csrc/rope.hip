@@ -118,41 +118,31 @@ static hipError_t launch_rope_generic(int dtype, int D, const void *x, void *y, 
                                       double lb, int transpose, hipStream_t s) {
     dim3 grid((T + kRopeTP - 1) / kRopeTP, (BH + kRopeRB - 1) / kRopeRB);
     if (dtype == 0 && D == 32)
-        hipLaunchKernelGGL((rope_kernel<float, 32>), grid, dim3(256), 0, s, (const float *)x,
-                           (float *)y, BH, T, lb, transpose);
-    else if (dtype == 0 && D == 64)
-        hipLaunchKernelGGL((rope_kernel<float, 64>), grid, dim3(256), 0, s, (const float *)x,
-                           (float *)y, BH, T, lb, transpose);
-    else if (dtype == 1 && D == 32)
-        hipLaunchKernelGGL((rope_kernel<uint16_t, 32>), grid, dim3(256), 0, s,
-                           (const uint16_t *)x, (uint16_t *)y, BH, T, lb, transpose);
-    else if (dtype == 1 && D == 64)
-        hipLaunchKernelGGL((rope_kernel<uint16_t, 64>), grid, dim3(256), 0, s,
-                           (const uint16_t *)x, (uint16_t *)y, BH, T, lb, transpose);
-    else
-        return hipErrorInvalidValue;
-    return hipGetLastError();
+        return launch(kRope, rope_kernel<float, 32>, grid, dim3(256), 0, s, x, y, BH, T, lb, transpose);
+    if (dtype == 0 && D == 64)
+        return launch(kRope, rope_kernel<float, 64>, grid, dim3(256), 0, s, x, y, BH, T, lb, transpose);
+    if (dtype == 1 && D == 32)
+        return launch(kRope, rope_kernel<uint16_t, 32>, grid, dim3(256), 0, s, x, y, BH, T, lb,
+                      transpose);
+    if (dtype == 1 && D == 64)
+        return launch(kRope, rope_kernel<uint16_t, 64>, grid, dim3(256), 0, s, x, y, BH, T, lb,
+                      transpose);
+    return hipErrorInvalidValue;
 }
 
 // One launch for one tensor (x1 == nullptr) or two tensors of the same shape.
 hipError_t launch_rope(int dtype, int D, const void *x0, void *y0, const void *x1, void *y1, int BH,
                        int T, float rope_base, int transpose, hipStream_t s) {
     const double lb = (double)rope_base;
-    timing_before(kRope, s);
-    hipError_t e = hipSuccess;
     if (dtype == 1 && D == 64) {
         const RopeFreq rf = make_rope_freq(lb, 64);
-        hipLaunchKernelGGL(rope_bf16_d64_kernel,
-                           dim3((T + kRope64TP - 1) / kRope64TP, (BH + kRope64RB - 1) / kRope64RB,
-                                x1 ? 2 : 1),
-                           dim3(256), 0, s, (const uint16_t *)x0, (uint16_t *)y0,
-                           (const uint16_t *)x1, (uint16_t *)y1, BH, T, rf, transpose);
-        e = hipGetLastError();
-    } else {
-        e = launch_rope_generic(dtype, D, x0, y0, BH, T, lb, transpose, s);
-        if (e == hipSuccess && x1) e = launch_rope_generic(dtype, D, x1, y1, BH, T, lb, transpose, s);
+        return launch(kRope, rope_bf16_d64_kernel,
+                      dim3((T + kRope64TP - 1) / kRope64TP, (BH + kRope64RB - 1) / kRope64RB,
+                           x1 ? 2 : 1),
+                      dim3(256), 0, s, x0, y0, x1, y1, BH, T, rf, transpose);
     }
-    timing_after(kRope, s);
+    hipError_t e = launch_rope_generic(dtype, D, x0, y0, BH, T, lb, transpose, s);
+    if (e == hipSuccess && x1) e = launch_rope_generic(dtype, D, x1, y1, BH, T, lb, transpose, s);
     return e;
 }
 
