@@ -42,7 +42,7 @@ __device__ __forceinline__ bf16x8 staged_operand(const uint16_t *st, int c, int 
 // ---------------------------------------------------------------------------
 // INTERP: some rung has w != 0 (rows r0 and r1 both loaded per rung).
 template <bool INTERP>
-__global__ __launch_bounds__(256) void bwd_dq_bf16_d64_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void bwd_dq_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const uint16_t *__restrict__ o, const float *__restrict__ lse, const uint16_t *__restrict__ dO,
     uint16_t *__restrict__ dq, float *__restrict__ delta_out, double *__restrict__ partials, int T,
@@ -200,7 +200,7 @@ __global__ __launch_bounds__(256) void bwd_dq_bf16_d64_kernel(
 
 // ---------------------------------------------------------------------------
 template <bool INTERP>
-__global__ __launch_bounds__(256) void bwd_dkdv_bf16_d64_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 : 4))) void bwd_dkdv_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const float *__restrict__ lse, const uint16_t *__restrict__ dO, const float *__restrict__ delta_in,
     uint16_t *__restrict__ dk, uint16_t *__restrict__ dv, const double *__restrict__ partials,

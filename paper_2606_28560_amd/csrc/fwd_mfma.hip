@@ -26,7 +26,7 @@ constexpr int kVtStride = 132;             // bf16 per dim row of the staged V^T
 
 // INTERP: some rung has w != 0, so the second row r1 is read.
 template <bool INTERP>
-__global__ __launch_bounds__(256) void fwd_bf16_d64_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void fwd_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     uint16_t *__restrict__ o, float *__restrict__ lse, int T, int W, RungTable rt, float sl2,
     int tiles) {
