@@ -5,7 +5,8 @@
 //
 // dq kernel (query-stationary, 64 queries per workgroup, 16 per wave):
 //   band:  S^T = K.Q^T and dP^T = V.dO^T on the matrix cores (16x32 tiles),
-//          dS = P (dP - Delta), dq^T += K^T (tau dS)^T with K^T staged in LDS;
+//          dS = P (dP - Delta), dq^T += K^T (tau dS)^T; the band's K and V rows are
+//          copied to LDS with direct-to-LDS loads;
 //   rungs: per-row bf16 dot2 products for <q, k[r0]>, <q, k[r1]>, <dO, v[r0]>,
 //          <dO, v[r1]> (the r1 terms are needed for dalpha even when w = 0; then row
 //          r1 of a query is row r0 of the previous query, taken from its lanes),
@@ -16,7 +17,7 @@
 // that read key row j are j..j+W (window) and, for rung k, j+floor(d_k) (as row r0,
 // weight 1-w) and j+floor(d_k)+1 (as row r1, weight w):
 //   band:  S = Q.K^T and dP = dO.V^T tiles, dk^T += Q^T (tau dS), dv^T += dO^T P with
-//          Q^T, dO^T staged in LDS;
+//          the band's q and dO rows copied to LDS with direct-to-LDS loads;
 //   rungs: per-row dot2 products on the VALU;
 //   each dk/dv row is written once; no atomics.  Workgroup 0 also sums the dalpha
 //   partials in a fixed order (float64), after the dq kernel has finished.
@@ -27,17 +28,6 @@ namespace fibattn {
 
 constexpr int kBwdB = 64;                // rows per workgroup
 constexpr int kStage = kBwdB + 16;       // staged rows
-constexpr int kRowStride = 72;           // bf16 per staged row (row-major)
-constexpr int kTStride = 132;            // bf16 per dim row of a staged transpose
-
-// A operand of a transposed-operand MFMA: dim out_dim(c, n) of the staged rows
-// base + 4g .. +4 and base + 16 + 4g .. +4 (k index 8g+j <-> block j/4, row 4g+j%4).
-__device__ __forceinline__ bf16x8 staged_operand(const uint16_t *st, int c, int n, int base, int g) {
-    const uint16_t *src = st + out_dim(c, n) * kTStride + base + 4 * g;
-    const uint2 a0 = *reinterpret_cast<const uint2 *>(src);
-    const uint2 a1 = *reinterpret_cast<const uint2 *>(src + 16);
-    return as_bf8(make_uint4(a0.x, a0.y, a1.x, a1.y));
-}
 
 // ---------------------------------------------------------------------------
 // INTERP: some rung has w != 0 (rows r0 and r1 both loaded per rung).
@@ -47,10 +37,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     const uint16_t *__restrict__ o, const float *__restrict__ lse, const uint16_t *__restrict__ dO,
     uint16_t *__restrict__ dq, float *__restrict__ delta_out, double *__restrict__ partials, int T,
     int W, RungTable rt, RopeFreq rf, float tau, int tiles) {
-    __shared__ __align__(16) uint16_t kr[kStage * kRowStride];
+    __shared__ __align__(16) uint16_t kr[kStage * kD];
+    __shared__ __align__(16) uint16_t vr[kStage * kD];
     __shared__ double sfreq[32];
-    __shared__ __align__(16) uint16_t vr[kStage * kRowStride];
-    __shared__ __align__(16) uint16_t kt[kD * kTStride];
     __shared__ double red[4];
 
     const int lane = threadIdx.x & 63;
@@ -84,6 +73,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     int nact = 0;
 #pragma unroll
     for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && rt.d0[r] <= last) ? 1 : 0;
+    nact = __builtin_amdgcn_readfirstlane(nact);  // wave-uniform: scalar branches
     // x = {k0, v0, k1, v1}: rows r0 and r1 = r0 - 1 of K and V (r1 filled by fill_r1
     // below when every w == 0)
     auto load_rung = [&](int r, Slice *x) {
@@ -99,10 +89,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     Slice xA[4], xB[4];
     if (0 < nact) load_rung(0, xA);  // in flight during the band phase
 
-    stage_rows(kr, kRowStride, K, T0 - 16, kStage, T);
-    stage_rows(vr, kRowStride, V, T0 - 16, kStage, T);
-    stage_transpose(kt, kTStride, K, T0 - 16, kStage, T);
+    // band rows [T0-16, T0+64) of K and V, straight to LDS (rows outside [0, T) are
+    // clamped copies: their keys are masked below)
+    dma_rows<kStage>(kr, K, T0 - 16, T);
+    dma_rows<kStage>(vr, V, T0 - 16, T);
     stage_freq(sfreq, rf);
+    wait_vmem();
     __syncthreads();
 
     // band (MFMA layout): keys [t0-16, t0+16)
@@ -110,8 +102,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
         const int sr = 16 * wv + 16 * b + nm;  // staged row
-        const f32x4 s = mfma_dot64(load_slice(kr + sr * kRowStride, gm), qm, f32x4{0.f, 0.f, 0.f, 0.f});
-        const f32x4 dp = mfma_dot64(load_slice(vr + sr * kRowStride, gm), gmm, f32x4{0.f, 0.f, 0.f, 0.f});
+        const f32x4 s = mfma_dot64(dma_slice(kr, sr, gm), qm, f32x4{0.f, 0.f, 0.f, 0.f});
+        const f32x4 dp = mfma_dot64(dma_slice(vr, sr, gm), gmm, f32x4{0.f, 0.f, 0.f, 0.f});
         float c[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -127,7 +119,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     Acc16 acc;
 #pragma unroll
     for (int c = 0; c < 4; ++c)
-        acc.c[c] = mfma(staged_operand(kt, c, nm, 16 * wv, gm), C, f32x4{0.f, 0.f, 0.f, 0.f});
+        acc.c[c] = mfma(dma_operand_t(kr, c, nm, 16 * wv, gm), C, f32x4{0.f, 0.f, 0.f, 0.f});
     acc_to_quad(acc, lane);
 
     // rungs (quad layout), two batches in flight; r1 = -1 is the zero row
@@ -207,8 +199,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
     int n_partials, float *__restrict__ dalpha, int T, int W, RungTable rt, RopeFreq rf, float tau,
     int tiles) {
     __shared__ double sfreq[32];
-    __shared__ __align__(16) uint16_t qt[kD * kTStride];
-    __shared__ __align__(16) uint16_t gt[kD * kTStride];
+    __shared__ __align__(16) uint16_t qr[kStage * kD];
+    __shared__ __align__(16) uint16_t gr[kStage * kD];
     __shared__ float sl[kStage], sd[kStage];
     __shared__ double red[256];
 
@@ -253,6 +245,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
     int nact = 0;
 #pragma unroll
     for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && t0 + rt.d0[r] < T) ? 1 : 0;
+    nact = __builtin_amdgcn_readfirstlane(nact);  // wave-uniform: scalar branches
     // rows of query i0 = j + d0 (and i0 + 1 when interpolating) for a rung
     auto load_rung = [&](int r, Slice *x) {
         const int i0c = min(j + rt.d0[r], T - 1);
@@ -276,24 +269,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
         else load_pair(0, xA);
     }
 
-    // stage q, dO rows (transposed), lse, Delta for queries [T0, T0+80)
-    stage_transpose(qt, kTStride, Q, T0, kStage, T);
-    stage_transpose(gt, kTStride, G, T0, kStage, T);
+    // q and dO rows, lse and Delta of queries [T0, T0+80) (rows past the end are
+    // clamped copies, masked below)
+    dma_rows<kStage>(qr, Q, T0, T);
+    dma_rows<kStage>(gr, G, T0, T);
     for (int c = threadIdx.x; c < kStage; c += 256) {
         const int row = T0 + c;
         sl[c] = row < T ? L[row] * kLog2e : 0.f;
         sd[c] = row < T ? Dl[row] : 0.f;
     }
     stage_freq(sfreq, rf);
+    wait_vmem();
     __syncthreads();
 
     // band (MFMA layout): queries [t0, t0 + 32) in two blocks
     uint32_t cw[4], pw[4];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
-        const int qrow = min(t0 + 16 * b + nm, T - 1);  // query row of this lane's A operand
-        const f32x4 s = mfma_dot64(load_row(Q, qrow, gm), km, f32x4{0.f, 0.f, 0.f, 0.f});
-        const f32x4 dp = mfma_dot64(load_row(G, qrow, gm), vm, f32x4{0.f, 0.f, 0.f, 0.f});
+        const int sq = 16 * wv + 16 * b + nm;  // staged query row of this lane's A operand
+        const f32x4 s = mfma_dot64(dma_slice(qr, sq, gm), km, f32x4{0.f, 0.f, 0.f, 0.f});
+        const f32x4 dp = mfma_dot64(dma_slice(gr, sq, gm), vm, f32x4{0.f, 0.f, 0.f, 0.f});
         float c[4], p[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -313,8 +308,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
     Acc16 adk, adv;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-        adk.c[c] = mfma(staged_operand(qt, c, nm, 16 * wv, gm), Cb, f32x4{0.f, 0.f, 0.f, 0.f});
-        adv.c[c] = mfma(staged_operand(gt, c, nm, 16 * wv, gm), Pb, f32x4{0.f, 0.f, 0.f, 0.f});
+        adk.c[c] = mfma(dma_operand_t(qr, c, nm, 16 * wv, gm), Cb, f32x4{0.f, 0.f, 0.f, 0.f});
+        adv.c[c] = mfma(dma_operand_t(gr, c, nm, 16 * wv, gm), Pb, f32x4{0.f, 0.f, 0.f, 0.f});
     }
     acc_to_quad(adk, lane);
     acc_to_quad(adv, lane);

@@ -5,15 +5,16 @@
 // one (batch, head) (four waves of 16).  For a wave's queries [t0, t0+16):
 //   - the window band lies in the 32 key rows [t0-16, t0+16).  Its logits are one
 //     16x32 tile of Q.K^T on the matrix cores, masked to 0 <= i - j <= W; the
-//     probability-weighted values are (V^T P^T) on the matrix cores, with V^T staged
-//     in LDS once per workgroup;
+//     probability-weighted values are (V^T P^T) on the matrix cores; the band's K
+//     and V rows are copied to LDS once per workgroup with direct-to-LDS loads;
 //   - every rung is a contiguous shifted block: query t0+n reads rows t0+n-floor(d)
 //     and t0+n-floor(d)-1.  Those logits are per-row dot products (bf16 dot2, four
 //     lanes per row) blended in score space; the blended values are accumulated on
 //     the VALU in the same register layout as the matrix-core output.
-// Softmax runs in base 2: the band sets the first running maximum, then rungs are
-// taken a batch at a time (their key and value rows loaded together), rescaling the
-// running sum and weighted values when the maximum grows.
+// Softmax runs in base 2: the band's maximum is the first running reference, then
+// rungs are taken a batch at a time (their key and value rows loaded together),
+// rescaling the running sum and weighted values only when a logit exceeds the
+// reference by a wide margin.
 #include "launch.h"
 #include "mfma.h"
 
@@ -21,8 +22,7 @@ namespace fibattn {
 
 constexpr int kFwdBQ = 64;                 // queries per workgroup
 constexpr int kBandRows = kFwdBQ + 16;     // staged band rows [T0-16, T0+64)
-constexpr int kRowStride = 72;             // bf16 per staged K row (row-major)
-constexpr int kVtStride = 132;             // bf16 per dim row of the staged V^T
+constexpr float kSlack = 8.f;              // log2 units a logit may exceed the running reference
 
 // INTERP: some rung has w != 0, so the second row r1 is read.
 template <bool INTERP>
@@ -32,8 +32,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     int tiles) {
     constexpr int RB = INTERP ? 1 : 2;  // rungs per load batch; two batches in flight
     constexpr int NS = INTERP ? 2 : 1;  // rows per rung (r0, and r1 when interpolating)
-    __shared__ __align__(16) uint16_t kr[kBandRows * kRowStride];
-    __shared__ __align__(16) uint16_t vt[kD * kVtStride];
+    __shared__ __align__(16) uint16_t kr[kBandRows * kD];
+    __shared__ __align__(16) uint16_t vr[kBandRows * kD];
 
     const int lane = threadIdx.x & 63;
     const int wv = threadIdx.x >> 6;
@@ -53,10 +53,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     int nact = 0;
 #pragma unroll
     for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && rt.d0[r] <= last) ? 1 : 0;
+    nact = __builtin_amdgcn_readfirstlane(nact);  // wave-uniform: scalar branches
 
     const int im = t0 + nm;  // query of this lane in the MFMA layout
     const int i = t0 + nq;   // ... in the quad layout
-    const Slice qm = load_row(Q, min(im, T - 1), gm);
     const Slice qq = load_row(Q, min(i, T - 1), gq);
 
     // rung rows of a batch: kx[x*NS + s], vx[x*NS + s] = row r_s of rung rb + x
@@ -74,18 +74,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     };
     Slice kA[RB * NS], vA[RB * NS], kB[RB * NS], vB[RB * NS];
     if (0 < nact) load_batch(0, kA, vA);  // in flight during the band phase
-
-    // band rows [T0-16, T0+64): K row-major, V transposed (zero outside [0, T))
-    stage_rows(kr, kRowStride, K, T0 - 16, kBandRows, T);
-    stage_transpose(vt, kVtStride, V, T0 - 16, kBandRows, T);
+    // band rows [T0-16, T0+64) of K and V, straight to LDS (rows outside [0, T) are
+    // clamped copies: their keys are masked below)
+    dma_rows<kBandRows>(kr, K, T0 - 16, T);
+    dma_rows<kBandRows>(vr, V, T0 - 16, T);
+    wait_vmem();
     __syncthreads();
 
     // ---- window band (MFMA layout): logits (log2 units), maximum, probabilities ----
+    const Slice qm = slice_from_quad(qq, lane);  // the wave's q rows in the MFMA layout
     float m = -INFINITY;
     f32x4 sb[2];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
-        const Slice kb = load_slice(kr + (16 * wv + 16 * b + nm) * kRowStride, gm);
+        const Slice kb = dma_slice(kr, 16 * wv + 16 * b + nm, gm);
         sb[b] = mfma_dot64(kb, qm, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -95,9 +97,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
             m = fmaxf(m, sb[b][e]);
         }
     }
-    m = max4(m);
-    if (m == -INFINITY) m = 0.f;  // only rows past the end of the sequence
-    float lb = 0.f;
+    m = max4(m);  // finite: key im itself is always in the band
+    float l = 0.f;
     uint32_t pw[4];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
@@ -105,27 +106,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             p[e] = fast_exp2(sb[b][e] - m);
-            lb += p[e];
+            l += p[e];
         }
         pw[2 * b] = pack_bf16(p[0], p[1]);
         pw[2 * b + 1] = pack_bf16(p[2], p[3]);
     }
-    float l = sum4(lb);
+    l = sum4(l);
     const bf16x8 P = as_bf8(make_uint4(pw[0], pw[1], pw[2], pw[3]));
+    // V^T.P^T, the A operand gathered from the row-major staged V
     Acc16 acc;
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        const uint16_t *src = vt + out_dim(c, nm) * kVtStride + 16 * wv + 4 * gm;
-        const uint2 a0 = *reinterpret_cast<const uint2 *>(src);
-        const uint2 a1 = *reinterpret_cast<const uint2 *>(src + 16);
-        acc.c[c] = mfma(as_bf8(make_uint4(a0.x, a0.y, a1.x, a1.y)), P, f32x4{0.f, 0.f, 0.f, 0.f});
-    }
+    for (int c = 0; c < 4; ++c)
+        acc.c[c] = mfma(dma_operand_t(vr, c, nm, 16 * wv, gm), P, f32x4{0.f, 0.f, 0.f, 0.f});
     // hand the band results to the quad layout
     acc_to_quad(acc, lane);
     m = to_quad(m, lane);
     l = to_quad(l, lane);
 
-    // ---- rungs (quad layout): logits of a batch, running maximum, rescale, values ----
+    // ---- rungs (quad layout): logits of a batch, running reference, values ----
     auto compute_batch = [&](int rb, const Slice *kx, const Slice *vx) {
         float s[RB];
         float mb = m;
@@ -141,11 +139,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
             s[x] = incl ? part : -INFINITY;
             mb = fmaxf(mb, s[x]);
         }
-        const float scale = fast_exp2(m - mb);
-        m = mb;
-        l *= scale;
+        // The running reference m moves only when a logit exceeds it by more than
+        // kSlack (log2 units), so exp2(s - m) <= 2^kSlack stays far inside float32
+        // range; o = acc / l and lse = m + log2(l) hold for any reference, and the
+        // rescale of acc and l is skipped unless some lane of the wave needs it.
+        const bool grow = mb > m + kSlack;
+        if (__builtin_amdgcn_ballot_w64(grow)) {
+            const float mn = grow ? mb : m;
+            const float scale = fast_exp2(m - mn);
+            m = mn;
+            l *= scale;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) acc.c[c] *= scale;
+            for (int c = 0; c < 4; ++c) acc.c[c] *= scale;
+        }
         float p[RB];
 #pragma unroll
         for (int x = 0; x < RB; ++x) {

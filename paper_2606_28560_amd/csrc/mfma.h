@@ -186,24 +186,22 @@ __device__ __forceinline__ void stage_freq(double *dst, const RopeFreq &rf) {
 __device__ __forceinline__ float to_quad(float x, int lane) {
     return __shfl(x, (lane >> 2) + 16 * (lane & 3), 64);
 }
+// A row slice held in the quad layout, moved to the MFMA layout (lane l serves row
+// l % 16 with slice l / 16; quad lanes 4n..4n+3 hold the slices of row n).
+__device__ __forceinline__ Slice slice_from_quad(const Slice &x, int lane) {
+    const int src = 4 * (lane & 15) + (lane >> 4);
+    Slice y;
+    y.a.x = __shfl(x.a.x, src, 64); y.a.y = __shfl(x.a.y, src, 64);
+    y.a.z = __shfl(x.a.z, src, 64); y.a.w = __shfl(x.a.w, src, 64);
+    y.b.x = __shfl(x.b.x, src, 64); y.b.y = __shfl(x.b.y, src, 64);
+    y.b.z = __shfl(x.b.z, src, 64); y.b.w = __shfl(x.b.w, src, 64);
+    return y;
+}
 __device__ __forceinline__ void acc_to_quad(Acc16 &a, int lane) {
 #pragma unroll
     for (int c = 0; c < 4; ++c)
 #pragma unroll
         for (int e = 0; e < 4; ++e) a.c[c][e] = to_quad(a.c[c][e], lane);
-}
-
-// Row-major staging of rows [r_begin, r_begin + nrows) into dst[(row - r_begin) * stride]
-// (zero outside [0, T)); 16-byte coalesced loads and stores.
-__device__ __forceinline__ void stage_rows(uint16_t *dst, int stride, const uint16_t *X, int r_begin,
-                                           int nrows, int T) {
-    for (int c = threadIdx.x; c < nrows * 8; c += blockDim.x) {
-        const int kk = c >> 3, ch = c & 7;
-        const int row = r_begin + kk;
-        uint4 val = make_uint4(0, 0, 0, 0);
-        if (row >= 0 && row < T) val = *reinterpret_cast<const uint4 *>(X + (size_t)row * kD + ch * 8);
-        *reinterpret_cast<uint4 *>(dst + kk * stride + ch * 8) = val;
-    }
 }
 
 __device__ __forceinline__ f32x4 mfma(const bf16x8 &a, const bf16x8 &b, const f32x4 &c) {
@@ -224,32 +222,54 @@ __device__ __forceinline__ int out_dim(int c, int m) {
     return (c < 2 ? 0 : 32) + 8 * (m >> 2) + 4 * (c & 1) + (m & 3);
 }
 
-// Transposed staging of rows [r_begin, r_begin + nrows) of a [*, 64] bf16 matrix into
-// dst[dim * stride + row - r_begin] (zero outside [0, T)).  Each work item reads one
-// 32-bit word (two dims) of four consecutive rows and writes two 8-byte runs.
-// nrows must be a multiple of 4; stride (in bf16) must be a multiple of 4 so that
-// the 8-byte runs are aligned (132 spreads 32 consecutive dim pairs over 16 bank
-// offsets).
-__device__ __forceinline__ void stage_transpose(uint16_t *dst, int stride, const uint16_t *X,
-                                                int r_begin, int nrows, int T) {
-    const int items = (nrows / 4) * 32;
-    for (int u = threadIdx.x; u < items; u += blockDim.x) {
-        const int dp = u & 31;      // dim pair
-        const int rg = u >> 5;      // group of four rows
-        uint32_t a[4];
+// Rows [r_begin, r_begin + NROWS) of a [*, 64] bf16 matrix copied to LDS with
+// direct-to-LDS loads (no registers; completion counts in vmcnt): row-major, 128-byte
+// rows whose 16-byte chunks are XOR-swizzled by the row (chunk c of band row r sits in
+// slot c ^ (r & 7)), so that lanes reading one chunk of consecutive rows spread over
+// the banks.  Rows outside [0, T) are clamped to a valid row: callers mask them.
+// Each wave moves 1 KB (8 rows) per instruction.  256 threads.
+template <int NROWS>
+__device__ __forceinline__ void dma_rows(uint16_t *dst, const uint16_t *X, int r_begin, int T) {
+    static_assert(NROWS % 8 == 0, "whole 1 KB blocks");
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int row = r_begin + 4 * rg + r;
-            a[r] = (row >= 0 && row < T) ? reinterpret_cast<const uint32_t *>(X + (size_t)row * kD)[dp] : 0u;
-        }
-        const uint2 lo = make_uint2(__builtin_amdgcn_perm(a[1], a[0], 0x05040100u),
-                                    __builtin_amdgcn_perm(a[3], a[2], 0x05040100u));
-        const uint2 hi = make_uint2(__builtin_amdgcn_perm(a[1], a[0], 0x07060302u),
-                                    __builtin_amdgcn_perm(a[3], a[2], 0x07060302u));
-        *reinterpret_cast<uint2 *>(dst + (2 * dp) * stride + 4 * rg) = lo;
-        *reinterpret_cast<uint2 *>(dst + (2 * dp + 1) * stride + 4 * rg) = hi;
+    for (int blk = wv; blk < NROWS / 8; blk += 4) {
+        const int rr = 8 * blk + (lane >> 3);
+        const int ch = (lane & 7) ^ (rr & 7);
+        const int row = min(max(r_begin + rr, 0), T - 1);
+        __builtin_amdgcn_global_load_lds(X + (size_t)row * kD + 8 * ch, dst + 512 * blk, 16, 0, 0);
     }
 }
+// Chunk c (dims 8c..8c+7) of band row rr staged by dma_rows.
+__device__ __forceinline__ uint4 dma_chunk(const uint16_t *src, int rr, int c) {
+    return *reinterpret_cast<const uint4 *>(src + rr * kD + 8 * (c ^ (rr & 7)));
+}
+__device__ __forceinline__ Slice dma_slice(const uint16_t *src, int rr, int g) {
+    Slice s;
+    s.a = dma_chunk(src, rr, g);
+    s.b = dma_chunk(src, rr, 4 + g);
+    return s;
+}
+// Element (band row rr, dim d) of rows staged by dma_rows.
+__device__ __forceinline__ uint16_t dma_elem(const uint16_t *src, int rr, int d) {
+    return src[rr * kD + 8 * ((d >> 3) ^ (rr & 7)) + (d & 7)];
+}
+// A operand of a transposed-operand MFMA from rows staged by dma_rows: output dim
+// out_dim(c, n); k index 8g + j is staged row base + 4g + (j & 3) + 16 (j >> 2).
+__device__ __forceinline__ bf16x8 dma_operand_t(const uint16_t *src, int c, int n, int base, int g) {
+    const int d = out_dim(c, n);
+    uint32_t a[4];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int r = base + 16 * h + 4 * g;
+        a[2 * h] = (uint32_t)dma_elem(src, r, d) | ((uint32_t)dma_elem(src, r + 1, d) << 16);
+        a[2 * h + 1] = (uint32_t)dma_elem(src, r + 2, d) | ((uint32_t)dma_elem(src, r + 3, d) << 16);
+    }
+    return as_bf8(make_uint4(a[0], a[1], a[2], a[3]));
+}
+// Waits for this wave's outstanding vector-memory loads, direct-to-LDS ones included.
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // Block index -> work item, keeping consecutive work items (the tiles of one
 // (batch, head)) on one XCD: workgroups are dispatched round-robin over 8 XCDs.
