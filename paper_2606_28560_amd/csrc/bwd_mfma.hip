@@ -12,7 +12,8 @@
 //          r1 of a query is row r0 of the previous query, taken from its lanes),
 //          dq += tau dS ((1-w) k[r0] + w k[r1]) on the VALU,
 //          dalpha partial += f (tau dS <q, k[r1]-k[r0]> + p <dO, v[r1]-v[r0]>);
-//   writes dq, Delta_i = <dO_i, o_i> and one float64 dalpha partial per workgroup.
+//   writes dq, Delta_i = <dO_i, o_i> and one float64 dalpha partial per workgroup
+//   (each query's terms in float32, then float64 across queries).
 // dk/dv kernel (key-stationary, 64 keys per workgroup, 16 per wave): the queries
 // that read key row j are j..j+W (window) and, for rung k, j+floor(d_k) (as row r0,
 // weight 1-w) and j+floor(d_k)+1 (as row r1, weight w):
@@ -64,8 +65,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     const Slice gmm = load_row(G, imc, gm);
     const Slice qq = load_row(Q, ic, gq);
     const Slice gqq = load_row(G, ic, gq);
-    const float delta = quad_sum(dot_slice(gqq, load_slice(o + off + (size_t)ic * kD, gq)));
-    const float delta_m = __shfl(delta, 4 * nm, 64);
+    const Slice oq = load_row(o + off, ic, gq);
     const float lse2 = L[ic] * kLog2e;
     const float lse2_m = L[imc] * kLog2e;
 
@@ -74,14 +74,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 #pragma unroll
     for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && rt.d0[r] <= last) ? 1 : 0;
     nact = __builtin_amdgcn_readfirstlane(nact);  // wave-uniform: scalar branches
-    // x = {k0, v0, k1, v1}: rows r0 and r1 = r0 - 1 of K and V (r1 filled by fill_r1
-    // below when every w == 0)
+    // x = {k0, v0, k1, v1}: rows r0 and r1 = r0 - 1 of K and V.  When every w == 0
+    // only the first query of each 16-lane row (queries t0, t0+4, t0+8, t0+12) loads
+    // its r1 rows here; fill_r1 takes the others from the previous query's lanes.
     auto load_rung = [&](int r, Slice *x) {
         const int R0 = min(max(i - rt.d0[r], 0), T - 1);
         x[0] = load_row(K, R0, gq);
         x[1] = load_row(V, R0, gq);
-        if (INTERP) {
-            const int R1 = max(R0 - 1, 0);
+        if (INTERP || (nq & 3) == 0) {
+            const int R1 = min(max(i - rt.d0[r] - 1, 0), T - 1);
             x[2] = load_row(K, R1, gq);
             x[3] = load_row(V, R1, gq);
         }
@@ -94,6 +95,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     dma_rows<kStage>(kr, K, T0 - 16, T);
     dma_rows<kStage>(vr, V, T0 - 16, T);
     stage_freq(sfreq, rf);
+    // Delta_i = <dO_i, o_i>, once every load of the prologue is in flight
+    const float delta = quad_sum(dot_slice(gqq, oq));
+    const float delta_m = __shfl(delta, 4 * nm, 64);
     wait_vmem();
     __syncthreads();
 
@@ -123,7 +127,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     acc_to_quad(acc, lane);
 
     // rungs (quad layout), two batches in flight; r1 = -1 is the zero row
-    double dal = 0.0;
+    float dal_q = 0.f;  // this query's dalpha terms (float32; summed in float64 below)
     auto compute_rung = [&](int r, const Slice *x) {  // x = {k0, v0, k1, v1}
         const int d0 = rt.d0[r];
         const float w = rt.w[r];
@@ -143,23 +147,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
             acc_axpy2(acc, cc * (1.f - w), x[0], cc * w, x[2]);
         else
             acc_axpy(acc, cc, x[0]);
-        if (gq == 0 && incl) dal += (double)rt.f[r] * (double)(cc * (s1 - s0) + p * (p1 - p0));
+        if (gq == 0 && incl) dal_q += (float)rt.f[r] * (cc * (s1 - s0) + p * (p1 - p0));
     };
-    // with every w == 0 only rows r0 are loaded for all queries: row r1 of query n is
-    // row r0 of query n - 1 (the quad below), and the tile's first query loads its own
-    auto fill_r1 = [&](int r, Slice *x) {
+    // with every w == 0, row r1 of query n is row r0 of query n - 1, four lanes below:
+    // a DPP row shift, which leaves the loaded rows of each 16-lane row's first query
+    auto fill_r1 = [&](Slice *x) {
         if (!INTERP) {
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 uint32_t *d = reinterpret_cast<uint32_t *>(&x[2 + h]);
                 const uint32_t *src = reinterpret_cast<const uint32_t *>(&x[h]);
 #pragma unroll
-                for (int u = 0; u < 8; ++u) d[u] = (uint32_t)__shfl((int)src[u], (lane - 4) & 63, 64);
-            }
-            if (nq == 0) {
-                const int R1 = min(max(i - rt.d0[r] - 1, 0), T - 1);
-                x[2] = load_row(K, R1, gq);
-                x[3] = load_row(V, R1, gq);
+                for (int u = 0; u < 8; ++u)
+                    d[u] = (uint32_t)__builtin_amdgcn_update_dpp((int)d[u], (int)src[u], 0x114, 0xF, 0xF, false);
             }
         }
     };
@@ -167,11 +167,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     for (int rb = 0; rb < kMaxRungs; rb += 2) {
         if (rb < nact) {
             if (rb + 1 < nact) load_rung(rb + 1, xB);
-            fill_r1(rb, xA);
+            fill_r1(xA);
             compute_rung(rb, xA);
             if (rb + 1 < nact) {
                 if (rb + 2 < nact) load_rung(rb + 2, xA);
-                fill_r1(rb + 1, xB);
+                fill_r1(xB);
                 compute_rung(rb + 1, xB);
             }
         }
@@ -183,6 +183,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         if (gq == 0) delta_out[(size_t)bh * T + i] = delta;
     }
     // workgroup dalpha partial: wave sums, then the four waves in order
+    double dal = (double)dal_q;
 #pragma unroll
     for (int st = 32; st >= 1; st >>= 1) dal += __shfl_xor(dal, st, 64);
     if (lane == 0) red[wv] = dal;
@@ -201,6 +202,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
     __shared__ double sfreq[32];
     __shared__ __align__(16) uint16_t qr[kStage * kD];
     __shared__ __align__(16) uint16_t gr[kStage * kD];
+    __shared__ __align__(16) uint16_t kown[kBwdB * kD];  // the tile's own K, V rows
+    __shared__ __align__(16) uint16_t vown[kBwdB * kD];
     __shared__ float sl[kStage], sd[kStage];
     __shared__ double red[256];
 
@@ -236,10 +239,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
     const int t0 = T0 + 16 * wv;
     const int jm = t0 + nm, jmc = min(jm, T - 1);  // MFMA layout key
     const int j = t0 + nq, jc = min(j, T - 1);     // quad layout key
-    const Slice km = load_row(K, jmc, gm);
-    const Slice vm = load_row(V, jmc, gm);
-    const Slice ks = load_row(K, jc, gq);
-    const Slice vs = load_row(V, jc, gq);
 
     // rungs: some key of this wave has j + floor(d) < T for a prefix of the table
     int nact = 0;
@@ -255,24 +254,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
         x[2] = load_row(Q, i1c, gq);
         x[3] = load_row(G, i1c, gq);
     };
-    auto load_pair = [&](int rb, Slice *x) {
-        const int ia = min(j + rt.d0[rb], T - 1);
-        const int ib = min(j + rt.d0[rb + 1], T - 1);
-        x[0] = load_row(Q, ia, gq);
-        x[1] = load_row(G, ia, gq);
-        x[2] = load_row(Q, ib, gq);
-        x[3] = load_row(G, ib, gq);
+    // two rungs' query rows (q, dO) with their lse (log2 units) and Delta
+    struct Pair {
+        Slice x[4];  // q0a, g0a, q0b, g0b
+        float le[2], de[2];
+    };
+    auto load_pair = [&](int rb, Pair &pr) {
+#pragma unroll
+        for (int y = 0; y < 2; ++y) {
+            const int ic = min(j + rt.d0[rb + y], T - 1);
+            pr.x[2 * y] = load_row(Q, ic, gq);
+            pr.x[2 * y + 1] = load_row(G, ic, gq);
+            pr.le[y] = L[ic] * kLog2e;
+            pr.de[y] = Dl[ic];
+        }
     };
     Slice xA[4], xB[4];
+    Pair pA;
     if (0 < nact) {  // in flight during the band phase
         if (INTERP) load_rung(0, xA);
-        else load_pair(0, xA);
+        else load_pair(0, pA);
     }
 
     // q and dO rows, lse and Delta of queries [T0, T0+80) (rows past the end are
     // clamped copies, masked below)
     dma_rows<kStage>(qr, Q, T0, T);
     dma_rows<kStage>(gr, G, T0, T);
+    dma_rows<kBwdB>(kown, K, T0, T);  // rows past the end are clamped copies, never stored
+    dma_rows<kBwdB>(vown, V, T0, T);
     for (int c = threadIdx.x; c < kStage; c += 256) {
         const int row = T0 + c;
         sl[c] = row < T ? L[row] * kLog2e : 0.f;
@@ -283,6 +292,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
     __syncthreads();
 
     // band (MFMA layout): queries [t0, t0 + 32) in two blocks
+    const Slice km = dma_slice(kown, 16 * wv + nm, gm);
+    const Slice vm = dma_slice(vown, 16 * wv + nm, gm);
     uint32_t cw[4], pw[4];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
@@ -314,30 +325,30 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
     acc_to_quad(adk, lane);
     acc_to_quad(adv, lane);
 
+    const Slice ks = dma_slice(kown, 16 * wv + nq, gq);  // this key's K, V rows (quad layout)
+    const Slice vs = dma_slice(vown, 16 * wv + nq, gq);
     if (!INTERP) {
-        // every w == 0: query j + d0 reads this row with weight 1; two rungs per batch,
-        // two batches in flight
-        auto compute_pair = [&](int rb, const Slice *x) {  // x = {q0a, g0a, q0b, g0b}
+        // every w == 0: query j + d0 reads this row with weight 1; two rungs per batch
+        auto compute_pair = [&](int rb, const Pair &pr) {
             float cc[2], pp[2];
 #pragma unroll
             for (int y = 0; y < 2; ++y) {
                 const int i0 = j + rt.d0[rb + y];
-                const int i0c = min(i0, T - 1);
                 const bool in0 = rb + y < nact && j < T && i0 < T;
-                const float sc = quad_sum(dot_slice(x[2 * y], ks));
-                const float dp = quad_sum(dot_slice(x[2 * y + 1], vs));
-                pp[y] = in0 ? fast_exp2(sc * sl2 - L[i0c] * kLog2e) : 0.f;
-                cc[y] = tau * pp[y] * (dp - Dl[i0c]);
+                const float sc = quad_sum(dot_slice(pr.x[2 * y], ks));
+                const float dp = quad_sum(dot_slice(pr.x[2 * y + 1], vs));
+                pp[y] = in0 ? fast_exp2(sc * sl2 - pr.le[y]) : 0.f;
+                cc[y] = tau * pp[y] * (dp - pr.de[y]);
             }
-            acc_axpy2(adk, cc[0], x[0], cc[1], x[2]);
-            acc_axpy2(adv, pp[0], x[1], pp[1], x[3]);
+            acc_axpy2(adk, cc[0], pr.x[0], cc[1], pr.x[2]);
+            acc_axpy2(adv, pp[0], pr.x[1], pp[1], pr.x[3]);
         };
-        // one batch in flight: the register budget keeps four waves per SIMD resident
+        // one pair in flight (register budget: four waves per SIMD)
 #pragma unroll
         for (int rb = 0; rb < kMaxRungs; rb += 2) {
             if (rb < nact) {
-                if (rb > 0) load_pair(rb, xA);
-                compute_pair(rb, xA);
+                if (rb > 0) load_pair(rb, pA);
+                compute_pair(rb, pA);
             }
         }
     } else {

@@ -100,9 +100,9 @@ __device__ __forceinline__ float max4(float x) {
 // lanes 4n .. 4n+3 share row n, lane 4n+g holding slice g of it, so the four lanes
 // of a row read 64 contiguous bytes per load instruction.  Sums over a quad use DPP
 // lane swaps (quad_perm [1,0,3,2] then [2,3,0,1]); every lane must be active.
-__device__ __forceinline__ float quad_sum(float x) {
-    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, false));
-    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xF, 0xF, false));
+__device__ __forceinline__ float quad_sum(float x) {  // folds into two v_add_f32_dpp
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, true));
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, true));
     return x;
 }
 
