@@ -193,7 +193,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 
 // ---------------------------------------------------------------------------
 template <bool INTERP>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 : 4))) void bwd_dkdv_bf16_d64_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void bwd_dkdv_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const float *__restrict__ lse, const uint16_t *__restrict__ dO, const float *__restrict__ delta_in,
     uint16_t *__restrict__ dk, uint16_t *__restrict__ dv, const double *__restrict__ partials,
@@ -202,10 +202,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
     __shared__ double sfreq[32];
     __shared__ __align__(16) uint16_t qr[kStage * kD];
     __shared__ __align__(16) uint16_t gr[kStage * kD];
-    __shared__ __align__(16) uint16_t kown[kBwdB * kD];  // the tile's own K, V rows
-    __shared__ __align__(16) uint16_t vown[kBwdB * kD];
+    // the tile's own K, V rows [T0 - kLead, T0 - kLead + kOwn): with interpolation also
+    // the neighbours j-1 and j+1 of every key j
+    constexpr int kLead = INTERP ? 4 : 0;
+    constexpr int kOwn = INTERP ? kBwdB + 8 : kBwdB;
+    __shared__ __align__(16) uint16_t kown[kOwn * kD];
+    __shared__ __align__(16) uint16_t vown[kOwn * kD];
     __shared__ float sl[kStage], sd[kStage];
-    __shared__ double red[256];
 
     const int lane = threadIdx.x & 63;
     const int wv = threadIdx.x >> 6;
@@ -223,8 +226,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
     const float *Dl = delta_in + (size_t)bh * T;
     const float sl2 = tau * kLog2e;
 
-    // final dalpha: the dq kernel has completed on this stream
+    // final dalpha: the dq kernel has completed on this stream (the reduction borrows
+    // kown before its rows are loaded)
     if (blockIdx.x == 0) {
+        double *red = reinterpret_cast<double *>(kown);
         double s = 0.0;
         for (int t = threadIdx.x; t < n_partials; t += 256) s += partials[t];
         red[threadIdx.x] = s;
@@ -234,25 +239,33 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
             __syncthreads();
         }
         if (threadIdx.x == 0) *dalpha = (float)red[0];
+        __syncthreads();
     }
 
     const int t0 = T0 + 16 * wv;
-    const int jm = t0 + nm, jmc = min(jm, T - 1);  // MFMA layout key
-    const int j = t0 + nq, jc = min(j, T - 1);     // quad layout key
+    const int jm = t0 + nm;  // MFMA layout key
+    const int j = t0 + nq;   // quad layout key
 
     // rungs: some key of this wave has j + floor(d) < T for a prefix of the table
     int nact = 0;
 #pragma unroll
     for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && t0 + rt.d0[r] < T) ? 1 : 0;
     nact = __builtin_amdgcn_readfirstlane(nact);  // wave-uniform: scalar branches
-    // rows of query i0 = j + d0 (and i0 + 1 when interpolating) for a rung
-    auto load_rung = [&](int r, Slice *x) {
-        const int i0c = min(j + rt.d0[r], T - 1);
-        const int i1c = min(j + rt.d0[r] + 1, T - 1);
-        x[0] = load_row(Q, i0c, gq);
-        x[1] = load_row(G, i0c, gq);
-        x[2] = load_row(Q, i1c, gq);
-        x[3] = load_row(G, i1c, gq);
+    // one interpolated rung: the rows (q, dO) of queries i0 = j + floor(d) and i0 + 1
+    // with their lse (log2 units) and Delta
+    struct Rung {
+        Slice x[4];  // q0, g0 (query i0), q1, g1 (query i0 + 1)
+        float le[2], de[2];
+    };
+    auto load_rung = [&](int r, Rung &ru) {
+#pragma unroll
+        for (int y = 0; y < 2; ++y) {
+            const int ic = min(j + rt.d0[r] + y, T - 1);
+            ru.x[2 * y] = load_row(Q, ic, gq);
+            ru.x[2 * y + 1] = load_row(G, ic, gq);
+            ru.le[y] = L[ic] * kLog2e;
+            ru.de[y] = Dl[ic];
+        }
     };
     // two rungs' query rows (q, dO) with their lse (log2 units) and Delta
     struct Pair {
@@ -269,10 +282,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
             pr.de[y] = Dl[ic];
         }
     };
-    Slice xA[4], xB[4];
     Pair pA;
+    Rung ru;
     if (0 < nact) {  // in flight during the band phase
-        if (INTERP) load_rung(0, xA);
+        if (INTERP) load_rung(0, ru);
         else load_pair(0, pA);
     }
 
@@ -280,8 +293,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
     // clamped copies, masked below)
     dma_rows<kStage>(qr, Q, T0, T);
     dma_rows<kStage>(gr, G, T0, T);
-    dma_rows<kBwdB>(kown, K, T0, T);  // rows past the end are clamped copies, never stored
-    dma_rows<kBwdB>(vown, V, T0, T);
+    dma_rows<kOwn>(kown, K, T0 - kLead, T);  // rows outside [0, T) are clamped copies
+    dma_rows<kOwn>(vown, V, T0 - kLead, T);
     for (int c = threadIdx.x; c < kStage; c += 256) {
         const int row = T0 + c;
         sl[c] = row < T ? L[row] * kLog2e : 0.f;
@@ -292,8 +305,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
     __syncthreads();
 
     // band (MFMA layout): queries [t0, t0 + 32) in two blocks
-    const Slice km = dma_slice(kown, 16 * wv + nm, gm);
-    const Slice vm = dma_slice(vown, 16 * wv + nm, gm);
+    const Slice km = dma_slice(kown, kLead + 16 * wv + nm, gm);
+    const Slice vm = dma_slice(vown, kLead + 16 * wv + nm, gm);
     uint32_t cw[4], pw[4];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
@@ -325,9 +338,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
     acc_to_quad(adk, lane);
     acc_to_quad(adv, lane);
 
-    const Slice ks = dma_slice(kown, 16 * wv + nq, gq);  // this key's K, V rows (quad layout)
-    const Slice vs = dma_slice(vown, 16 * wv + nq, gq);
+    const int jo = kLead + 16 * wv + nq;  // this key's row in kown / vown (quad layout)
     if (!INTERP) {
+        const Slice ks = dma_slice(kown, jo, gq);
+        const Slice vs = dma_slice(vown, jo, gq);
         // every w == 0: query j + d0 reads this row with weight 1; two rungs per batch
         auto compute_pair = [&](int rb, const Pair &pr) {
             float cc[2], pp[2];
@@ -352,43 +366,42 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(INTERP ? 2 
             }
         }
     } else {
-        // neighbours j-1 and j+1 are shared by every rung
-        const int jmn = min(max(j - 1, 0), T - 1);
-        const int jpn = min(j + 1, T - 1);
-        const Slice kmn = load_row(K, jmn, gq);
-        const Slice vmn = load_row(V, jmn, gq);
-        const Slice kpn = load_row(K, jpn, gq);
-        const Slice vpn = load_row(V, jpn, gq);
-        auto compute_rung = [&](int r, const Slice *x) {  // x = {q0, g0, q1, g1}
+        // query i0 = j + floor(d) reads this row as r0 (weight 1 - w) and row j-1 as
+        // r1; query i0 + 1 reads row j+1 as r0 and this row as r1 (weight w).  One
+        // rung in flight (register budget: four waves per SIMD); rows j-1, j, j+1
+        // come from kown / vown.
+        auto compute_rung = [&](int r, const Rung &ru) {
             const float w = rt.w[r];
-            // query i0 = j + d0 reads this row as r0 (weight 1 - w) and j-1 as r1
             const int i0 = j + rt.d0[r];
             const bool in0 = r < nact && j < T && i0 < T && (w == 0.f || j >= 1);
-            const int i0c = min(i0, T - 1);
-            const float sa = quad_sum((1.f - w) * dot_slice(x[0], ks) + w * dot_slice(x[0], kmn));
-            const float da = quad_sum((1.f - w) * dot_slice(x[1], vs) + w * dot_slice(x[1], vmn));
-            const float pa = in0 ? fast_exp2(sa * sl2 - L[i0c] * kLog2e) : 0.f;
-            const float ca = tau * pa * (da - Dl[i0c]);
-            // query i1 = i0 + 1 reads row j+1 as r0 and this row as r1 (weight w)
-            const int i1 = i0 + 1;
-            const bool in1 = r < nact && j < T && i1 < T && w != 0.f;
-            const int i1c = min(i1, T - 1);
-            const float sb = quad_sum((1.f - w) * dot_slice(x[2], kpn) + w * dot_slice(x[2], ks));
-            const float db = quad_sum((1.f - w) * dot_slice(x[3], vpn) + w * dot_slice(x[3], vs));
-            const float pb = in1 ? fast_exp2(sb * sl2 - L[i1c] * kLog2e) : 0.f;
-            const float cb = tau * pb * (db - Dl[i1c]);
-            acc_axpy2(adk, (1.f - w) * ca, x[0], w * cb, x[2]);
-            acc_axpy2(adv, (1.f - w) * pa, x[1], w * pb, x[3]);
+            const bool in1 = r < nact && j < T && i0 + 1 < T && w != 0.f;
+            float sa, sb, da, db;
+            {
+                const Slice kj = dma_slice(kown, jo, gq);
+                const Slice kl = dma_slice(kown, jo - 1, gq);
+                const Slice kh = dma_slice(kown, jo + 1, gq);
+                sa = quad_sum((1.f - w) * dot_slice(ru.x[0], kj) + w * dot_slice(ru.x[0], kl));
+                sb = quad_sum((1.f - w) * dot_slice(ru.x[2], kh) + w * dot_slice(ru.x[2], kj));
+            }
+            {
+                const Slice vj = dma_slice(vown, jo, gq);
+                const Slice vl = dma_slice(vown, jo - 1, gq);
+                const Slice vh = dma_slice(vown, jo + 1, gq);
+                da = quad_sum((1.f - w) * dot_slice(ru.x[1], vj) + w * dot_slice(ru.x[1], vl));
+                db = quad_sum((1.f - w) * dot_slice(ru.x[3], vh) + w * dot_slice(ru.x[3], vj));
+            }
+            const float pa = in0 ? fast_exp2(sa * sl2 - ru.le[0]) : 0.f;
+            const float ca = tau * pa * (da - ru.de[0]);
+            const float pb = in1 ? fast_exp2(sb * sl2 - ru.le[1]) : 0.f;
+            const float cb = tau * pb * (db - ru.de[1]);
+            acc_axpy2(adk, (1.f - w) * ca, ru.x[0], w * cb, ru.x[2]);
+            acc_axpy2(adv, (1.f - w) * pa, ru.x[1], w * pb, ru.x[3]);
         };
 #pragma unroll
-        for (int rb = 0; rb < kMaxRungs; rb += 2) {
-            if (rb < nact) {
-                if (rb + 1 < nact) load_rung(rb + 1, xB);
-                compute_rung(rb, xA);
-                if (rb + 1 < nact) {
-                    if (rb + 2 < nact) load_rung(rb + 2, xA);
-                    compute_rung(rb + 1, xB);
-                }
+        for (int r = 0; r < kMaxRungs; ++r) {
+            if (r < nact) {
+                if (r > 0) load_rung(r, ru);
+                compute_rung(r, ru);
             }
         }
     }
