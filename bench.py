@@ -53,15 +53,15 @@ def parse_args():
 #   bench.py --eager --steps 10 --warmup 2 --no-cpu-baseline --no-t4096 --copy-probe-mb 256
 # each scaled by what the same counter reads for the plain 256 MiB device copy of that run.
 # They hold only for the kernel sources they were taken on (COUNTER_SOURCES_SHA).
-COUNTER_SOURCES_SHA = "6ed9aa1b7097cf75350ec0e557b525d1bece916cd755925459842a6fb30b9dca"
+COUNTER_SOURCES_SHA = "48d5a1fc26296c3d0374fd8a9595362bd55b05fa28fe38d05e0ec492ba7577e9"
 COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
 COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
-    "forward": (12376.2, 8448.0),
-    "bwd_dq": (20774.0, 8480.4),
-    "bwd_dkdv": (16787.8, 16384.0),
+    "forward": (12402.1, 8448.0),
+    "bwd_dq": (20779.1, 8480.1),
+    "bwd_dkdv": (17457.4, 16384.0),
     "rope": (8212.2, 16384.0),
 }
-COPY_PROBE_KIB = (262144.0, 131093.2, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
+COPY_PROBE_KIB = (262144.0, 131093.1, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
 
 
 def kernel_sources_sha() -> str:
@@ -234,8 +234,11 @@ def t4096_figure(steps: int, warmup: int, eager: bool):
     ms, _ = timed(run, steps, warmup)
     msf, _ = timed(fwd, steps, warmup)
     qh = wl.queries_heads
+    from paper_2606_28560_amd import fibattn as F
+    kt = {k: round(kernel_time(F, sets, k, steps, 1)[0], 6) for k in ("forward", "bwd_dq", "bwd_dkdv", "rope")}
     return {"workload": wl.name, "alpha": float(call.alpha), "ms_per_step": ms,
-            "value": qh / (ms * 1e-3), "fwd_only_ms": msf, "fwd_only_value": qh / (msf * 1e-3)}
+            "value": qh / (ms * 1e-3), "fwd_only_ms": msf, "fwd_only_value": qh / (msf * 1e-3),
+            "kernels_mean_ms": kt}
 
 
 def main():
