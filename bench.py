@@ -43,6 +43,8 @@ def parse_args():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the oracle sample")
     p.add_argument("--no-t4096", action="store_true", help="skip the T=4096 figure")
+    p.add_argument("--no-integer-offsets", action="store_true",
+                   help="skip the continuous vs rounded-offset stagger figure")
     p.add_argument("--copy-probe-mb", type=int, default=0,
                    help="also run one plain device copy of this many MiB (counter calibration)")
     return p.parse_args()
@@ -241,6 +243,37 @@ def t4096_figure(steps: int, warmup: int, eager: bool):
             "kernels_mean_ms": kt}
 
 
+def integer_offsets_figure(steps: int, warmup: int, eager: bool, layer: int = 3):
+    """Attention forward + backward of a static-stagger layer (B=16, H=8, T=1024, W=8)
+    on continuous offsets alpha * f (interpolated) and on the same offsets rounded to
+    integers (one row per rung)."""
+    import dataclasses
+
+    import numpy as np
+
+    from paper_2606_28560_amd import schedules, workloads
+
+    wl = workloads.workload("stagger16_T1024")
+    call = next(c for c in wl.calls if c.W == 8 and c.layer == layer)
+    rounded = dataclasses.replace(call, base=schedules.integer_base(call.alpha, call.base),
+                                  alpha=np.float32(1.0))
+    out = {"workload": wl.name, "layer": layer, "alpha": float(call.alpha)}
+    for tag, c in (("continuous", call), ("integer", rounded)):
+        from paper_2606_28560_amd import fibattn as F
+        sets = [Step(wl, c, i) for i in range(3)]
+        if eager:
+            run = lambda i: attn_one(F, sets[i % len(sets)])  # noqa: E731
+        else:
+            gs = [capture(lambda st=st: attn_one(F, st)) for st in sets]
+            run = lambda i: gs[i % len(gs)].replay()  # noqa: E731
+        ms, _ = timed(run, steps, warmup)
+        out[tag + "_ms"] = ms
+        out[tag + "_value"] = wl.queries_heads / (ms * 1e-3)
+        del sets
+    out["integer_speedup"] = out["continuous_ms"] / out["integer_ms"]
+    return out
+
+
 def main():
     args = parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -321,6 +354,8 @@ def main():
     }
     if not args.no_t4096:
         result["t4096"] = t4096_figure(max(5, args.steps // 4), 2, args.eager)
+    if not args.no_integer_offsets:
+        result["integer_offsets"] = integer_offsets_figure(max(5, args.steps // 4), 2, args.eager)
     if args.copy_probe_mb:
         a = torch.empty(args.copy_probe_mb * 2**20, dtype=torch.uint8, device="cuda")
         b = torch.empty_like(a)

@@ -45,3 +45,16 @@ def alpha_coprime_stagger(L: int = 16, S: int = 7) -> np.ndarray:
     lin = np.arange(L, dtype=np.float64)
     src = (S * np.arange(L)) % L
     return (0.5 + lin[src] / (L - 1)).astype(np.float32)
+
+
+def integer_base(alpha, base) -> tuple:
+    """Static offsets rounded to integers, as a base table for alpha = 1.
+
+    Section 2 runs the static schedules on integer offsets (a boolean mask) without
+    giving the rounding rule.  The reading taken here: d_k = fl32(alpha * f_k) (the
+    float32 product every rung table uses), rounded half to even, dropping 0 and
+    repeats.  Passing the result with alpha = 1 selects the integer-offset kernels,
+    which never read a second row."""
+    a = np.float32(alpha)
+    d = np.rint(np.asarray(base, dtype=np.float32) * a).astype(np.int64)
+    return tuple(int(x) for x in np.unique(d[d > 0]))

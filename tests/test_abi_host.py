@@ -59,6 +59,30 @@ def test_stagger_float32_floor_cases():
     assert tab[610] == (427, 0.0)
 
 
+def test_integer_base_rounds_half_to_even():
+    # alpha = 0.5 by hand: 0.5 f = 0.5, 1, 1.5, 2.5, 4, 6.5, 10.5, 17, 27.5, 44.5, 72,
+    # 116.5, 188.5, 305, 493.5 -> half to even 0, 1, 2, 2, 4, 6, 10, 17, 28, 44, 72,
+    # 116, 188, 305, 494; 0 and the repeated 2 dropped
+    assert schedules.integer_base(0.5, schedules.FIB15) == (
+        1, 2, 4, 6, 10, 17, 28, 44, 72, 116, 188, 305, 494)
+    assert schedules.integer_base(1.0, schedules.FIB15) == schedules.FIB15
+    assert schedules.integer_base(2.0, schedules.POW2_11) == tuple(1 << j for j in range(1, 12))
+
+
+@pytest.mark.parametrize("layer", [0, 3, 7, 11, 15])
+def test_integer_base_gives_integer_rungs(layer):
+    # a pre-rounded base with alpha = 1 is the integer path: every weight 0, every
+    # distance one of the rounded offsets beyond the window, equal to the oracle's
+    a = schedules.alpha_linear_stagger(16)[layer]
+    base = schedules.integer_base(a, schedules.FIB15)
+    assert all(b2 > b1 for b1, b2 in zip(base, base[1:])) and base[0] >= 1
+    lib_tab = F.fibattn_rung_table(1.0, base, 8)
+    assert all(w == 0.0 for _, w, _ in lib_tab)
+    assert [d0 for d0, _, _ in lib_tab] == [b for b in base if b > 8]
+    ref = oracle.rungs(1.0, base, 8)
+    assert [(int(r[0]), float(r[1]), int(r[2])) for r in ref] == [(d, w, f) for d, w, f in lib_tab]
+
+
 def test_rung_table_rejects_bad_input():
     for alpha, base in ((0.0, [1, 2]), (-1.0, [1]), (float("nan"), [1]), (1.0, [2, 2]),
                         (1.0, [0, 3]), (1.0, list(range(1, 40)))):

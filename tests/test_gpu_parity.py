@@ -80,6 +80,20 @@ def test_full_size_parity(wl, ci):
     print(rep, flush=True)
 
 
+@pytest.mark.parametrize("layer", [3, 11])
+def test_integer_offsets_from_rounded_base(layer):
+    # static stagger on integer offsets: the rounded base with alpha = 1 runs the
+    # kernels that read one row per rung; the oracle gets the same table
+    wl = workloads.workload("stagger16_T1024")
+    a = schedules.alpha_linear_stagger(16)[layer]
+    base = schedules.integer_base(a, FIB)
+    print(f"integer offsets: layer {layer} alpha {float(a):.7f} base {base}", flush=True)
+    x = inputs.attention_inputs(4, wl.H, wl.T, wl.D, wl.dtype, wl.case, 200 + layer)
+    got = gpu_run(x["q"], x["k"], x["v"], x["dO"], 8, base, 1.0)
+    ref = oracle_run(x["q"], x["k"], x["v"], x["dO"], 8, base, 1.0)
+    compare(got, ref, wl.dtype, f"integer offsets layer {layer}")
+
+
 def test_backward_at_extrapolation_length():
     # the T = 4096 workload is forward-only; the backward at that shape is checked too
     wl = workloads.workload("extrap_coprime16_T4096")
