@@ -34,13 +34,13 @@ def _load():
     i, f, d = ctypes.c_int, ctypes.c_float, ctypes.c_double
     lib.oracle_rungs.argtypes = [f, _ip, i, i, _ip, _fp, _ip, _fp]
     lib.oracle_rungs.restype = i
-    lib.oracle_forward.argtypes = [i, i, i, i, i, _ip, i, f, _dp, _dp, _dp, _dp, _dp]
+    lib.oracle_forward.argtypes = [i, i, i, i, i, i, _ip, i, f, _dp, _dp, _dp, _dp, _dp]
     lib.oracle_forward.restype = i
-    lib.oracle_backward.argtypes = [i, i, i, i, i, _ip, i, f, _dp, _dp, _dp, _dp, _dp, _dp, _dp, _dp, _dp]
+    lib.oracle_backward.argtypes = [i, i, i, i, i, i, _ip, i, f, _dp, _dp, _dp, _dp, _dp, _dp, _dp, _dp, _dp]
     lib.oracle_backward.restype = i
-    lib.oracle_forward_table.argtypes = [i, i, i, i, i, i, _ip, _dp, _ip, _dp, _dp, _dp, _dp, _dp]
+    lib.oracle_forward_table.argtypes = [i, i, i, i, i, i, i, _ip, _dp, _ip, _dp, _dp, _dp, _dp, _dp]
     lib.oracle_forward_table.restype = None
-    lib.oracle_backward_table.argtypes = [i, i, i, i, i, i, _ip, _dp, _ip, _dp, _dp, _dp, _dp, _dp, _dp, _dp, _dp, _dp]
+    lib.oracle_backward_table.argtypes = [i, i, i, i, i, i, i, _ip, _dp, _ip, _dp, _dp, _dp, _dp, _dp, _dp, _dp, _dp, _dp]
     lib.oracle_backward_table.restype = None
     lib.oracle_rope.argtypes = [i, i, i, i, d, i, _dp, _dp]
     lib.oracle_rope.restype = None
@@ -64,6 +64,14 @@ def _base(base) -> np.ndarray:
     return np.ascontiguousarray(np.asarray(base, dtype=np.int32).reshape(-1))
 
 
+def _heads(q, k):
+    """(B, H, Hkv, T, D) of q [B, H, T, D] and k [B, Hkv, T, D], H a multiple of Hkv."""
+    B, H, T, D = q.shape
+    if k.ndim != 4 or k.shape[0] != B or k.shape[2:] != (T, D) or k.shape[1] < 1 or H % k.shape[1]:
+        raise ValueError(f"k shape {k.shape} does not group q shape {q.shape}")
+    return B, H, k.shape[1], T, D
+
+
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
 
@@ -83,14 +91,15 @@ def rungs(alpha: float, base, W: int):
 
 
 def forward(q, k, v, W: int, base, alpha: float):
-    """o [B,H,T,D] and lse [B,H,T] in float64 (Section 2)."""
+    """o [B,H,T,D] and lse [B,H,T] in float64 (Section 2); k, v may have fewer heads
+    (grouped heads: [B,Hkv,T,D])."""
     lib = _load()
     q, k, v = _f64(q), _f64(k), _f64(v)
-    B, H, T, D = q.shape
+    B, H, Hkv, T, D = _heads(q, k)
     b = _base(base)
     o = np.empty_like(q)
     lse = np.empty((B, H, T), np.float64)
-    rc = lib.oracle_forward(B, H, T, D, W, _ptr(b, _ip), b.size, ctypes.c_float(np.float32(alpha)),
+    rc = lib.oracle_forward(B, H, Hkv, T, D, W, _ptr(b, _ip), b.size, ctypes.c_float(np.float32(alpha)),
                             _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse))
     if rc != 0:
         raise ValueError("bad oracle input")
@@ -98,14 +107,15 @@ def forward(q, k, v, W: int, base, alpha: float):
 
 
 def backward(q, k, v, dO, W: int, base, alpha: float):
-    """dq, dk, dv (float64 [B,H,T,D]), dalpha and the L1 mass of its terms."""
+    """dq [B,H,T,D], dk, dv (shaped like k, v), dalpha and the L1 mass of its terms,
+    in float64."""
     lib = _load()
     q, k, v, dO = _f64(q), _f64(k), _f64(v), _f64(dO)
-    B, H, T, D = q.shape
+    B, H, Hkv, T, D = _heads(q, k)
     b = _base(base)
-    dq = np.empty_like(q); dk = np.empty_like(q); dv = np.empty_like(q)
+    dq = np.empty_like(q); dk = np.empty_like(k); dv = np.empty_like(k)
     da = ctypes.c_double(0.0); l1 = ctypes.c_double(0.0)
-    rc = lib.oracle_backward(B, H, T, D, W, _ptr(b, _ip), b.size, ctypes.c_float(np.float32(alpha)),
+    rc = lib.oracle_backward(B, H, Hkv, T, D, W, _ptr(b, _ip), b.size, ctypes.c_float(np.float32(alpha)),
                              _ptr(q), _ptr(k), _ptr(v), _ptr(dO), _ptr(dq), _ptr(dk), _ptr(dv),
                              ctypes.byref(da), ctypes.byref(l1))
     if rc != 0:
@@ -117,11 +127,11 @@ def forward_table(q, k, v, W: int, d0, w, f):
     """Forward on an explicit rung table (w in float64); used for finite differences in alpha."""
     lib = _load()
     q, k, v = _f64(q), _f64(k), _f64(v)
-    B, H, T, D = q.shape
+    B, H, Hkv, T, D = _heads(q, k)
     d0 = _base(d0); f = _base(f); w = np.ascontiguousarray(w, np.float64)
     o = np.empty_like(q)
     lse = np.empty((B, H, T), np.float64)
-    lib.oracle_forward_table(B, H, T, D, W, d0.size, _ptr(d0, _ip), _ptr(w), _ptr(f, _ip),
+    lib.oracle_forward_table(B, H, Hkv, T, D, W, d0.size, _ptr(d0, _ip), _ptr(w), _ptr(f, _ip),
                              _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse))
     return o, lse
 
@@ -129,11 +139,11 @@ def forward_table(q, k, v, W: int, d0, w, f):
 def backward_table(q, k, v, dO, W: int, d0, w, f):
     lib = _load()
     q, k, v, dO = _f64(q), _f64(k), _f64(v), _f64(dO)
-    B, H, T, D = q.shape
+    B, H, Hkv, T, D = _heads(q, k)
     d0 = _base(d0); f = _base(f); w = np.ascontiguousarray(w, np.float64)
-    dq = np.empty_like(q); dk = np.empty_like(q); dv = np.empty_like(q)
+    dq = np.empty_like(q); dk = np.empty_like(k); dv = np.empty_like(k)
     da = ctypes.c_double(0.0); l1 = ctypes.c_double(0.0)
-    lib.oracle_backward_table(B, H, T, D, W, d0.size, _ptr(d0, _ip), _ptr(w), _ptr(f, _ip),
+    lib.oracle_backward_table(B, H, Hkv, T, D, W, d0.size, _ptr(d0, _ip), _ptr(w), _ptr(f, _ip),
                               _ptr(q), _ptr(k), _ptr(v), _ptr(dO), _ptr(dq), _ptr(dk), _ptr(dv),
                               ctypes.byref(da), ctypes.byref(l1))
     return dq, dk, dv, da.value, l1.value

@@ -35,8 +35,14 @@
  * true positions before gathering): rotate-half pairing (j, j + D/2) with inverse
  * frequency base^(-2j/D); angles in float64.
  *
- * Tensors are [B, H, T, D] float64, C-contiguous.  Work is split over (b, h) with
- * OpenMP; each (b, h) is independent, so results do not depend on thread count.
+ * Grouped key/value heads (Section 3 "Model and training": 8 query heads share 2
+ * key/value heads): q, o, dO, dq are [B, H, T, D], k, v, dk, dv are [B, Hkv, T, D]
+ * with H a multiple of Hkv; query head h reads key/value head h / (H / Hkv), and
+ * dk, dv sum the contributions of the H / Hkv query heads of the group.
+ *
+ * Tensors are float64, C-contiguous.  Work is split with OpenMP over (b, h) in the
+ * forward and over (b, key/value head) in the backward, each unit written by one
+ * thread in a fixed order, so results do not depend on the thread count.
  */
 #include <math.h>
 #include <stdlib.h>
@@ -126,13 +132,14 @@ static double dot_row(const double *x, const double *M, int r, int D)
 /* Forward on an explicit rung table (w in float64).                          */
 /* ------------------------------------------------------------------------- */
 
-void oracle_forward_table(int B, int H, int T, int D, int W,
+void oracle_forward_table(int B, int H, int Hkv, int T, int D, int W,
                           int n, const int *d0, const double *w, const int *f,
                           const double *q, const double *k, const double *v,
                           double *o, double *lse)
 {
     const double tau = 1.0 / sqrt((double)D);
     const int BH = B * H;
+    const int G = H / Hkv;  /* query heads per key/value head */
 #pragma omp parallel
     {
         entry_t *e = (entry_t *)malloc(sizeof(entry_t) * (size_t)(W + 1 + n));
@@ -140,7 +147,8 @@ void oracle_forward_table(int B, int H, int T, int D, int W,
 #pragma omp for schedule(dynamic, 1)
         for (int bh = 0; bh < BH; ++bh) {
             const size_t off = (size_t)bh * T * D;
-            const double *Q = q + off, *Kx = k + off, *V = v + off;
+            const size_t kvoff = (size_t)((bh / H) * Hkv + (bh % H) / G) * T * D;
+            const double *Q = q + off, *Kx = k + kvoff, *V = v + kvoff;
             for (int i = 0; i < T; ++i) {
                 const double *qi = Q + (size_t)i * D;
                 int m = query_entries(i, W, n, d0, w, f, e);
@@ -177,7 +185,7 @@ void oracle_forward_table(int B, int H, int T, int D, int W,
 /* f_k * dL/dw; l1 = sum of |f_k * dL/dw| (the magnitude of the terms).        */
 /* ------------------------------------------------------------------------- */
 
-void oracle_backward_table(int B, int H, int T, int D, int W,
+void oracle_backward_table(int B, int H, int Hkv, int T, int D, int W,
                            int n, const int *d0, const double *w, const int *f,
                            const double *q, const double *k, const double *v,
                            const double *dO,
@@ -185,10 +193,11 @@ void oracle_backward_table(int B, int H, int T, int D, int W,
                            double *dalpha, double *l1)
 {
     const double tau = 1.0 / sqrt((double)D);
-    const int BH = B * H;
-    double *part = (double *)calloc((size_t)BH * 2, sizeof(double));
-    memset(dk, 0, sizeof(double) * (size_t)BH * T * D);
-    memset(dv, 0, sizeof(double) * (size_t)BH * T * D);
+    const int BHkv = B * Hkv;
+    const int G = H / Hkv;  /* query heads sharing one key/value head */
+    double *part = (double *)calloc((size_t)BHkv * 2, sizeof(double));
+    memset(dk, 0, sizeof(double) * (size_t)BHkv * T * D);
+    memset(dv, 0, sizeof(double) * (size_t)BHkv * T * D);
 #pragma omp parallel
     {
         const int cap = W + 1 + n;
@@ -197,15 +206,21 @@ void oracle_backward_table(int B, int H, int T, int D, int W,
         double *p = (double *)malloc(sizeof(double) * (size_t)cap);
         double *dP = (double *)malloc(sizeof(double) * (size_t)cap);
         double *oi = (double *)malloc(sizeof(double) * (size_t)D);
+        /* one key/value head at a time: its G query heads scatter into the same dk, dv */
 #pragma omp for schedule(dynamic, 1)
-        for (int bh = 0; bh < BH; ++bh) {
+        for (int bk = 0; bk < BHkv; ++bk) {
+          const size_t kvoff = (size_t)bk * T * D;
+          const double *Kx = k + kvoff, *V = v + kvoff;
+          double *DK = dk + kvoff, *DV = dv + kvoff;
+          double acc = 0.0, acc1 = 0.0;
+          for (int hg = 0; hg < G; ++hg) {
+            const int bh = (bk / Hkv) * H + (bk % Hkv) * G + hg;
             const size_t off = (size_t)bh * T * D;
-            const double *Q = q + off, *Kx = k + off, *V = v + off, *G = dO + off;
-            double *DQ = dq + off, *DK = dk + off, *DV = dv + off;
-            double acc = 0.0, acc1 = 0.0;
+            const double *Q = q + off, *Gd = dO + off;
+            double *DQ = dq + off;
             for (int i = 0; i < T; ++i) {
                 const double *qi = Q + (size_t)i * D;
-                const double *gi = G + (size_t)i * D;
+                const double *gi = Gd + (size_t)i * D;
                 int m = query_entries(i, W, n, d0, w, f, e);
                 /* forward recomputed exactly */
                 double mx = -INFINITY;
@@ -260,13 +275,14 @@ void oracle_backward_table(int B, int H, int T, int D, int W,
                     }
                 }
             }
-            part[2 * bh] = acc;
-            part[2 * bh + 1] = acc1;
+          }
+          part[2 * bk] = acc;
+          part[2 * bk + 1] = acc1;
         }
         free(e); free(s); free(p); free(dP); free(oi);
     }
     double sa = 0.0, s1 = 0.0;
-    for (int bh = 0; bh < BH; ++bh) { sa += part[2 * bh]; s1 += part[2 * bh + 1]; }
+    for (int bk = 0; bk < BHkv; ++bk) { sa += part[2 * bk]; s1 += part[2 * bk + 1]; }
     free(part);
     *dalpha = sa;
     *l1 = s1;
@@ -285,18 +301,19 @@ static int table_from_alpha(float alpha, const int *base, int K, int W,
     return n;
 }
 
-int oracle_forward(int B, int H, int T, int D, int W, const int *base, int K, float alpha,
+int oracle_forward(int B, int H, int Hkv, int T, int D, int W, const int *base, int K, float alpha,
                    const double *q, const double *k, const double *v, double *o, double *lse)
 {
     int d0[ORACLE_MAX_RUNGS], f[ORACLE_MAX_RUNGS];
     double w[ORACLE_MAX_RUNGS];
     int n = table_from_alpha(alpha, base, K, W, d0, w, f);
     if (n < 0) return -1;
-    oracle_forward_table(B, H, T, D, W, n, d0, w, f, q, k, v, o, lse);
+    if (Hkv < 1 || H % Hkv != 0) return -1;
+    oracle_forward_table(B, H, Hkv, T, D, W, n, d0, w, f, q, k, v, o, lse);
     return 0;
 }
 
-int oracle_backward(int B, int H, int T, int D, int W, const int *base, int K, float alpha,
+int oracle_backward(int B, int H, int Hkv, int T, int D, int W, const int *base, int K, float alpha,
                     const double *q, const double *k, const double *v, const double *dO,
                     double *dq, double *dk, double *dv, double *dalpha, double *l1)
 {
@@ -304,7 +321,8 @@ int oracle_backward(int B, int H, int T, int D, int W, const int *base, int K, f
     double w[ORACLE_MAX_RUNGS];
     int n = table_from_alpha(alpha, base, K, W, d0, w, f);
     if (n < 0) return -1;
-    oracle_backward_table(B, H, T, D, W, n, d0, w, f, q, k, v, dO, dq, dk, dv, dalpha, l1);
+    if (Hkv < 1 || H % Hkv != 0) return -1;
+    oracle_backward_table(B, H, Hkv, T, D, W, n, d0, w, f, q, k, v, dO, dq, dk, dv, dalpha, l1);
     return 0;
 }
 

@@ -88,8 +88,11 @@ def dense_autograd(q, k, v, dO, W, base, alpha):
     B, H, T, D = q.shape
     tau = 1.0 / math.sqrt(D)
     Q = torch.tensor(q, dtype=torch.float64, requires_grad=True)
-    Kt = torch.tensor(k, dtype=torch.float64, requires_grad=True)
-    V = torch.tensor(v, dtype=torch.float64, requires_grad=True)
+    Kleaf = torch.tensor(k, dtype=torch.float64, requires_grad=True)
+    Vleaf = torch.tensor(v, dtype=torch.float64, requires_grad=True)
+    # grouped heads: each key/value head serves H / Hkv consecutive query heads
+    Kt = Kleaf.repeat_interleave(H // k.shape[1], dim=1)
+    V = Vleaf.repeat_interleave(H // k.shape[1], dim=1)
     a = torch.tensor(float(np.float32(alpha)), dtype=torch.float64, requires_grad=True)
     rungs = []
     seen = set()
@@ -126,8 +129,8 @@ def dense_autograd(q, k, v, dO, W, base, alpha):
         o = o + P[..., T + j:T + j + 1] * Vk
     L = (o * torch.tensor(dO)).sum()
     L.backward()
-    return (o.detach().numpy(), lse.detach().numpy(), Q.grad.numpy(), Kt.grad.numpy(),
-            V.grad.numpy(), float(a.grad))
+    return (o.detach().numpy(), lse.detach().numpy(), Q.grad.numpy(), Kleaf.grad.numpy(),
+            Vleaf.grad.numpy(), float(a.grad))
 
 
 # ---------------------------------------------------------------------------
@@ -168,6 +171,44 @@ def test_forward_backward_match_autograd(T, D, W, base, alpha):
     np.testing.assert_allclose(dk, dka, atol=1e-11)
     np.testing.assert_allclose(dv, dva, atol=1e-11)
     assert abs(da - daa) <= 1e-10 * max(1.0, l1)
+
+
+@pytest.mark.parametrize("Hkv,case", [(1, 1), (2, 3), (2, 5)])
+def test_grouped_heads_match_autograd(Hkv, case):
+    # k, v with fewer heads, read by groups of query heads; autograd sums the group's
+    # gradients into the shared dk, dv through repeat_interleave
+    T, D, W, base, alpha = CASES[case]
+    q, dO = rand((2, 4, T, D), 21), rand((2, 4, T, D), 24)
+    k, v = rand((2, Hkv, T, D), 22), rand((2, Hkv, T, D), 23)
+    o, lse = oracle.forward(q, k, v, W, base, alpha)
+    dq, dk, dv, da, l1 = oracle.backward(q, k, v, dO, W, base, alpha)
+    oa, la, dqa, dka, dva, daa = dense_autograd(q, k, v, dO, W, base, alpha)
+    assert dk.shape == k.shape and dv.shape == v.shape
+    np.testing.assert_allclose(o, oa, atol=1e-12)
+    np.testing.assert_allclose(lse, la, atol=1e-12)
+    np.testing.assert_allclose(dq, dqa, atol=1e-11)
+    np.testing.assert_allclose(dk, dka, atol=1e-11)
+    np.testing.assert_allclose(dv, dva, atol=1e-11)
+    assert abs(da - daa) <= 1e-10 * max(1.0, l1)
+
+
+def test_grouped_heads_equal_repeated_heads():
+    # sharing a key/value head is the same as giving each query head its own copy,
+    # with dk, dv summed over the copies
+    T, D, W, base, alpha, G = 40, 8, 4, FIB[:9], 0.83, 3
+    q, dO = rand((2, 6, T, D), 31), rand((2, 6, T, D), 34)
+    k, v = rand((2, 2, T, D), 32), rand((2, 2, T, D), 33)
+    kr, vr = np.repeat(k, G, axis=1), np.repeat(v, G, axis=1)
+    o, lse = oracle.forward(q, k, v, W, base, alpha)
+    orr, lr = oracle.forward(q, kr, vr, W, base, alpha)
+    np.testing.assert_allclose(o, orr, rtol=0, atol=1e-14)
+    np.testing.assert_allclose(lse, lr, rtol=0, atol=1e-14)
+    dq, dk, dv, da, l1 = oracle.backward(q, k, v, dO, W, base, alpha)
+    dqr, dkr, dvr, dar, l1r = oracle.backward(q, kr, vr, dO, W, base, alpha)
+    np.testing.assert_allclose(dq, dqr, rtol=0, atol=1e-14)
+    np.testing.assert_allclose(dk, dkr.reshape(2, 2, G, T, D).sum(2), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dv, dvr.reshape(2, 2, G, T, D).sum(2), rtol=0, atol=1e-12)
+    assert abs(da - dar) <= 1e-12 * max(1.0, l1) and abs(l1 - l1r) <= 1e-12 * l1
 
 
 # ---------------------------------------------------------------------------
