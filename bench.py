@@ -43,6 +43,7 @@ def parse_args():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the oracle sample")
     p.add_argument("--no-t4096", action="store_true", help="skip the T=4096 figure")
+    p.add_argument("--no-gqa", action="store_true", help="skip the grouped-heads figure")
     p.add_argument("--no-integer-offsets", action="store_true",
                    help="skip the continuous vs rounded-offset stagger figure")
     p.add_argument("--copy-probe-mb", type=int, default=0,
@@ -100,7 +101,7 @@ def alg_bytes(kernel: str, D: int, s: int) -> int:
 class Step:
     """Buffers of one rotation set and the launches of one step."""
 
-    def __init__(self, wl, call, set_index):
+    def __init__(self, wl, call, set_index, kv_heads=None):
         import torch
 
         from paper_2606_28560_amd import inputs
@@ -108,11 +109,17 @@ class Step:
 
         self.F = F
         self.call = call
-        x = inputs.attention_inputs(wl.B, wl.H, wl.T, wl.D, wl.dtype, wl.case, 1000 + set_index)
+        hkv = kv_heads or wl.H
+        x = inputs.attention_inputs(wl.B, wl.H, wl.T, wl.D, wl.dtype, wl.case, 1000 + set_index,
+                                    names=("q", "dO"))
+        x.update(inputs.attention_inputs(wl.B, hkv, wl.T, wl.D, wl.dtype, wl.case, 1000 + set_index,
+                                         names=("k", "v")))
         dev = "cuda"
         self.q, self.k, self.v, self.dO = (x[n].to(dev) for n in ("q", "k", "v", "dO"))
-        self.qr, self.kr, self.o = (torch.empty_like(self.q) for _ in range(3))
-        self.dq, self.dk, self.dv = (torch.empty_like(self.q) for _ in range(3))
+        self.grouped = hkv != wl.H
+        self.qr, self.o = torch.empty_like(self.q), torch.empty_like(self.q)
+        self.kr = torch.empty_like(self.k)
+        self.dq, self.dk, self.dv = torch.empty_like(self.q), torch.empty_like(self.k), torch.empty_like(self.v)
         self.lse = torch.empty((wl.B, wl.H, wl.T), device=dev, dtype=torch.float32)
         self.da = torch.empty(1, device=dev, dtype=torch.float32)
         need = F.fibattn_backward_workspace_bytes(wl.B, wl.H, wl.T, wl.D, call.W, len(call.base))
@@ -120,7 +127,11 @@ class Step:
 
     def forward(self):
         F, c = self.F, self.call
-        F.fibattn_rope_qk(self.q, self.k, ROPE_BASE, q_out=self.qr, k_out=self.kr)
+        if self.grouped:  # q and k have different head counts: one RoPE launch each
+            F.fibattn_rope(self.q, ROPE_BASE, out=self.qr)
+            F.fibattn_rope(self.k, ROPE_BASE, out=self.kr)
+        else:
+            F.fibattn_rope_qk(self.q, self.k, ROPE_BASE, q_out=self.qr, k_out=self.kr)
         F.fibattn_forward(self.qr, self.kr, self.v, c.W, c.base, c.alpha, o=self.o, lse=self.lse)
 
     def backward(self):
@@ -274,6 +285,31 @@ def integer_offsets_figure(steps: int, warmup: int, eager: bool, layer: int = 3)
     return out
 
 
+def gqa_figure(steps: int, warmup: int, eager: bool, kv_heads: int = 2):
+    """The 60M model's layer with its grouped key/value heads (8 query heads, 2 key/value
+    heads; B=8, T=1024, W=8, Fibonacci, alpha=1): the full step (RoPE of q and of k,
+    forward, backward) and per-kernel launch durations."""
+    from paper_2606_28560_amd import fibattn as F
+    from paper_2606_28560_amd import workloads
+
+    wl = workloads.workload("layer_60m_fixed_T1024")
+    call = wl.calls[0]
+    sets = [Step(wl, call, i, kv_heads=kv_heads) for i in range(4)]
+    if eager:
+        run = lambda i: sets[i % len(sets)]()  # noqa: E731
+    else:
+        gs = [capture(s) for s in sets]
+        run = lambda i: gs[i % len(gs)].replay()  # noqa: E731
+    ms, _ = timed(run, steps, warmup)
+    kt = {}
+    for k in ("forward", "bwd_dq", "bwd_dkdv", "rope"):
+        kms, n = kernel_time(F, sets, k, steps, 2 if k == "rope" else 1)
+        kt[k] = round(kms * n / steps, 6)  # per step (RoPE: the q and the k launch)
+    qh = wl.queries_heads
+    return {"workload": wl.name, "H": wl.H, "H_kv": kv_heads, "ms_per_step": ms,
+            "value": qh / (ms * 1e-3), "kernels_ms_per_step": kt}
+
+
 def main():
     args = parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -354,6 +390,8 @@ def main():
     }
     if not args.no_t4096:
         result["t4096"] = t4096_figure(max(5, args.steps // 4), 2, args.eager)
+    if not args.no_gqa:
+        result["gqa"] = gqa_figure(max(5, args.steps // 4), 2, args.eager)
     if not args.no_integer_offsets:
         result["integer_offsets"] = integer_offsets_figure(max(5, args.steps // 4), 2, args.eager)
     if args.copy_probe_mb:

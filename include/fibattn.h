@@ -120,6 +120,31 @@ fibattn_status_t fibattn_backward(const void *q, const void *k, const void *v,
                                   fibattn_dtype_t dtype, hipStream_t stream);
 
 /*
+ * Grouped key/value heads (Section 3 "Model and training": the model's 8 query heads
+ * share 2 key/value heads).  As fibattn_forward / fibattn_backward, with
+ *   q, o, dO, dq : [B,H,T,d_head];  lse : [B,H,T]
+ *   k, v, dk, dv : [B,H_kv,T,d_head], H_kv >= 1 dividing H
+ * Query head h of batch b reads key/value head h / (H / H_kv) of batch b; dk, dv are
+ * the sums over the H / H_kv query heads of each group (reduced inside the library
+ * in a fixed order; no atomics).  The workspace is fibattn_backward_workspace_bytes
+ * with the query head count H.  H_kv == H is exactly fibattn_forward /
+ * fibattn_backward.  Returns FIBATTN_ERR_INVALID_ARG when H_kv does not divide H.
+ */
+fibattn_status_t fibattn_forward_gqa(const void *q, const void *k, const void *v,
+                                     void *o, float *lse,
+                                     int B, int H, int H_kv, int T, int d_head, int W,
+                                     const int32_t *base, int K, float alpha,
+                                     fibattn_dtype_t dtype, hipStream_t stream);
+
+fibattn_status_t fibattn_backward_gqa(const void *q, const void *k, const void *v,
+                                      const void *o, const float *lse, const void *dO,
+                                      void *dq, void *dk, void *dv, float *dalpha,
+                                      void *workspace, size_t workspace_bytes,
+                                      int B, int H, int H_kv, int T, int d_head, int W,
+                                      const int32_t *base, int K, float alpha, float rope_base,
+                                      fibattn_dtype_t dtype, hipStream_t stream);
+
+/*
  * RoPE at the true positions t = 0..T-1 (Section 2 "Attended set"; base 1e4 in
  * Section 3).  Rotate-half pairing: (x_j, x_{j+D/2}) rotates by the angle
  * t * rope_base^(-2j/D), j < D/2; angles are evaluated in float64 and their cosine

@@ -91,19 +91,28 @@ fibattn_status_t fibattn_rung_table(float alpha, const int32_t *base, int K, int
     return FIBATTN_OK;
 }
 
-fibattn_status_t fibattn_forward(const void *q, const void *k, const void *v, void *o, float *lse,
-                                 int B, int H, int T, int d_head, int W, const int32_t *base,
-                                 int K, float alpha, fibattn_dtype_t dtype, hipStream_t stream) {
+fibattn_status_t fibattn_forward_gqa(const void *q, const void *k, const void *v, void *o,
+                                     float *lse, int B, int H, int H_kv, int T, int d_head, int W,
+                                     const int32_t *base, int K, float alpha, fibattn_dtype_t dtype,
+                                     hipStream_t stream) {
     fibattn_status_t st = check_common(B, H, T, d_head, W, K, dtype);
     if (st != FIBATTN_OK) return st;
+    if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
     if (!q || !k || !v || !o || !lse) return FIBATTN_ERR_INVALID_ARG;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse))
         return FIBATTN_ERR_INVALID_ARG;
     RungTable rt;
     st = build_table(alpha, base, K, W, &rt);
     if (st != FIBATTN_OK) return st;
-    hipError_t e = launch_forward((int)dtype, d_head, q, k, v, o, lse, B * H, T, W, rt, stream);
+    const Heads hd{H, H / H_kv};
+    hipError_t e = launch_forward((int)dtype, d_head, q, k, v, o, lse, B * H, hd, T, W, rt, stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
+fibattn_status_t fibattn_forward(const void *q, const void *k, const void *v, void *o, float *lse,
+                                 int B, int H, int T, int d_head, int W, const int32_t *base,
+                                 int K, float alpha, fibattn_dtype_t dtype, hipStream_t stream) {
+    return fibattn_forward_gqa(q, k, v, o, lse, B, H, H, T, d_head, W, base, K, alpha, dtype, stream);
 }
 
 size_t fibattn_backward_workspace_bytes(int B, int H, int T, int d_head, int W, int K) {
@@ -118,14 +127,15 @@ size_t fibattn_backward_workspace_bytes(int B, int H, int T, int d_head, int W, 
     return align256(sizeof(float) * (size_t)B * H * T) + align256(sizeof(double) * np);
 }
 
-fibattn_status_t fibattn_backward(const void *q, const void *k, const void *v, const void *o,
-                                  const float *lse, const void *dO, void *dq, void *dk, void *dv,
-                                  float *dalpha, void *workspace, size_t workspace_bytes, int B,
-                                  int H, int T, int d_head, int W, const int32_t *base, int K,
-                                  float alpha, float rope_base, fibattn_dtype_t dtype,
-                                  hipStream_t stream) {
+fibattn_status_t fibattn_backward_gqa(const void *q, const void *k, const void *v, const void *o,
+                                      const float *lse, const void *dO, void *dq, void *dk,
+                                      void *dv, float *dalpha, void *workspace,
+                                      size_t workspace_bytes, int B, int H, int H_kv, int T,
+                                      int d_head, int W, const int32_t *base, int K, float alpha,
+                                      float rope_base, fibattn_dtype_t dtype, hipStream_t stream) {
     fibattn_status_t st = check_common(B, H, T, d_head, W, K, dtype);
     if (st != FIBATTN_OK) return st;
+    if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
     if (!q || !k || !v || !o || !lse || !dO || !dq || !dk || !dv || !dalpha)
         return FIBATTN_ERR_INVALID_ARG;
     const void *ptrs[] = {q, k, v, o, lse, dO, dq, dk, dv};
@@ -141,9 +151,20 @@ fibattn_status_t fibattn_backward(const void *q, const void *k, const void *v, c
     float *delta_ws = (float *)workspace;
     double *partials = (double *)((char *)workspace + align256(sizeof(float) * (size_t)B * H * T));
     const RopeFreq rf = make_rope_freq((double)rope_base, d_head);
+    const Heads hd{H, H / H_kv};
     hipError_t e = launch_backward((int)dtype, d_head, q, k, v, o, lse, dO, dq, dk, dv, dalpha,
-                                   delta_ws, partials, B * H, T, W, rt, rf, rope_base, stream);
+                                   delta_ws, partials, B * H, hd, T, W, rt, rf, rope_base, stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
+fibattn_status_t fibattn_backward(const void *q, const void *k, const void *v, const void *o,
+                                  const float *lse, const void *dO, void *dq, void *dk, void *dv,
+                                  float *dalpha, void *workspace, size_t workspace_bytes, int B,
+                                  int H, int T, int d_head, int W, const int32_t *base, int K,
+                                  float alpha, float rope_base, fibattn_dtype_t dtype,
+                                  hipStream_t stream) {
+    return fibattn_backward_gqa(q, k, v, o, lse, dO, dq, dk, dv, dalpha, workspace, workspace_bytes,
+                                B, H, H, T, d_head, W, base, K, alpha, rope_base, dtype, stream);
 }
 
 fibattn_status_t fibattn_rope(const void *x, void *y, int B, int H, int T, int d_head,

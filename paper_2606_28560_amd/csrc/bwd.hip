@@ -30,7 +30,7 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(
     const S *__restrict__ q, const S *__restrict__ k, const S *__restrict__ v,
     const S *__restrict__ o, const float *__restrict__ lse, const S *__restrict__ dO,
     S *__restrict__ dq, float *__restrict__ delta_out, double *__restrict__ partials, int T,
-    int W, RungTable rt, float tau) {
+    int W, RungTable rt, float tau, Heads hd) {
     constexpr int VN = Vec<S>::N;
     constexpr int LPQ = D / VN;
     constexpr int QPB = 256 / LPQ;
@@ -40,9 +40,10 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(
     const int sub = threadIdx.x % LPQ;
     const int i = blockIdx.x * QPB + g;
     const size_t off = (size_t)blockIdx.y * T * D;
+    const size_t kvoff = (size_t)hd.kv_of(blockIdx.y) * T * D;
     const S *Q = q + off;
-    const S *K = k + off;
-    const S *V = v + off;
+    const S *K = k + kvoff;
+    const S *V = v + kvoff;
     const int col = sub * VN;
     const float sl2 = tau * kLog2e;
 
@@ -120,7 +121,7 @@ template <typename S, int D>
 __global__ __launch_bounds__(256) void bwd_dkdv_kernel(
     const S *__restrict__ q, const S *__restrict__ k, const S *__restrict__ v,
     const float *__restrict__ lse, const S *__restrict__ dO, const float *__restrict__ delta_in,
-    S *__restrict__ dk, S *__restrict__ dv, int T, int W, RungTable rt, float tau) {
+    S *__restrict__ dk, S *__restrict__ dv, int T, int W, RungTable rt, float tau, Heads hd) {
     constexpr int VN = Vec<S>::N;
     constexpr int LPQ = D / VN;
     constexpr int QPB = 256 / LPQ;
@@ -129,13 +130,9 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(
     const int sub = threadIdx.x % LPQ;
     const int j = blockIdx.x * QPB + g;
     if (j >= T) return;  // whole lane groups leave together; no block barrier below
-    const size_t off = (size_t)blockIdx.y * T * D;
-    const S *Q = q + off;
-    const S *K = k + off;
-    const S *V = v + off;
-    const S *G = dO + off;
-    const float *L = lse + (size_t)blockIdx.y * T;
-    const float *Dl = delta_in + (size_t)blockIdx.y * T;
+    const size_t kvoff = (size_t)blockIdx.y * T * D;  // blockIdx.y: batch * key/value head
+    const S *K = k + kvoff;
+    const S *V = v + kvoff;
     const int col = sub * VN;
     const float sl2 = tau * kLog2e;
 
@@ -145,74 +142,84 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(
 #pragma unroll
     for (int c = 0; c < VN; ++c) { adk[c] = 0.f; adv[c] = 0.f; }
 
-    // window: queries i = j .. j+W read row j with weight 1
-    const int imax = min(T - 1, j + W);
-    for (int i = j; i <= imax; ++i) {
-        Vec<S>::load(Q + (size_t)i * D + col, qv);
-        Vec<S>::load(G + (size_t)i * D + col, gv);
-        const float s = group_sum<LPQ>(dot<VN>(qv, kj));
-        const float dP = group_sum<LPQ>(dot<VN>(gv, vj));
-        const float p = exp2f(s * sl2 - L[i] * kLog2e);
-        const float c = tau * p * (dP - Dl[i]);
-#pragma unroll
-        for (int x = 0; x < VN; ++x) {
-            adk[x] = fmaf(c, qv[x], adk[x]);
-            adv[x] = fmaf(p, gv[x], adv[x]);
-        }
-    }
-    // rungs
-    for (int r = 0; r < rt.n; ++r) {
-        const int d0 = rt.d0[r];
-        const float w = rt.w[r];
-        const int i0 = j + d0;
-        if (i0 >= T) break;  // d0 increases with r
-        float kn[VN], vn[VN];
-        // query i0 reads row j as r0 (weight 1-w) and row j-1 as r1; included iff w <= j
-        if (w == 0.f || j >= 1) {
-            Vec<S>::load(Q + (size_t)i0 * D + col, qv);
-            Vec<S>::load(G + (size_t)i0 * D + col, gv);
-            float s = (1.f - w) * dot<VN>(qv, kj);
-            float dP = (1.f - w) * dot<VN>(gv, vj);
-            if (w != 0.f) {
-                Vec<S>::load(K + (size_t)(j - 1) * D + col, kn);
-                Vec<S>::load(V + (size_t)(j - 1) * D + col, vn);
-                s = fmaf(w, dot<VN>(qv, kn), s);
-                dP = fmaf(w, dot<VN>(gv, vn), dP);
-            }
-            s = group_sum<LPQ>(s);
-            dP = group_sum<LPQ>(dP);
-            const float p = exp2f(s * sl2 - L[i0] * kLog2e);
-            const float c = tau * p * (dP - Dl[i0]) * (1.f - w);
-            const float pw = p * (1.f - w);
+    // every query head of the group reads this key row; their terms add up
+    for (int hg = 0; hg < hd.G; ++hg) {
+        const int bh = hd.q_of(blockIdx.y, hg);
+        const size_t off = (size_t)bh * T * D;
+        const S *Q = q + off;
+        const S *G = dO + off;
+        const float *L = lse + (size_t)bh * T;
+        const float *Dl = delta_in + (size_t)bh * T;
+
+        // window: queries i = j .. j+W read row j with weight 1
+        const int imax = min(T - 1, j + W);
+        for (int i = j; i <= imax; ++i) {
+            Vec<S>::load(Q + (size_t)i * D + col, qv);
+            Vec<S>::load(G + (size_t)i * D + col, gv);
+            const float s = group_sum<LPQ>(dot<VN>(qv, kj));
+            const float dP = group_sum<LPQ>(dot<VN>(gv, vj));
+            const float p = exp2f(s * sl2 - L[i] * kLog2e);
+            const float c = tau * p * (dP - Dl[i]);
 #pragma unroll
             for (int x = 0; x < VN; ++x) {
                 adk[x] = fmaf(c, qv[x], adk[x]);
-                adv[x] = fmaf(pw, gv[x], adv[x]);
+                adv[x] = fmaf(p, gv[x], adv[x]);
             }
         }
-        // query i0+1 reads row j+1 as r0 and row j as r1 (weight w); always included
-        const int i1 = i0 + 1;
-        if (w != 0.f && i1 < T) {
-            Vec<S>::load(Q + (size_t)i1 * D + col, qv);
-            Vec<S>::load(G + (size_t)i1 * D + col, gv);
-            Vec<S>::load(K + (size_t)(j + 1) * D + col, kn);
-            Vec<S>::load(V + (size_t)(j + 1) * D + col, vn);
-            float s = fmaf(1.f - w, dot<VN>(qv, kn), w * dot<VN>(qv, kj));
-            float dP = fmaf(1.f - w, dot<VN>(gv, vn), w * dot<VN>(gv, vj));
-            s = group_sum<LPQ>(s);
-            dP = group_sum<LPQ>(dP);
-            const float p = exp2f(s * sl2 - L[i1] * kLog2e);
-            const float c = tau * p * (dP - Dl[i1]) * w;
-            const float pw = p * w;
+        // rungs
+        for (int r = 0; r < rt.n; ++r) {
+            const int d0 = rt.d0[r];
+            const float w = rt.w[r];
+            const int i0 = j + d0;
+            if (i0 >= T) break;  // d0 increases with r
+            float kn[VN], vn[VN];
+            // query i0 reads row j as r0 (weight 1-w) and row j-1 as r1; included iff w <= j
+            if (w == 0.f || j >= 1) {
+                Vec<S>::load(Q + (size_t)i0 * D + col, qv);
+                Vec<S>::load(G + (size_t)i0 * D + col, gv);
+                float s = (1.f - w) * dot<VN>(qv, kj);
+                float dP = (1.f - w) * dot<VN>(gv, vj);
+                if (w != 0.f) {
+                    Vec<S>::load(K + (size_t)(j - 1) * D + col, kn);
+                    Vec<S>::load(V + (size_t)(j - 1) * D + col, vn);
+                    s = fmaf(w, dot<VN>(qv, kn), s);
+                    dP = fmaf(w, dot<VN>(gv, vn), dP);
+                }
+                s = group_sum<LPQ>(s);
+                dP = group_sum<LPQ>(dP);
+                const float p = exp2f(s * sl2 - L[i0] * kLog2e);
+                const float c = tau * p * (dP - Dl[i0]) * (1.f - w);
+                const float pw = p * (1.f - w);
 #pragma unroll
-            for (int x = 0; x < VN; ++x) {
-                adk[x] = fmaf(c, qv[x], adk[x]);
-                adv[x] = fmaf(pw, gv[x], adv[x]);
+                for (int x = 0; x < VN; ++x) {
+                    adk[x] = fmaf(c, qv[x], adk[x]);
+                    adv[x] = fmaf(pw, gv[x], adv[x]);
+                }
+            }
+            // query i0+1 reads row j+1 as r0 and row j as r1 (weight w); always included
+            const int i1 = i0 + 1;
+            if (w != 0.f && i1 < T) {
+                Vec<S>::load(Q + (size_t)i1 * D + col, qv);
+                Vec<S>::load(G + (size_t)i1 * D + col, gv);
+                Vec<S>::load(K + (size_t)(j + 1) * D + col, kn);
+                Vec<S>::load(V + (size_t)(j + 1) * D + col, vn);
+                float s = fmaf(1.f - w, dot<VN>(qv, kn), w * dot<VN>(qv, kj));
+                float dP = fmaf(1.f - w, dot<VN>(gv, vn), w * dot<VN>(gv, vj));
+                s = group_sum<LPQ>(s);
+                dP = group_sum<LPQ>(dP);
+                const float p = exp2f(s * sl2 - L[i1] * kLog2e);
+                const float c = tau * p * (dP - Dl[i1]) * w;
+                const float pw = p * w;
+#pragma unroll
+                for (int x = 0; x < VN; ++x) {
+                    adk[x] = fmaf(c, qv[x], adk[x]);
+                    adv[x] = fmaf(pw, gv[x], adv[x]);
+                }
             }
         }
     }
-    Vec<S>::store(dk + off + (size_t)j * D + col, adk);
-    Vec<S>::store(dv + off + (size_t)j * D + col, adv);
+    Vec<S>::store(dk + kvoff + (size_t)j * D + col, adk);
+    Vec<S>::store(dv + kvoff + (size_t)j * D + col, adv);
 }
 
 // ---------------------------------------------------------------------------
@@ -250,17 +257,18 @@ size_t bwd_num_partials(int dtype, int D, int BH, int T) {
 template <typename S, int D>
 static hipError_t launch_bwd_t(const void *q, const void *k, const void *v, const void *o,
                                const float *lse, const void *dO, void *dq, void *dk, void *dv,
-                               float *dalpha, float *delta_ws, double *partials, int BH, int T,
-                               int W, const RungTable &rt, hipStream_t s) {
+                               float *dalpha, float *delta_ws, double *partials, int BH,
+                               const Heads &hd, int T, int W, const RungTable &rt, hipStream_t s) {
     constexpr int QPB = 256 / (D / Vec<S>::N);
     const float tau = 1.f / sqrtf((float)D);
     dim3 grid((T + QPB - 1) / QPB, BH);
     hipError_t e = launch(kBwdDq, bwd_dq_kernel<S, D>, grid, dim3(256), 0, s, (const S *)q,
                           (const S *)k, (const S *)v, (const S *)o, lse, (const S *)dO, (S *)dq,
-                          delta_ws, partials, T, W, rt, tau);
+                          delta_ws, partials, T, W, rt, tau, hd);
     if (e != hipSuccess) return e;
-    e = launch(kBwdDkDv, bwd_dkdv_kernel<S, D>, grid, dim3(256), 0, s, (const S *)q, (const S *)k,
-               (const S *)v, lse, (const S *)dO, delta_ws, (S *)dk, (S *)dv, T, W, rt, tau);
+    e = launch(kBwdDkDv, bwd_dkdv_kernel<S, D>, dim3(grid.x, BH / hd.G), dim3(256), 0, s,
+               (const S *)q, (const S *)k, (const S *)v, lse, (const S *)dO, delta_ws, (S *)dk,
+               (S *)dv, T, W, rt, tau, hd);
     if (e != hipSuccess) return e;
     return launch(kDalphaReduce, dalpha_reduce_kernel, dim3(1), dim3(256), 0, s, partials,
                   (size_t)grid.x * grid.y, dalpha);
@@ -269,11 +277,11 @@ static hipError_t launch_bwd_t(const void *q, const void *k, const void *v, cons
 static hipError_t launch_backward_generic(int dtype, int D, const void *q, const void *k, const void *v,
                                           const void *o, const float *lse, const void *dO, void *dq,
                                           void *dk, void *dv, float *dalpha, float *delta_ws,
-                                          double *partials, int BH, int T, int W, const RungTable &rt,
-                                          hipStream_t s) {
+                                          double *partials, int BH, const Heads &hd, int T, int W,
+                                          const RungTable &rt, hipStream_t s) {
 #define FIBATTN_BWD(S_, D_)                                                                  \
     return launch_bwd_t<S_, D_>(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials, \
-                                BH, T, W, rt, s)
+                                BH, hd, T, W, rt, s)
     if (dtype == 0 && D == 32) FIBATTN_BWD(float, 32);
     if (dtype == 0 && D == 64) FIBATTN_BWD(float, 64);
     if (dtype == 1 && D == 32) FIBATTN_BWD(uint16_t, 32);
@@ -286,15 +294,23 @@ static hipError_t launch_backward_generic(int dtype, int D, const void *q, const
 hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const void *v,
                            const void *o, const float *lse, const void *dO, void *dq, void *dk,
                            void *dv, float *dalpha, float *delta_ws, double *partials, int BH,
-                           int T, int W, const RungTable &rt, const RopeFreq &rf, float rope_base,
-                           hipStream_t s) {
+                           const Heads &hd, int T, int W, const RungTable &rt, const RopeFreq &rf,
+                           float rope_base, hipStream_t s) {
     if (backward_mfma_supported(dtype, D, W))
         return launch_backward_mfma(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials, BH,
-                                    T, W, rt, rf, s);
+                                    hd, T, W, rt, rf, s);
     hipError_t e = launch_backward_generic(dtype, D, q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws,
-                                           partials, BH, T, W, rt, s);
-    // R^T on dq and dk in place: gradients w.r.t. the unrotated q, k
-    if (e == hipSuccess && rf.on) e = launch_rope(dtype, D, dq, dq, dk, dk, BH, T, rope_base, 1, s);
+                                           partials, BH, hd, T, W, rt, s);
+    // R^T on dq and dk in place: gradients w.r.t. the unrotated q, k (R^T is linear, so
+    // it also carries the group sum in dk)
+    if (e == hipSuccess && rf.on) {
+        if (hd.G == 1) {
+            e = launch_rope(dtype, D, dq, dq, dk, dk, BH, T, rope_base, 1, s);
+        } else {
+            e = launch_rope(dtype, D, dq, dq, nullptr, nullptr, BH, T, rope_base, 1, s);
+            if (e == hipSuccess) e = launch_rope(dtype, D, dk, dk, nullptr, nullptr, BH / hd.G, T, rope_base, 1, s);
+        }
+    }
     return e;
 }
 

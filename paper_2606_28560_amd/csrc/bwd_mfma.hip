@@ -37,7 +37,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const uint16_t *__restrict__ o, const float *__restrict__ lse, const uint16_t *__restrict__ dO,
     uint16_t *__restrict__ dq, float *__restrict__ delta_out, double *__restrict__ partials, int T,
-    int W, RungTable rt, RopeFreq rf, float tau, int tiles) {
+    int W, RungTable rt, RopeFreq rf, float tau, int tiles, Heads hd) {
     __shared__ __align__(16) uint16_t kr[kStage * kD];
     __shared__ __align__(16) uint16_t vr[kStage * kD];
     __shared__ double sfreq[32];
@@ -51,9 +51,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     const int bh = blk / tiles;
     const int T0 = (blk % tiles) * kBwdB;
     const size_t off = (size_t)bh * T * kD;
+    const size_t kvoff = (size_t)hd.kv_of(bh) * T * kD;
     const uint16_t *Q = q + off;
-    const uint16_t *K = k + off;
-    const uint16_t *V = v + off;
+    const uint16_t *K = k + kvoff;
+    const uint16_t *V = v + kvoff;
     const uint16_t *G = dO + off;
     const float *L = lse + (size_t)bh * T;
     const float sl2 = tau * kLog2e;
@@ -192,39 +193,45 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 }
 
 // ---------------------------------------------------------------------------
-template <bool INTERP>
+// NH: query heads of a group processed side by side.  The workgroup's four waves are
+// kKG = 4 / NH key groups of 16 keys times NH head slots; a group of G query heads
+// takes G / NH passes (ONE_PASS: G == NH, no pass loop), and the head slots' dk, dv
+// are summed through LDS at the end.
+template <bool INTERP, int NH, bool ONE_PASS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void bwd_dkdv_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const float *__restrict__ lse, const uint16_t *__restrict__ dO, const float *__restrict__ delta_in,
     uint16_t *__restrict__ dk, uint16_t *__restrict__ dv, const double *__restrict__ partials,
     int n_partials, float *__restrict__ dalpha, int T, int W, RungTable rt, RopeFreq rf, float tau,
-    int tiles) {
-    __shared__ double sfreq[32];
-    __shared__ __align__(16) uint16_t qr[kStage * kD];
-    __shared__ __align__(16) uint16_t gr[kStage * kD];
+    int tiles, Heads hd) {
+    constexpr int kKG = 4 / NH;          // key groups of 16 per workgroup
+    constexpr int kKeys = 16 * kKG;      // keys per workgroup
+    constexpr int kSt = kKeys + 16;      // staged query rows per head slot
     // the tile's own K, V rows [T0 - kLead, T0 - kLead + kOwn): with interpolation also
     // the neighbours j-1 and j+1 of every key j
     constexpr int kLead = INTERP ? 4 : 0;
-    constexpr int kOwn = INTERP ? kBwdB + 8 : kBwdB;
+    constexpr int kOwn = kKeys + (INTERP ? 8 : 0);
+    __shared__ double sfreq[32];
+    // q rows of every head slot, then their dO rows
+    __shared__ __align__(16) uint16_t stage[2 * NH * kSt * kD];
     __shared__ __align__(16) uint16_t kown[kOwn * kD];
     __shared__ __align__(16) uint16_t vown[kOwn * kD];
-    __shared__ float sl[kStage], sd[kStage];
+    __shared__ float sl[NH * kSt], sd[NH * kSt];
 
     const int lane = threadIdx.x & 63;
-    const int wv = threadIdx.x >> 6;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int kg = wv / NH, hs = wv % NH;      // key group, head slot
     const int nm = lane & 15, gm = lane >> 4;  // MFMA layout
     const int nq = lane >> 2, gq = lane & 3;   // quad layout
     const int blk = xcd_remap(blockIdx.x, gridDim.x);
-    const int bh = blk / tiles;
-    const int T0 = (blk % tiles) * kBwdB;
-    const size_t off = (size_t)bh * T * kD;
-    const uint16_t *Q = q + off;
-    const uint16_t *K = k + off;
-    const uint16_t *V = v + off;
-    const uint16_t *G = dO + off;
-    const float *L = lse + (size_t)bh * T;
-    const float *Dl = delta_in + (size_t)bh * T;
+    const int bk = blk / tiles;                // batch * key/value heads + key/value head
+    const int T0 = (blk % tiles) * kKeys;
+    const size_t kvoff = (size_t)bk * T * kD;
+    const uint16_t *K = k + kvoff;
+    const uint16_t *V = v + kvoff;
     const float sl2 = tau * kLog2e;
+    uint16_t *qr = stage + hs * kSt * kD;            // this wave's head slot
+    uint16_t *gr = stage + (NH + hs) * kSt * kD;
 
     // final dalpha: the dq kernel has completed on this stream (the reduction borrows
     // kown before its rows are loaded)
@@ -242,174 +249,240 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         __syncthreads();
     }
 
-    const int t0 = T0 + 16 * wv;
-    const int jm = t0 + nm;  // MFMA layout key
-    const int j = t0 + nq;   // quad layout key
+    const int t0 = T0 + 16 * kg;
+    const int jm = t0 + nm;      // MFMA layout key
+    const int j_key = t0 + nq;   // quad layout key
+    const int jo = kLead + 16 * kg + nq;  // this key's row in kown / vown (quad layout)
 
     // rungs: some key of this wave has j + floor(d) < T for a prefix of the table
     int nact = 0;
 #pragma unroll
     for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && t0 + rt.d0[r] < T) ? 1 : 0;
     nact = __builtin_amdgcn_readfirstlane(nact);  // wave-uniform: scalar branches
-    // one interpolated rung: the rows (q, dO) of queries i0 = j + floor(d) and i0 + 1
-    // with their lse (log2 units) and Delta
-    struct Rung {
-        Slice x[4];  // q0, g0 (query i0), q1, g1 (query i0 + 1)
-        float le[2], de[2];
-    };
-    auto load_rung = [&](int r, Rung &ru) {
-#pragma unroll
-        for (int y = 0; y < 2; ++y) {
-            const int ic = min(j + rt.d0[r] + y, T - 1);
-            ru.x[2 * y] = load_row(Q, ic, gq);
-            ru.x[2 * y + 1] = load_row(G, ic, gq);
-            ru.le[y] = L[ic] * kLog2e;
-            ru.de[y] = Dl[ic];
-        }
-    };
-    // two rungs' query rows (q, dO) with their lse (log2 units) and Delta
-    struct Pair {
-        Slice x[4];  // q0a, g0a, q0b, g0b
-        float le[2], de[2];
-    };
-    auto load_pair = [&](int rb, Pair &pr) {
-#pragma unroll
-        for (int y = 0; y < 2; ++y) {
-            const int ic = min(j + rt.d0[rb + y], T - 1);
-            pr.x[2 * y] = load_row(Q, ic, gq);
-            pr.x[2 * y + 1] = load_row(G, ic, gq);
-            pr.le[y] = L[ic] * kLog2e;
-            pr.de[y] = Dl[ic];
-        }
-    };
-    Pair pA;
-    Rung ru;
-    if (0 < nact) {  // in flight during the band phase
-        if (INTERP) load_rung(0, ru);
-        else load_pair(0, pA);
-    }
 
-    // q and dO rows, lse and Delta of queries [T0, T0+80) (rows past the end are
-    // clamped copies, masked below)
-    dma_rows<kStage>(qr, Q, T0, T);
-    dma_rows<kStage>(gr, G, T0, T);
-    dma_rows<kOwn>(kown, K, T0 - kLead, T);  // rows outside [0, T) are clamped copies
-    dma_rows<kOwn>(vown, V, T0 - kLead, T);
-    for (int c = threadIdx.x; c < kStage; c += 256) {
-        const int row = T0 + c;
-        sl[c] = row < T ? L[row] * kLog2e : 0.f;
-        sd[c] = row < T ? Dl[row] : 0.f;
-    }
-    stage_freq(sfreq, rf);
-    wait_vmem();
-    __syncthreads();
-
-    // band (MFMA layout): queries [t0, t0 + 32) in two blocks
-    const Slice km = dma_slice(kown, kLead + 16 * wv + nm, gm);
-    const Slice vm = dma_slice(vown, kLead + 16 * wv + nm, gm);
-    uint32_t cw[4], pw[4];
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-        const int sq = 16 * wv + 16 * b + nm;  // staged query row of this lane's A operand
-        const f32x4 s = mfma_dot64(dma_slice(qr, sq, gm), km, f32x4{0.f, 0.f, 0.f, 0.f});
-        const f32x4 dp = mfma_dot64(dma_slice(gr, sq, gm), vm, f32x4{0.f, 0.f, 0.f, 0.f});
-        float c[4], p[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int si = 16 * wv + 16 * b + 4 * gm + e;  // staged index of the query
-            const int qi = T0 + si;
-            const bool ok = qi < T && jm < T && qi >= jm && qi - jm <= W;
-            p[e] = ok ? fast_exp2(s[e] * sl2 - sl[si]) : 0.f;
-            c[e] = tau * p[e] * (dp[e] - sd[si]);
-        }
-        cw[2 * b] = pack_bf16(c[0], c[1]);
-        cw[2 * b + 1] = pack_bf16(c[2], c[3]);
-        pw[2 * b] = pack_bf16(p[0], p[1]);
-        pw[2 * b + 1] = pack_bf16(p[2], p[3]);
-    }
-    const bf16x8 Cb = as_bf8(make_uint4(cw[0], cw[1], cw[2], cw[3]));
-    const bf16x8 Pb = as_bf8(make_uint4(pw[0], pw[1], pw[2], pw[3]));
     Acc16 adk, adv;
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        adk.c[c] = mfma(dma_operand_t(qr, c, nm, 16 * wv, gm), Cb, f32x4{0.f, 0.f, 0.f, 0.f});
-        adv.c[c] = mfma(dma_operand_t(gr, c, nm, 16 * wv, gm), Pb, f32x4{0.f, 0.f, 0.f, 0.f});
-    }
-    acc_to_quad(adk, lane);
-    acc_to_quad(adv, lane);
+    acc_zero(adk);
+    acc_zero(adv);
+    const int passes = ONE_PASS ? 1 : hd.G / NH;
+    for (int pass = 0; pass < passes; ++pass) {
+        // an opaque copy of the key index keeps the per-rung index arithmetic inside the
+        // pass loop (hoisted for all rungs at once it would not fit the registers)
+        int j = j_key;
+        asm volatile("" : "+v"(j));
+        const int bh = hd.q_of(bk, pass * NH + hs);  // this wave's query head
+        const size_t off = (size_t)bh * T * kD;
+        const uint16_t *Q = q + off;
+        const uint16_t *Gd = dO + off;
+        const float *L = lse + (size_t)bh * T;
+        const float *Dl = delta_in + (size_t)bh * T;
 
-    const int jo = kLead + 16 * wv + nq;  // this key's row in kown / vown (quad layout)
-    if (!INTERP) {
-        const Slice ks = dma_slice(kown, jo, gq);
-        const Slice vs = dma_slice(vown, jo, gq);
-        // every w == 0: query j + d0 reads this row with weight 1; two rungs per batch
-        auto compute_pair = [&](int rb, const Pair &pr) {
-            float cc[2], pp[2];
+        // one interpolated rung: the rows (q, dO) of queries i0 = j + floor(d) and
+        // i0 + 1 with their lse (log2 units) and Delta
+        struct Rung {
+            Slice x[4];  // q0, g0 (query i0), q1, g1 (query i0 + 1)
+            float le[2], de[2];
+        };
+        auto load_rung = [&](int r, Rung &ru) {
 #pragma unroll
             for (int y = 0; y < 2; ++y) {
-                const int i0 = j + rt.d0[rb + y];
-                const bool in0 = rb + y < nact && j < T && i0 < T;
-                const float sc = quad_sum(dot_slice(pr.x[2 * y], ks));
-                const float dp = quad_sum(dot_slice(pr.x[2 * y + 1], vs));
-                pp[y] = in0 ? fast_exp2(sc * sl2 - pr.le[y]) : 0.f;
-                cc[y] = tau * pp[y] * (dp - pr.de[y]);
+                const int ic = min(j + rt.d0[r] + y, T - 1);
+                ru.x[2 * y] = load_row(Q, ic, gq);
+                ru.x[2 * y + 1] = load_row(Gd, ic, gq);
+                ru.le[y] = L[ic] * kLog2e;
+                ru.de[y] = Dl[ic];
             }
-            acc_axpy2(adk, cc[0], pr.x[0], cc[1], pr.x[2]);
-            acc_axpy2(adv, pp[0], pr.x[1], pp[1], pr.x[3]);
         };
-        // one pair in flight (register budget: four waves per SIMD)
+        // two rungs' query rows (q, dO) with their lse (log2 units) and Delta
+        struct Pair {
+            Slice x[4];  // q0a, g0a, q0b, g0b
+            float le[2], de[2];
+        };
+        auto load_pair = [&](int rb, Pair &pr) {
 #pragma unroll
-        for (int rb = 0; rb < kMaxRungs; rb += 2) {
-            if (rb < nact) {
-                if (rb > 0) load_pair(rb, pA);
-                compute_pair(rb, pA);
+            for (int y = 0; y < 2; ++y) {
+                const int ic = min(j + rt.d0[rb + y], T - 1);
+                pr.x[2 * y] = load_row(Q, ic, gq);
+                pr.x[2 * y + 1] = load_row(Gd, ic, gq);
+                pr.le[y] = L[ic] * kLog2e;
+                pr.de[y] = Dl[ic];
+            }
+        };
+        Pair pA;
+        Rung ru;
+        if (0 < nact) {  // in flight during the band phase
+            if (INTERP) load_rung(0, ru);
+            else load_pair(0, pA);
+        }
+
+        if (pass > 0) __syncthreads();  // every wave is done with the previous pass's rows
+        // q and dO rows, lse and Delta of queries [T0, T0 + kSt) of every head slot (rows
+        // past the end are clamped copies, masked below)
+#pragma unroll 1
+        for (int u = 0; u < NH; ++u) {
+            const size_t ou = (size_t)hd.q_of(bk, pass * NH + u) * T;
+            dma_rows<kSt>(stage + u * kSt * kD, q + ou * kD, T0, T);
+            dma_rows<kSt>(stage + (NH + u) * kSt * kD, dO + ou * kD, T0, T);
+            for (int c = threadIdx.x; c < kSt; c += 256) {
+                const int row = T0 + c;
+                sl[u * kSt + c] = row < T ? lse[ou + row] * kLog2e : 0.f;
+                sd[u * kSt + c] = row < T ? delta_in[ou + row] : 0.f;
             }
         }
-    } else {
-        // query i0 = j + floor(d) reads this row as r0 (weight 1 - w) and row j-1 as
-        // r1; query i0 + 1 reads row j+1 as r0 and this row as r1 (weight w).  One
-        // rung in flight (register budget: four waves per SIMD); rows j-1, j, j+1
-        // come from kown / vown.
-        auto compute_rung = [&](int r, const Rung &ru) {
-            const float w = rt.w[r];
-            const int i0 = j + rt.d0[r];
-            const bool in0 = r < nact && j < T && i0 < T && (w == 0.f || j >= 1);
-            const bool in1 = r < nact && j < T && i0 + 1 < T && w != 0.f;
-            float sa, sb, da, db;
-            {
-                const Slice kj = dma_slice(kown, jo, gq);
-                const Slice kl = dma_slice(kown, jo - 1, gq);
-                const Slice kh = dma_slice(kown, jo + 1, gq);
-                sa = quad_sum((1.f - w) * dot_slice(ru.x[0], kj) + w * dot_slice(ru.x[0], kl));
-                sb = quad_sum((1.f - w) * dot_slice(ru.x[2], kh) + w * dot_slice(ru.x[2], kj));
-            }
-            {
-                const Slice vj = dma_slice(vown, jo, gq);
-                const Slice vl = dma_slice(vown, jo - 1, gq);
-                const Slice vh = dma_slice(vown, jo + 1, gq);
-                da = quad_sum((1.f - w) * dot_slice(ru.x[1], vj) + w * dot_slice(ru.x[1], vl));
-                db = quad_sum((1.f - w) * dot_slice(ru.x[3], vh) + w * dot_slice(ru.x[3], vj));
-            }
-            const float pa = in0 ? fast_exp2(sa * sl2 - ru.le[0]) : 0.f;
-            const float ca = tau * pa * (da - ru.de[0]);
-            const float pb = in1 ? fast_exp2(sb * sl2 - ru.le[1]) : 0.f;
-            const float cb = tau * pb * (db - ru.de[1]);
-            acc_axpy2(adk, (1.f - w) * ca, ru.x[0], w * cb, ru.x[2]);
-            acc_axpy2(adv, (1.f - w) * pa, ru.x[1], w * pb, ru.x[3]);
-        };
+        if (pass == 0) {
+            dma_rows<kOwn>(kown, K, T0 - kLead, T);  // rows outside [0, T) are clamped copies
+            dma_rows<kOwn>(vown, V, T0 - kLead, T);
+            stage_freq(sfreq, rf);
+        }
+        wait_vmem();
+        __syncthreads();
+
+        // band (MFMA layout): queries [t0, t0 + 32) in two blocks
+        {
+            const Slice km = dma_slice(kown, kLead + 16 * kg + nm, gm);
+            const Slice vm = dma_slice(vown, kLead + 16 * kg + nm, gm);
+            uint32_t cw[4], pw[4];
 #pragma unroll
-        for (int r = 0; r < kMaxRungs; ++r) {
-            if (r < nact) {
-                if (r > 0) load_rung(r, ru);
-                compute_rung(r, ru);
+            for (int b = 0; b < 2; ++b) {
+                const int sq = 16 * kg + 16 * b + nm;  // staged query row of this lane's A operand
+                const f32x4 s = mfma_dot64(dma_slice(qr, sq, gm), km, f32x4{0.f, 0.f, 0.f, 0.f});
+                const f32x4 dp = mfma_dot64(dma_slice(gr, sq, gm), vm, f32x4{0.f, 0.f, 0.f, 0.f});
+                float c[4], p[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int si = 16 * kg + 16 * b + 4 * gm + e;  // staged index of the query
+                    const int qi = T0 + si;
+                    const bool ok = qi < T && jm < T && qi >= jm && qi - jm <= W;
+                    p[e] = ok ? fast_exp2(s[e] * sl2 - sl[hs * kSt + si]) : 0.f;
+                    c[e] = tau * p[e] * (dp[e] - sd[hs * kSt + si]);
+                }
+                cw[2 * b] = pack_bf16(c[0], c[1]);
+                cw[2 * b + 1] = pack_bf16(c[2], c[3]);
+                pw[2 * b] = pack_bf16(p[0], p[1]);
+                pw[2 * b + 1] = pack_bf16(p[2], p[3]);
+            }
+            const bf16x8 Cb = as_bf8(make_uint4(cw[0], cw[1], cw[2], cw[3]));
+            const bf16x8 Pb = as_bf8(make_uint4(pw[0], pw[1], pw[2], pw[3]));
+            Acc16 bk_, bv_;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                bk_.c[c] = mfma(dma_operand_t(qr, c, nm, 16 * kg, gm), Cb, f32x4{0.f, 0.f, 0.f, 0.f});
+                bv_.c[c] = mfma(dma_operand_t(gr, c, nm, 16 * kg, gm), Pb, f32x4{0.f, 0.f, 0.f, 0.f});
+            }
+            acc_to_quad(bk_, lane);
+            acc_to_quad(bv_, lane);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                adk.c[c] += bk_.c[c];
+                adv.c[c] += bv_.c[c];
+            }
+        }
+
+        if (!INTERP) {
+            const Slice ks = dma_slice(kown, jo, gq);
+            const Slice vs = dma_slice(vown, jo, gq);
+            // every w == 0: query j + d0 reads this row with weight 1; two rungs per batch
+            auto compute_pair = [&](int rb, const Pair &pr) {
+                float cc[2], pp[2];
+#pragma unroll
+                for (int y = 0; y < 2; ++y) {
+                    const int i0 = j + rt.d0[rb + y];
+                    const bool in0 = rb + y < nact && j < T && i0 < T;
+                    const float sc = quad_sum(dot_slice(pr.x[2 * y], ks));
+                    const float dp = quad_sum(dot_slice(pr.x[2 * y + 1], vs));
+                    pp[y] = in0 ? fast_exp2(sc * sl2 - pr.le[y]) : 0.f;
+                    cc[y] = tau * pp[y] * (dp - pr.de[y]);
+                }
+                acc_axpy2(adk, cc[0], pr.x[0], cc[1], pr.x[2]);
+                acc_axpy2(adv, pp[0], pr.x[1], pp[1], pr.x[3]);
+            };
+            // one pair in flight (register budget: four waves per SIMD)
+#pragma unroll
+            for (int rb = 0; rb < kMaxRungs; rb += 2) {
+                if (rb < nact) {
+                    if (rb > 0) load_pair(rb, pA);
+                    compute_pair(rb, pA);
+                }
+            }
+        } else {
+            // query i0 = j + floor(d) reads this row as r0 (weight 1 - w) and row j-1
+            // as r1; query i0 + 1 reads row j+1 as r0 and this row as r1 (weight w).
+            // One rung in flight (register budget: four waves per SIMD); rows j-1, j,
+            // j+1 come from kown / vown.
+            auto compute_rung = [&](int r, const Rung &ru) {
+                const float w = rt.w[r];
+                const int i0 = j + rt.d0[r];
+                const bool in0 = r < nact && j < T && i0 < T && (w == 0.f || j >= 1);
+                const bool in1 = r < nact && j < T && i0 + 1 < T && w != 0.f;
+                float sa, sb, da, db;
+                {
+                    const Slice kj = dma_slice(kown, jo, gq);
+                    const Slice kl = dma_slice(kown, jo - 1, gq);
+                    const Slice kh = dma_slice(kown, jo + 1, gq);
+                    sa = quad_sum((1.f - w) * dot_slice(ru.x[0], kj) + w * dot_slice(ru.x[0], kl));
+                    sb = quad_sum((1.f - w) * dot_slice(ru.x[2], kh) + w * dot_slice(ru.x[2], kj));
+                }
+                {
+                    const Slice vj = dma_slice(vown, jo, gq);
+                    const Slice vl = dma_slice(vown, jo - 1, gq);
+                    const Slice vh = dma_slice(vown, jo + 1, gq);
+                    da = quad_sum((1.f - w) * dot_slice(ru.x[1], vj) + w * dot_slice(ru.x[1], vl));
+                    db = quad_sum((1.f - w) * dot_slice(ru.x[3], vh) + w * dot_slice(ru.x[3], vj));
+                }
+                const float pa = in0 ? fast_exp2(sa * sl2 - ru.le[0]) : 0.f;
+                const float ca = tau * pa * (da - ru.de[0]);
+                const float pb = in1 ? fast_exp2(sb * sl2 - ru.le[1]) : 0.f;
+                const float cb = tau * pb * (db - ru.de[1]);
+                acc_axpy2(adk, (1.f - w) * ca, ru.x[0], w * cb, ru.x[2]);
+                acc_axpy2(adv, (1.f - w) * pa, ru.x[1], w * pb, ru.x[3]);
+            };
+#pragma unroll
+            for (int r = 0; r < kMaxRungs; ++r) {
+                if (r < nact) {
+                    if (r > 0) load_rung(r, ru);
+                    compute_rung(r, ru);
+                }
             }
         }
     }
 
-    if (rf.on) acc_rope_t(adk, j, sfreq + 8 * gq);  // gradient w.r.t. the unrotated k
-    if (j < T) {
-        store_acc(dk + off + (size_t)j * kD, gq, adk, 1.f);
-        store_acc(dv + off + (size_t)j * kD, gq, adv, 1.f);
+    if constexpr (NH > 1) {
+        // sum the head slots: slots 1.. hand their accumulators (quad layout, 32 floats
+        // per lane) to slot 0 of the same key group through the staging LDS
+        static_assert(sizeof(stage) >= (size_t)(4 - kKG) * 64 * 32 * sizeof(float), "LDS for the sum");
+        float *xfer = reinterpret_cast<float *>(stage);
+        __syncthreads();  // every wave is done with the staged rows
+        if (hs > 0) {
+            float *dst = xfer + ((size_t)(kg * (NH - 1) + hs - 1) * 64 + lane) * 32;
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    dst[4 * c + e] = adk.c[c][e];
+                    dst[16 + 4 * c + e] = adv.c[c][e];
+                }
+        }
+        __syncthreads();
+        if (hs == 0) {
+#pragma unroll 1
+            for (int u = 1; u < NH; ++u) {
+                const float *src = xfer + ((size_t)(kg * (NH - 1) + u - 1) * 64 + lane) * 32;
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        adk.c[c][e] += src[4 * c + e];
+                        adv.c[c][e] += src[16 + 4 * c + e];
+                    }
+            }
+        }
+    }
+
+    if (hs == 0) {
+        if (rf.on) acc_rope_t(adk, j_key, sfreq + 8 * gq);  // gradient w.r.t. the unrotated k
+        if (j_key < T) {
+            store_acc(dk + kvoff + (size_t)j_key * kD, gq, adk, 1.f);
+            store_acc(dv + kvoff + (size_t)j_key * kD, gq, adv, 1.f);
+        }
     }
 }
 
@@ -417,10 +490,26 @@ bool backward_mfma_supported(int dtype, int D, int W) { return dtype == 1 && D =
 
 size_t bwd_mfma_num_partials(int BH, int T) { return (size_t)((T + kBwdB - 1) / kBwdB) * (size_t)BH; }
 
+template <int NH>
+static hipError_t launch_dkdv(bool interp, const void *q, const void *k, const void *v,
+                              const float *lse, const void *dO, const float *delta_ws, void *dk,
+                              void *dv, const double *partials, int n_partials, float *dalpha,
+                              int BH, const Heads &hd, int T, int W, const RungTable &rt,
+                              const RopeFreq &rf, float tau, hipStream_t s) {
+    constexpr int keys = 64 / NH;
+    const int tiles = (T + keys - 1) / keys;
+    const bool one = hd.G == NH;
+    auto kern = interp ? (one ? bwd_dkdv_bf16_d64_kernel<true, NH, true> : bwd_dkdv_bf16_d64_kernel<true, NH, false>)
+                       : (one ? bwd_dkdv_bf16_d64_kernel<false, NH, true> : bwd_dkdv_bf16_d64_kernel<false, NH, false>);
+    return launch(kBwdDkDv, kern, dim3(tiles * (BH / hd.G)), dim3(256), 0, s, q, k, v, lse, dO,
+                  delta_ws, dk, dv, partials, n_partials, dalpha, T, W, rt, rf, tau, tiles, hd);
+}
+
 hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, const void *o,
                                 const float *lse, const void *dO, void *dq, void *dk, void *dv,
-                                float *dalpha, float *delta_ws, double *partials, int BH, int T,
-                                int W, const RungTable &rt, const RopeFreq &rf, hipStream_t s) {
+                                float *dalpha, float *delta_ws, double *partials, int BH,
+                                const Heads &hd, int T, int W, const RungTable &rt,
+                                const RopeFreq &rf, hipStream_t s) {
     const int tiles = (T + kBwdB - 1) / kBwdB;
     const float tau = 1.f / sqrtf(64.f);
     const int nb = tiles * BH;
@@ -428,11 +517,17 @@ hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, con
     for (int r = 0; r < rt.n; ++r) interp = interp || rt.w[r] != 0.f;
     hipError_t e = launch(kBwdDq, interp ? bwd_dq_bf16_d64_kernel<true> : bwd_dq_bf16_d64_kernel<false>,
                           dim3(nb), dim3(256), 0, s, q, k, v, o, lse, dO, dq, delta_ws, partials,
-                          T, W, rt, rf, tau, tiles);
+                          T, W, rt, rf, tau, tiles, hd);
     if (e != hipSuccess) return e;
-    return launch(kBwdDkDv, interp ? bwd_dkdv_bf16_d64_kernel<true> : bwd_dkdv_bf16_d64_kernel<false>,
-                  dim3(nb), dim3(256), 0, s, q, k, v, lse, dO, delta_ws, dk, dv, partials, nb,
-                  dalpha, T, W, rt, rf, tau, tiles);
+    // query heads per key/value head processed side by side in a workgroup
+    if (hd.G % 4 == 0)
+        return launch_dkdv<4>(interp, q, k, v, lse, dO, delta_ws, dk, dv, partials, nb, dalpha, BH,
+                              hd, T, W, rt, rf, tau, s);
+    if (hd.G % 2 == 0)
+        return launch_dkdv<2>(interp, q, k, v, lse, dO, delta_ws, dk, dv, partials, nb, dalpha, BH,
+                              hd, T, W, rt, rf, tau, s);
+    return launch_dkdv<1>(interp, q, k, v, lse, dO, delta_ws, dk, dv, partials, nb, dalpha, BH, hd,
+                          T, W, rt, rf, tau, s);
 }
 
 }  // namespace fibattn

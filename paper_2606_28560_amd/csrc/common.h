@@ -19,6 +19,18 @@ struct RungTable {
     int f[kMaxRungs];
 };
 
+// Grouped key/value heads (Section 3 "Model and training": 8 query heads share 2
+// key/value heads): query head h of batch b reads key/value head h / G of that batch.
+struct Heads {
+    int H;  // query heads per batch
+    int G;  // query heads per key/value head (1: one key/value head per query head)
+    __host__ __device__ int kv_heads() const { return H / G; }
+    // (batch * H + h) -> (batch * H/G + h/G)
+    __host__ __device__ int kv_of(int bh) const { return (bh / H) * (H / G) + (bh % H) / G; }
+    // (batch * H/G + hk), group member g -> batch * H + hk * G + g
+    __host__ __device__ int q_of(int bk, int g) const { return (bk / (H / G)) * H + (bk % (H / G)) * G + g; }
+};
+
 // RoPE inverse frequencies base^(-2j/D) for j < D/2 <= 32, evaluated in float64 on
 // the host; `on` = 0 when no rotation is requested.
 struct RopeFreq {

@@ -20,7 +20,7 @@ template <typename S, int D>
 __global__ __launch_bounds__(256) void fwd_kernel(const S *__restrict__ q, const S *__restrict__ k,
                                                   const S *__restrict__ v, S *__restrict__ o,
                                                   float *__restrict__ lse, int T, int W,
-                                                  RungTable rt, float scale_log2) {
+                                                  RungTable rt, float scale_log2, Heads hd) {
     constexpr int VN = Vec<S>::N;
     constexpr int LPQ = D / VN;
     constexpr int QPB = 256 / LPQ;
@@ -31,9 +31,10 @@ __global__ __launch_bounds__(256) void fwd_kernel(const S *__restrict__ q, const
     const int sub = threadIdx.x % LPQ;
     const int i = blockIdx.x * QPB + g;
     const size_t off = (size_t)blockIdx.y * T * D;
+    const size_t kvoff = (size_t)hd.kv_of(blockIdx.y) * T * D;
     const S *Q = q + off;
-    const S *K = k + off;
-    const S *V = v + off;
+    const S *K = k + kvoff;
+    const S *V = v + kvoff;
     float *sc = smem + g * cap;
     const int col = sub * VN;
 
@@ -108,23 +109,25 @@ __global__ __launch_bounds__(256) void fwd_kernel(const S *__restrict__ q, const
 
 template <typename S, int D>
 static hipError_t launch_fwd_t(const void *q, const void *k, const void *v, void *o, float *lse,
-                               int BH, int T, int W, const RungTable &rt, hipStream_t s) {
+                               int BH, const Heads &hd, int T, int W, const RungTable &rt,
+                               hipStream_t s) {
     constexpr int LPQ = D / Vec<S>::N;
     constexpr int QPB = 256 / LPQ;
     dim3 grid((T + QPB - 1) / QPB, BH);
     const size_t lds = sizeof(float) * QPB * (size_t)(W + 1 + rt.n);
     const float scale_log2 = kLog2e / sqrtf((float)D);
     return launch(kForward, fwd_kernel<S, D>, grid, dim3(256), (unsigned)lds, s, (const S *)q,
-                  (const S *)k, (const S *)v, (S *)o, lse, T, W, rt, scale_log2);
+                  (const S *)k, (const S *)v, (S *)o, lse, T, W, rt, scale_log2, hd);
 }
 
 hipError_t launch_forward(int dtype, int D, const void *q, const void *k, const void *v, void *o,
-                          float *lse, int BH, int T, int W, const RungTable &rt, hipStream_t s) {
-    if (forward_mfma_supported(dtype, D, W)) return launch_forward_mfma(q, k, v, o, lse, BH, T, W, rt, s);
-    if (dtype == 0 && D == 32) return launch_fwd_t<float, 32>(q, k, v, o, lse, BH, T, W, rt, s);
-    if (dtype == 0 && D == 64) return launch_fwd_t<float, 64>(q, k, v, o, lse, BH, T, W, rt, s);
-    if (dtype == 1 && D == 32) return launch_fwd_t<uint16_t, 32>(q, k, v, o, lse, BH, T, W, rt, s);
-    if (dtype == 1 && D == 64) return launch_fwd_t<uint16_t, 64>(q, k, v, o, lse, BH, T, W, rt, s);
+                          float *lse, int BH, const Heads &hd, int T, int W, const RungTable &rt,
+                          hipStream_t s) {
+    if (forward_mfma_supported(dtype, D, W)) return launch_forward_mfma(q, k, v, o, lse, BH, hd, T, W, rt, s);
+    if (dtype == 0 && D == 32) return launch_fwd_t<float, 32>(q, k, v, o, lse, BH, hd, T, W, rt, s);
+    if (dtype == 0 && D == 64) return launch_fwd_t<float, 64>(q, k, v, o, lse, BH, hd, T, W, rt, s);
+    if (dtype == 1 && D == 32) return launch_fwd_t<uint16_t, 32>(q, k, v, o, lse, BH, hd, T, W, rt, s);
+    if (dtype == 1 && D == 64) return launch_fwd_t<uint16_t, 64>(q, k, v, o, lse, BH, hd, T, W, rt, s);
     return hipErrorInvalidValue;
 }
 

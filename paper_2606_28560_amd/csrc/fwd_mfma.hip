@@ -29,7 +29,7 @@ template <bool INTERP>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void fwd_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     uint16_t *__restrict__ o, float *__restrict__ lse, int T, int W, RungTable rt, float sl2,
-    int tiles) {
+    int tiles, Heads hd) {
     constexpr int RB = INTERP ? 1 : 2;  // rungs per load batch; two batches in flight
     constexpr int NS = INTERP ? 2 : 1;  // rows per rung (r0, and r1 when interpolating)
     __shared__ __align__(16) uint16_t kr[kBandRows * kD];
@@ -43,9 +43,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     const int bh = blk / tiles;
     const int T0 = (blk % tiles) * kFwdBQ;
     const size_t off = (size_t)bh * T * kD;
+    const size_t kvoff = (size_t)hd.kv_of(bh) * T * kD;
     const uint16_t *Q = q + off;
-    const uint16_t *K = k + off;
-    const uint16_t *V = v + off;
+    const uint16_t *K = k + kvoff;
+    const uint16_t *V = v + kvoff;
 
     const int t0 = T0 + 16 * wv;
     const int last = t0 + 15;  // the wave's last query
@@ -194,11 +195,12 @@ static bool any_interp(const RungTable &rt) {
 bool forward_mfma_supported(int dtype, int D, int W) { return dtype == 1 && D == 64 && W <= 16; }
 
 hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void *o, float *lse,
-                               int BH, int T, int W, const RungTable &rt, hipStream_t s) {
+                               int BH, const Heads &hd, int T, int W, const RungTable &rt,
+                               hipStream_t s) {
     const int tiles = (T + kFwdBQ - 1) / kFwdBQ;
     const float sl2 = kLog2e / sqrtf(64.f);
     return launch(kForward, any_interp(rt) ? fwd_bf16_d64_kernel<true> : fwd_bf16_d64_kernel<false>,
-                  dim3(tiles * BH), dim3(256), 0, s, q, k, v, o, lse, T, W, rt, sl2, tiles);
+                  dim3(tiles * BH), dim3(256), 0, s, q, k, v, o, lse, T, W, rt, sl2, tiles, hd);
 }
 
 }  // namespace fibattn

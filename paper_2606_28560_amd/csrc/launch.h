@@ -30,8 +30,10 @@ hipError_t launch(int id, void (*kernel)(P...), dim3 grid, dim3 block, unsigned 
 }
 
 // dtype: 0 float32, 1 bfloat16.  All launchers return hipGetLastError() of their launches.
+// BH = batch * query heads; k, v (and dk, dv) hold BH / hd.G heads.
 hipError_t launch_forward(int dtype, int D, const void *q, const void *k, const void *v, void *o,
-                          float *lse, int BH, int T, int W, const RungTable &rt, hipStream_t s);
+                          float *lse, int BH, const Heads &hd, int T, int W, const RungTable &rt,
+                          hipStream_t s);
 
 // Number of dalpha partials the dq kernel writes (one per workgroup).
 size_t bwd_num_partials(int dtype, int D, int BH, int T);
@@ -39,19 +41,21 @@ size_t bwd_num_partials(int dtype, int D, int BH, int T);
 hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const void *v,
                            const void *o, const float *lse, const void *dO, void *dq, void *dk,
                            void *dv, float *dalpha, float *delta_ws, double *partials, int BH,
-                           int T, int W, const RungTable &rt, const RopeFreq &rf, float rope_base,
-                           hipStream_t s);
+                           const Heads &hd, int T, int W, const RungTable &rt, const RopeFreq &rf,
+                           float rope_base, hipStream_t s);
 
 // bfloat16, d_head = 64, W <= 16: matrix-core band + VALU rungs (fwd_mfma.hip, bwd_mfma.hip).
 bool forward_mfma_supported(int dtype, int D, int W);
 hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void *o, float *lse,
-                               int BH, int T, int W, const RungTable &rt, hipStream_t s);
+                               int BH, const Heads &hd, int T, int W, const RungTable &rt,
+                               hipStream_t s);
 bool backward_mfma_supported(int dtype, int D, int W);
 size_t bwd_mfma_num_partials(int BH, int T);
 hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, const void *o,
                                 const float *lse, const void *dO, void *dq, void *dk, void *dv,
-                                float *dalpha, float *delta_ws, double *partials, int BH, int T,
-                                int W, const RungTable &rt, const RopeFreq &rf, hipStream_t s);
+                                float *dalpha, float *delta_ws, double *partials, int BH,
+                                const Heads &hd, int T, int W, const RungTable &rt,
+                                const RopeFreq &rf, hipStream_t s);
 
 RopeFreq make_rope_freq(double rope_base, int D);  // on = 0 when rope_base <= 0
 

@@ -21,8 +21,8 @@ MAX_RUNGS = 32
 MAX_WINDOW = 128
 KERNEL_IDS = {"rope": 0, "forward": 1, "bwd_dq": 2, "bwd_dkdv": 3, "dalpha_reduce": 4}
 EXPORTED = ("fibattn_rung_table", "fibattn_forward", "fibattn_backward_workspace_bytes",
-            "fibattn_backward", "fibattn_rope", "fibattn_rope_qk", "fibattn_status_string",
-            "fibattn_timing_begin", "fibattn_timing_end")
+            "fibattn_backward", "fibattn_forward_gqa", "fibattn_backward_gqa", "fibattn_rope",
+            "fibattn_rope_qk", "fibattn_status_string", "fibattn_timing_begin", "fibattn_timing_end")
 
 
 class FibattnError(RuntimeError):
@@ -55,6 +55,11 @@ def lib():
     L.fibattn_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                    i, i, i, i, i, ip, i, f, f, i, vp]
     L.fibattn_backward.restype = i
+    L.fibattn_forward_gqa.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, ip, i, f, i, vp]
+    L.fibattn_forward_gqa.restype = i
+    L.fibattn_backward_gqa.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+                                       i, i, i, i, i, i, ip, i, f, f, i, vp]
+    L.fibattn_backward_gqa.restype = i
     L.fibattn_rope.argtypes = [vp, vp, i, i, i, i, f, i, i, vp]
     L.fibattn_rope.restype = i
     L.fibattn_rope_qk.argtypes = [vp, vp, vp, vp, i, i, i, i, f, i, vp]
@@ -123,13 +128,26 @@ def fibattn_rung_table(alpha: float, base, W: int):
     return [(int(d0[a]), np.float32(w[a]), int(f[a])) for a in range(n.value)]
 
 
+def _kv_heads(q, k):
+    """Key/value head count: k, v are [B,H_kv,T,D] with H_kv dividing H (grouped heads)."""
+    B, H, T, D = q.shape
+    if k.dim() != 4 or k.shape[0] != B or tuple(k.shape[2:]) != (T, D) or k.shape[1] < 1 \
+            or H % k.shape[1]:
+        raise ValueError(f"k: shape {tuple(k.shape)} does not group q {tuple(q.shape)}")
+    return k.shape[1]
+
+
 def fibattn_forward(q, k, v, W: int, base, alpha: float, *, o=None, lse=None, stream=None):
-    """o, lse = forward of post-RoPE q, k and v ([B,H,T,D], float32 or bfloat16)."""
+    """o, lse = forward of post-RoPE q, k and v (float32 or bfloat16).
+
+    q: [B,H,T,D]; k, v: [B,H_kv,T,D] with H_kv dividing H (H_kv < H: grouped heads)."""
     import torch
 
     B, H, T, D = q.shape
-    for n_, t in (("q", q), ("k", k), ("v", v)):
-        _check_tensor(n_, t, q.shape, q.dtype)
+    Hkv = _kv_heads(q, k)
+    _check_tensor("q", q, q.shape, q.dtype)
+    for n_, t in (("k", k), ("v", v)):
+        _check_tensor(n_, t, (B, Hkv, T, D), q.dtype)
     if o is None:
         o = torch.empty_like(q)
     if lse is None:
@@ -137,10 +155,14 @@ def fibattn_forward(q, k, v, W: int, base, alpha: float, *, o=None, lse=None, st
     _check_tensor("o", o, q.shape, q.dtype)
     _check_tensor("lse", lse, (B, H, T), torch.float32)
     b, bp = _base_array(base)
-    st = lib().fibattn_forward(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
-                               B, H, T, D, int(W), bp, b.size, ctypes.c_float(alpha),
-                               _dtype_code(q), _stream(stream))
-    _check("fibattn_forward", st)
+    ptrs = (q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr())
+    tail = (T, D, int(W), bp, b.size, ctypes.c_float(alpha), _dtype_code(q), _stream(stream))
+    if Hkv == H:
+        st = lib().fibattn_forward(*ptrs, B, H, *tail)
+        _check("fibattn_forward", st)
+    else:
+        st = lib().fibattn_forward_gqa(*ptrs, B, H, Hkv, *tail)
+        _check("fibattn_forward_gqa", st)
     return o, lse
 
 
@@ -152,30 +174,40 @@ def fibattn_backward(q, k, v, o, lse, dO, W: int, base, alpha: float, *, dq=None
                      dalpha=None, workspace=None, rope_base: float = 0.0, stream=None):
     """dq, dk, dv, dalpha (a 1-element float32 device tensor).
 
-    rope_base > 0: dq, dk are returned w.r.t. the unrotated q, k (R^T applied)."""
+    k, v (and dk, dv) may have fewer heads than q (grouped heads; dk, dv then sum over
+    each group).  rope_base > 0: dq, dk are returned w.r.t. the unrotated q, k (R^T
+    applied)."""
     import torch
 
     B, H, T, D = q.shape
-    for n_, t in (("q", q), ("k", k), ("v", v), ("o", o), ("dO", dO)):
-        _check_tensor(n_, t, q.shape, q.dtype)
+    Hkv = _kv_heads(q, k)
+    kvs = (B, Hkv, T, D)
+    for n_, t, sh in (("q", q, q.shape), ("k", k, kvs), ("v", v, kvs), ("o", o, q.shape),
+                      ("dO", dO, q.shape)):
+        _check_tensor(n_, t, sh, q.dtype)
     _check_tensor("lse", lse, (B, H, T), torch.float32)
     dq = torch.empty_like(q) if dq is None else dq
-    dk = torch.empty_like(q) if dk is None else dk
-    dv = torch.empty_like(q) if dv is None else dv
-    for n_, t in (("dq", dq), ("dk", dk), ("dv", dv)):
-        _check_tensor(n_, t, q.shape, q.dtype)
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    for n_, t, sh in (("dq", dq, q.shape), ("dk", dk, kvs), ("dv", dv, kvs)):
+        _check_tensor(n_, t, sh, q.dtype)
     if dalpha is None:
         dalpha = torch.empty(1, device=q.device, dtype=torch.float32)
     b, bp = _base_array(base)
     need = fibattn_backward_workspace_bytes(B, H, T, D, W, b.size)
     if workspace is None:
         workspace = torch.empty(max(need, 1), device=q.device, dtype=torch.uint8)
-    st = lib().fibattn_backward(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
-                                dO.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
-                                dalpha.data_ptr(), workspace.data_ptr(), workspace.numel(),
-                                B, H, T, D, int(W), bp, b.size, ctypes.c_float(alpha),
-                                ctypes.c_float(rope_base), _dtype_code(q), _stream(stream))
-    _check("fibattn_backward", st)
+    ptrs = (q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), dO.data_ptr(),
+            dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), dalpha.data_ptr(), workspace.data_ptr(),
+            workspace.numel())
+    tail = (T, D, int(W), bp, b.size, ctypes.c_float(alpha), ctypes.c_float(rope_base),
+            _dtype_code(q), _stream(stream))
+    if Hkv == H:
+        st = lib().fibattn_backward(*ptrs, B, H, *tail)
+        _check("fibattn_backward", st)
+    else:
+        st = lib().fibattn_backward_gqa(*ptrs, B, H, Hkv, *tail)
+        _check("fibattn_backward_gqa", st)
     return dq, dk, dv, dalpha
 
 

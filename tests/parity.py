@@ -38,7 +38,7 @@ def gpu_run(q, k, v, dO, W, base, alpha, backward=True, poison=True):
     out = {"o": o, "lse": lse}
     if backward:
         G = to_gpu(dO)
-        dq, dk, dv = (torch.empty_like(Q) for _ in range(3))
+        dq, dk, dv = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
         da = torch.empty(1, device="cuda", dtype=torch.float32)
         if poison:
             for t in (dq, dk, dv, da):

@@ -118,5 +118,10 @@ def test_invalid_arguments_return_codes_without_gpu():
     assert L.fibattn_rope_qk(16, 16, 16, None, 1, 1, 8, 64, ctypes.c_float(1e4), 1, None) == 1
     assert L.fibattn_rope_qk(16, 16, 16, 16, 1, 1, 8, 64, ctypes.c_float(1.0), 1, None) == 1
     assert L.fibattn_rope_qk(16, 16, 16, 16, 1, 1, 8, 48, ctypes.c_float(1e4), 1, None) == 2
+    # grouped heads: H_kv must divide H
+    for hkv in (0, 3, 16):
+        assert L.fibattn_forward_gqa(16, 16, 16, 16, 16, 1, 8, hkv, 8, 64, 8, b, 15, one, 1, None) == 1
+        assert L.fibattn_backward_gqa(16, 16, 16, 16, 16, 16, 16, 16, 16, 16, 16, 1 << 30,
+                                      1, 8, hkv, 8, 64, 8, b, 15, one, zero, 1, None) == 1
     for s in range(5):
         assert F.status_string(s)

@@ -161,6 +161,72 @@ def test_pipeline_with_rope(dtype, D, W, alpha):
             dtype, f"pipeline {dtype} D{D} W{W}")
 
 
+GQA = [
+    # (B, H, H_kv, T, D, dtype, W, base, alpha): grouped key/value heads.  bf16 d64
+    # W<=16 runs the matrix-core kernels, whose dk/dv workgroup takes 4, 2 or 1 query
+    # heads of a group side by side (G = 4, 8: four; G = 2: two; G = 3: one at a time)
+    (2, 4, 2, 333, 32, "fp32", 8, FIB, 0.7310586),
+    (1, 4, 1, 300, 64, "fp32", 6, FIB, 1.0),
+    (2, 4, 2, 300, 64, "bf16", 8, FIB, 1.0),
+    (1, 8, 2, 333, 64, "bf16", 8, FIB, 0.9),
+    (1, 8, 1, 290, 64, "bf16", 10, POW2, 1.3),
+    (1, 6, 2, 257, 64, "bf16", 8, FIB, 1.0),
+    (1, 6, 2, 257, 64, "bf16", 12, FIB, 0.75),
+    (1, 4, 2, 150, 64, "bf16", 20, FIB, 1.1),
+]
+
+
+def _gqa_inputs(B, H, Hkv, T, D, dtype, seed):
+    x = inputs.attention_inputs(B, H, T, D, dtype, 300 + seed, 0, names=("q", "dO"))
+    x.update(inputs.attention_inputs(B, Hkv, T, D, dtype, 300 + seed, 0, names=("k", "v")))
+    return x
+
+
+@pytest.mark.parametrize("B,H,Hkv,T,D,dtype,W,base,alpha", GQA)
+def test_grouped_heads_parity(B, H, Hkv, T, D, dtype, W, base, alpha):
+    idx = GQA.index((B, H, Hkv, T, D, dtype, W, base, alpha))
+    print(f"gqa case {idx}: B{B} H{H} Hkv{Hkv} T{T} D{D} {dtype} W{W} alpha={alpha}", flush=True)
+    x = _gqa_inputs(B, H, Hkv, T, D, dtype, idx)
+    got = gpu_run(x["q"], x["k"], x["v"], x["dO"], W, base, alpha)
+    ref = oracle_run(x["q"], x["k"], x["v"], x["dO"], W, base, alpha)
+    assert got["dk"].shape == (B, Hkv, T, D)
+    compare(got, ref, dtype, f"gqa case {idx}")
+
+
+@pytest.mark.parametrize("alpha", [1.0, 0.7])
+def test_grouped_heads_full_size(alpha):
+    # the 60M model's layer with its 2 key/value heads: B = 8, H = 8, T = 1024
+    print(f"gqa full size alpha={alpha}", flush=True)
+    x = _gqa_inputs(8, 8, 2, 1024, 64, "bf16", 50 + int(alpha * 10))
+    got = gpu_run(x["q"], x["k"], x["v"], x["dO"], 8, FIB, alpha)
+    ref = oracle_run(x["q"], x["k"], x["v"], x["dO"], 8, FIB, alpha)
+    compare(got, ref, "bf16", f"gqa full alpha {alpha}")
+
+
+@pytest.mark.parametrize("dtype,D,W,alpha", [("bf16", 64, 8, 0.85), ("fp32", 32, 6, 1.0)])
+def test_grouped_heads_pipeline_with_rope(dtype, D, W, alpha):
+    # RoPE of q (4 heads) and k (2 heads), attention, backward with R^T fused: dk is
+    # the group sum, rotated back
+    B, H, Hkv, T = 1, 4, 2, 200
+    x = _gqa_inputs(B, H, Hkv, T, D, dtype, 90 + D)
+    Q = F.fibattn_rope(x["q"].cuda(), 10000.0)
+    K = F.fibattn_rope(x["k"].cuda(), 10000.0)
+    V, G = x["v"].cuda(), x["dO"].cuda()
+    o, lse = F.fibattn_forward(Q, K, V, W, FIB, alpha)
+    dq, dk, dv, da = F.fibattn_backward(Q, K, V, o, lse, G, W, FIB, alpha, rope_base=10000.0)
+    torch.cuda.synchronize()
+    rq, rk = oracle.rope(x["q"]), oracle.rope(x["k"])
+    rq, rk = (inputs.round_to(r.astype(np.float32), dtype).double().numpy() for r in (rq, rk))
+    ro, rl = oracle.forward(rq, rk, x["v"], W, FIB, alpha)
+    rdq, rdk, rdv, rda, l1 = oracle.backward(rq, rk, x["v"], x["dO"], W, FIB, alpha)
+    rdq, rdk = oracle.rope(rdq, transpose=True), oracle.rope(rdk, transpose=True)
+    got = {"o": o, "lse": lse, "dq": dq, "dk": dk, "dv": dv}
+    got = {kk: vv.double().cpu().numpy() for kk, vv in got.items()}
+    got["dalpha"] = float(da.item())
+    compare(got, {"o": ro, "lse": rl, "dq": rdq, "dk": rdk, "dv": rdv, "dalpha": rda, "l1": l1},
+            dtype, f"gqa pipeline {dtype} D{D}")
+
+
 def test_rope_qk_matches_two_single_launches():
     x = _case_inputs(2, 3, 333, 64, "bf16", 52)
     q, k = x["q"].cuda(), x["k"].cuda()
