@@ -145,6 +145,48 @@ fibattn_status_t fibattn_backward_gqa(const void *q, const void *k, const void *
                                       fibattn_dtype_t dtype, hipStream_t stream);
 
 /*
+ * Device-resident alpha (Section 2, "The per-layer scalar": alpha = 0.5 + sigmoid(theta)
+ * with theta learned per layer), so that a training step never reads alpha on the host.
+ *
+ * fibattn_device_table builds, on the stream, the rung table of *alpha (a device
+ * float) for a host base table (same rules and errors as fibattn_rung_table, checked
+ * on the host) and window W into `table`, a caller-owned device buffer of
+ * fibattn_device_table_bytes() bytes, 16-byte aligned.  The table is read by
+ * fibattn_forward_dt / fibattn_backward_dt, which take it in place of (base, K, alpha)
+ * and otherwise behave as fibattn_forward_gqa / fibattn_backward_gqa; W must be the
+ * one the table was built with.  A table may hold any weights, so these calls always
+ * run the interpolating kernels.  An alpha that is not finite and positive yields a
+ * table that makes every output (o, lse, dq, dk, dv, dalpha) NaN.
+ *
+ * fibattn_alpha_from_theta: alpha[l] = 0.5 + sigmoid(theta[l]), l < n (sigmoid in
+ * float64, rounded once to float32).  fibattn_dtheta: dtheta[l] = dalpha[l] *
+ * sigmoid(theta[l]) (1 - sigmoid(theta[l])).  All pointers are device float32 arrays.
+ */
+size_t fibattn_device_table_bytes(void);
+
+fibattn_status_t fibattn_device_table(const float *alpha, const int32_t *base, int K, int W,
+                                      void *table, hipStream_t stream);
+
+fibattn_status_t fibattn_forward_dt(const void *q, const void *k, const void *v,
+                                    void *o, float *lse,
+                                    int B, int H, int H_kv, int T, int d_head, int W,
+                                    const void *table, fibattn_dtype_t dtype, hipStream_t stream);
+
+fibattn_status_t fibattn_backward_dt(const void *q, const void *k, const void *v,
+                                     const void *o, const float *lse, const void *dO,
+                                     void *dq, void *dk, void *dv, float *dalpha,
+                                     void *workspace, size_t workspace_bytes,
+                                     int B, int H, int H_kv, int T, int d_head, int W,
+                                     const void *table, float rope_base,
+                                     fibattn_dtype_t dtype, hipStream_t stream);
+
+fibattn_status_t fibattn_alpha_from_theta(const float *theta, float *alpha, int n,
+                                          hipStream_t stream);
+
+fibattn_status_t fibattn_dtheta(const float *theta, const float *dalpha, float *dtheta, int n,
+                                hipStream_t stream);
+
+/*
  * RoPE at the true positions t = 0..T-1 (Section 2 "Attended set"; base 1e4 in
  * Section 3).  Rotate-half pairing: (x_j, x_{j+D/2}) rotates by the angle
  * t * rope_base^(-2j/D), j < D/2; angles are evaluated in float64 and their cosine
@@ -170,9 +212,10 @@ const char *fibattn_status_string(fibattn_status_t status);
 
 /*
  * Kernel timing (instrumentation for benchmarks; not thread-safe).
- * fibattn_timing_begin(id, capacity) makes the library record a HIP event pair
- * on the launch stream around each of the next `capacity` launches of kernel `id`
- * (0 rope, 1 forward, 2 backward dq+dalpha, 3 backward dk/dv, 4 dalpha reduce).
+ * fibattn_timing_begin(id, capacity) makes the library launch each of the next
+ * `capacity` launches of kernel `id` with a HIP event pair that takes the dispatch's
+ * own start and end timestamps on the launch stream (0 rope, 1 forward, 2 backward
+ * dq+dalpha, 3 backward dk/dv, 4 dalpha reduce, 5 device-alpha kernels).
  * fibattn_timing_end(&avg_ms, &count) synchronises on the last event, returns
  * the mean launch duration and the number of launches timed, and stops timing.
  */

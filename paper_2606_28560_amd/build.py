@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libfibattn.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-SOURCES = ["api.hip", "fwd.hip", "bwd.hip", "rope.hip", "fwd_mfma.hip", "bwd_mfma.hip"]
+SOURCES = ["api.hip", "fwd.hip", "bwd.hip", "rope.hip", "fwd_mfma.hip", "bwd_mfma.hip", "alpha.hip"]
 
 CFLAGS = [
     "--offload-arch=gfx950",

@@ -14,32 +14,25 @@ using namespace fibattn;
 
 namespace {
 
-// d_k = fl32(alpha * f_k) as one float32 multiply (volatile keeps the product a
-// separately rounded float even under aggressive host optimisation).
-fibattn_status_t build_table(float alpha, const int32_t *base, int K, int W, RungTable *rt) {
+// The base table's own rules (Section 2): K <= FIBATTN_MAX_RUNGS, entries >= 1 and
+// strictly increasing.
+fibattn_status_t check_base(const int32_t *base, int K, BaseTable *b) {
     if (K < 0 || K > FIBATTN_MAX_RUNGS || (K > 0 && base == nullptr)) return FIBATTN_ERR_INVALID_ARG;
-    if (!(alpha > 0.f) || !isfinite(alpha)) return FIBATTN_ERR_INVALID_ARG;
-    memset(rt, 0, sizeof(*rt));  // unused entries are read (and masked) by batched kernels
-    int n = 0;
-    float last = -1.f;
+    b->K = K;
+    for (int a = 0; a < kMaxRungs; ++a) b->f[a] = 0;
     for (int a = 0; a < K; ++a) {
         if (base[a] < 1) return FIBATTN_ERR_INVALID_ARG;
         if (a > 0 && base[a] <= base[a - 1]) return FIBATTN_ERR_INVALID_ARG;
-        volatile float fa = (float)base[a];
-        volatile float d = alpha * fa;
-        const float dd = d;
-        if (!isfinite(dd) || dd > 2147483520.f) return FIBATTN_ERR_INVALID_ARG;
-        if (!(dd > (float)W)) continue;   // coincides with the window: union, not counted twice
-        if (n > 0 && dd == last) continue;  // equal distances are one entry
-        const float fl = floorf(dd);
-        rt->d0[n] = (int)fl;
-        rt->w[n] = dd - fl;               // exact in float32
-        rt->f[n] = base[a];
-        last = dd;
-        ++n;
+        b->f[a] = base[a];
     }
-    rt->n = n;
     return FIBATTN_OK;
+}
+
+fibattn_status_t build_table(float alpha, const int32_t *base, int K, int W, RungTable *rt) {
+    BaseTable b;
+    fibattn_status_t st = check_base(base, K, &b);
+    if (st != FIBATTN_OK) return st;
+    return rung_table_fill(alpha, b, W, rt) ? FIBATTN_OK : FIBATTN_ERR_INVALID_ARG;
 }
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
@@ -105,7 +98,8 @@ fibattn_status_t fibattn_forward_gqa(const void *q, const void *k, const void *v
     st = build_table(alpha, base, K, W, &rt);
     if (st != FIBATTN_OK) return st;
     const Heads hd{H, H / H_kv};
-    hipError_t e = launch_forward((int)dtype, d_head, q, k, v, o, lse, B * H, hd, T, W, rt, stream);
+    hipError_t e = launch_forward((int)dtype, d_head, q, k, v, o, lse, B * H, hd, T, W, rt, nullptr,
+                                  stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
 }
 
@@ -153,7 +147,8 @@ fibattn_status_t fibattn_backward_gqa(const void *q, const void *k, const void *
     const RopeFreq rf = make_rope_freq((double)rope_base, d_head);
     const Heads hd{H, H / H_kv};
     hipError_t e = launch_backward((int)dtype, d_head, q, k, v, o, lse, dO, dq, dk, dv, dalpha,
-                                   delta_ws, partials, B * H, hd, T, W, rt, rf, rope_base, stream);
+                                   delta_ws, partials, B * H, hd, T, W, rt, nullptr, rf, rope_base,
+                                   stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
 }
 
@@ -165,6 +160,81 @@ fibattn_status_t fibattn_backward(const void *q, const void *k, const void *v, c
                                   hipStream_t stream) {
     return fibattn_backward_gqa(q, k, v, o, lse, dO, dq, dk, dv, dalpha, workspace, workspace_bytes,
                                 B, H, H, T, d_head, W, base, K, alpha, rope_base, dtype, stream);
+}
+
+// ---- device-resident alpha -------------------------------------------------------
+
+size_t fibattn_device_table_bytes(void) { return align256(sizeof(RungTable)); }
+
+fibattn_status_t fibattn_device_table(const float *alpha, const int32_t *base, int K, int W,
+                                      void *table, hipStream_t stream) {
+    if (!alpha || !table || !aligned16(table) || W < 0 || W > FIBATTN_MAX_WINDOW)
+        return FIBATTN_ERR_INVALID_ARG;
+    BaseTable b;
+    fibattn_status_t st = check_base(base, K, &b);
+    if (st != FIBATTN_OK) return st;
+    hipError_t e = launch_rung_table(alpha, b, W, (RungTable *)table, stream);
+    return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
+fibattn_status_t fibattn_forward_dt(const void *q, const void *k, const void *v, void *o, float *lse,
+                                    int B, int H, int H_kv, int T, int d_head, int W,
+                                    const void *table, fibattn_dtype_t dtype, hipStream_t stream) {
+    fibattn_status_t st = check_common(B, H, T, d_head, W, 0, dtype);
+    if (st != FIBATTN_OK) return st;
+    if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
+    if (!q || !k || !v || !o || !lse || !table) return FIBATTN_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse) ||
+        !aligned16(table))
+        return FIBATTN_ERR_INVALID_ARG;
+    RungTable unused;
+    memset(&unused, 0, sizeof(unused));
+    const Heads hd{H, H / H_kv};
+    hipError_t e = launch_forward((int)dtype, d_head, q, k, v, o, lse, B * H, hd, T, W, unused,
+                                  (const RungTable *)table, stream);
+    return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
+fibattn_status_t fibattn_backward_dt(const void *q, const void *k, const void *v, const void *o,
+                                     const float *lse, const void *dO, void *dq, void *dk, void *dv,
+                                     float *dalpha, void *workspace, size_t workspace_bytes, int B,
+                                     int H, int H_kv, int T, int d_head, int W, const void *table,
+                                     float rope_base, fibattn_dtype_t dtype, hipStream_t stream) {
+    fibattn_status_t st = check_common(B, H, T, d_head, W, 0, dtype);
+    if (st != FIBATTN_OK) return st;
+    if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
+    if (!q || !k || !v || !o || !lse || !dO || !dq || !dk || !dv || !dalpha || !table)
+        return FIBATTN_ERR_INVALID_ARG;
+    const void *ptrs[] = {q, k, v, o, lse, dO, dq, dk, dv, table};
+    for (const void *p : ptrs)
+        if (!aligned16(p)) return FIBATTN_ERR_INVALID_ARG;
+    if (!(rope_base == 0.f || (rope_base > 1.f && isfinite(rope_base)))) return FIBATTN_ERR_INVALID_ARG;
+    if (!workspace || !aligned16(workspace) ||
+        workspace_bytes < fibattn_backward_workspace_bytes(B, H, T, d_head, W, 0))
+        return FIBATTN_ERR_WORKSPACE;
+    RungTable unused;
+    memset(&unused, 0, sizeof(unused));
+    float *delta_ws = (float *)workspace;
+    double *partials = (double *)((char *)workspace + align256(sizeof(float) * (size_t)B * H * T));
+    const RopeFreq rf = make_rope_freq((double)rope_base, d_head);
+    const Heads hd{H, H / H_kv};
+    hipError_t e = launch_backward((int)dtype, d_head, q, k, v, o, lse, dO, dq, dk, dv, dalpha,
+                                   delta_ws, partials, B * H, hd, T, W, unused,
+                                   (const RungTable *)table, rf, rope_base, stream);
+    return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
+fibattn_status_t fibattn_alpha_from_theta(const float *theta, float *alpha, int n, hipStream_t stream) {
+    if (!theta || !alpha || n < 1) return FIBATTN_ERR_INVALID_ARG;
+    hipError_t e = launch_alpha_from_theta(theta, alpha, n, stream);
+    return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
+fibattn_status_t fibattn_dtheta(const float *theta, const float *dalpha, float *dtheta, int n,
+                                hipStream_t stream) {
+    if (!theta || !dalpha || !dtheta || n < 1) return FIBATTN_ERR_INVALID_ARG;
+    hipError_t e = launch_dtheta(theta, dalpha, dtheta, n, stream);
+    return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
 }
 
 fibattn_status_t fibattn_rope(const void *x, void *y, int B, int H, int T, int d_head,

@@ -25,12 +25,15 @@ namespace fibattn {
 // ---------------------------------------------------------------------------
 // dq, Delta and per-workgroup dalpha partials.
 // ---------------------------------------------------------------------------
-template <typename S, int D>
+// DEV: the rung table is the one at rtp, built on the device (rt_arg unused).
+template <typename S, int D, bool DEV>
 __global__ __launch_bounds__(256) void bwd_dq_kernel(
     const S *__restrict__ q, const S *__restrict__ k, const S *__restrict__ v,
     const S *__restrict__ o, const float *__restrict__ lse, const S *__restrict__ dO,
     S *__restrict__ dq, float *__restrict__ delta_out, double *__restrict__ partials, int T,
-    int W, RungTable rt, float tau, Heads hd) {
+    int W, RungTable rt_arg, const RungTable *__restrict__ rtp, float tau, Heads hd) {
+    const RungTable &rt = DEV ? *rtp : rt_arg;
+    const bool bad = DEV && rt.n < 0;  // a device alpha that is not finite and positive
     constexpr int VN = Vec<S>::N;
     constexpr int LPQ = D / VN;
     constexpr int QPB = 256 / LPQ;
@@ -54,7 +57,7 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(
         Vec<S>::load(dO + off + (size_t)i * D + col, gv);
         Vec<S>::load(o + off + (size_t)i * D + col, kv);
         const float delta = group_sum<LPQ>(dot<VN>(gv, kv));
-        if (sub == 0) delta_out[(size_t)blockIdx.y * T + i] = delta;
+        if (sub == 0) delta_out[(size_t)blockIdx.y * T + i] = bad ? NAN : delta;
         const float lse2 = lse[(size_t)blockIdx.y * T + i] * kLog2e;
 #pragma unroll
         for (int c = 0; c < VN; ++c) acc[c] = 0.f;
@@ -102,6 +105,11 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(
             const float gw = c * (s1 - s0) + p * (dP1 - dP0);
             dal += (double)rt.f[r] * (double)gw;
         }
+        if (bad) {
+#pragma unroll
+            for (int x = 0; x < VN; ++x) acc[x] = NAN;
+            dal = NAN;
+        }
         Vec<S>::store(dq + off + (size_t)i * D + col, acc);
     }
     red[threadIdx.x] = (sub == 0 && i < T) ? dal : 0.0;
@@ -117,11 +125,13 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(
 // ---------------------------------------------------------------------------
 // dk, dv: one key row per lane group.
 // ---------------------------------------------------------------------------
-template <typename S, int D>
+template <typename S, int D, bool DEV>
 __global__ __launch_bounds__(256) void bwd_dkdv_kernel(
     const S *__restrict__ q, const S *__restrict__ k, const S *__restrict__ v,
     const float *__restrict__ lse, const S *__restrict__ dO, const float *__restrict__ delta_in,
-    S *__restrict__ dk, S *__restrict__ dv, int T, int W, RungTable rt, float tau, Heads hd) {
+    S *__restrict__ dk, S *__restrict__ dv, int T, int W, RungTable rt_arg,
+    const RungTable *__restrict__ rtp, float tau, Heads hd) {
+    const RungTable &rt = DEV ? *rtp : rt_arg;
     constexpr int VN = Vec<S>::N;
     constexpr int LPQ = D / VN;
     constexpr int QPB = 256 / LPQ;
@@ -218,6 +228,10 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(
             }
         }
     }
+    if (DEV && rt.n < 0) {  // a device alpha that is not finite and positive
+#pragma unroll
+        for (int x = 0; x < VN; ++x) { adk[x] = NAN; adv[x] = NAN; }
+    }
     Vec<S>::store(dk + kvoff + (size_t)j * D + col, adk);
     Vec<S>::store(dv + kvoff + (size_t)j * D + col, adv);
 }
@@ -258,17 +272,18 @@ template <typename S, int D>
 static hipError_t launch_bwd_t(const void *q, const void *k, const void *v, const void *o,
                                const float *lse, const void *dO, void *dq, void *dk, void *dv,
                                float *dalpha, float *delta_ws, double *partials, int BH,
-                               const Heads &hd, int T, int W, const RungTable &rt, hipStream_t s) {
+                               const Heads &hd, int T, int W, const RungTable &rt,
+                               const RungTable *rtp, hipStream_t s) {
     constexpr int QPB = 256 / (D / Vec<S>::N);
     const float tau = 1.f / sqrtf((float)D);
     dim3 grid((T + QPB - 1) / QPB, BH);
-    hipError_t e = launch(kBwdDq, bwd_dq_kernel<S, D>, grid, dim3(256), 0, s, (const S *)q,
-                          (const S *)k, (const S *)v, (const S *)o, lse, (const S *)dO, (S *)dq,
-                          delta_ws, partials, T, W, rt, tau, hd);
+    hipError_t e = launch(kBwdDq, rtp ? bwd_dq_kernel<S, D, true> : bwd_dq_kernel<S, D, false>, grid,
+                          dim3(256), 0, s, (const S *)q, (const S *)k, (const S *)v, (const S *)o,
+                          lse, (const S *)dO, (S *)dq, delta_ws, partials, T, W, rt, rtp, tau, hd);
     if (e != hipSuccess) return e;
-    e = launch(kBwdDkDv, bwd_dkdv_kernel<S, D>, dim3(grid.x, BH / hd.G), dim3(256), 0, s,
-               (const S *)q, (const S *)k, (const S *)v, lse, (const S *)dO, delta_ws, (S *)dk,
-               (S *)dv, T, W, rt, tau, hd);
+    e = launch(kBwdDkDv, rtp ? bwd_dkdv_kernel<S, D, true> : bwd_dkdv_kernel<S, D, false>,
+               dim3(grid.x, BH / hd.G), dim3(256), 0, s, (const S *)q, (const S *)k, (const S *)v,
+               lse, (const S *)dO, delta_ws, (S *)dk, (S *)dv, T, W, rt, rtp, tau, hd);
     if (e != hipSuccess) return e;
     return launch(kDalphaReduce, dalpha_reduce_kernel, dim3(1), dim3(256), 0, s, partials,
                   (size_t)grid.x * grid.y, dalpha);
@@ -278,10 +293,10 @@ static hipError_t launch_backward_generic(int dtype, int D, const void *q, const
                                           const void *o, const float *lse, const void *dO, void *dq,
                                           void *dk, void *dv, float *dalpha, float *delta_ws,
                                           double *partials, int BH, const Heads &hd, int T, int W,
-                                          const RungTable &rt, hipStream_t s) {
+                                          const RungTable &rt, const RungTable *rtp, hipStream_t s) {
 #define FIBATTN_BWD(S_, D_)                                                                  \
     return launch_bwd_t<S_, D_>(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials, \
-                                BH, hd, T, W, rt, s)
+                                BH, hd, T, W, rt, rtp, s)
     if (dtype == 0 && D == 32) FIBATTN_BWD(float, 32);
     if (dtype == 0 && D == 64) FIBATTN_BWD(float, 64);
     if (dtype == 1 && D == 32) FIBATTN_BWD(uint16_t, 32);
@@ -294,13 +309,13 @@ static hipError_t launch_backward_generic(int dtype, int D, const void *q, const
 hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const void *v,
                            const void *o, const float *lse, const void *dO, void *dq, void *dk,
                            void *dv, float *dalpha, float *delta_ws, double *partials, int BH,
-                           const Heads &hd, int T, int W, const RungTable &rt, const RopeFreq &rf,
-                           float rope_base, hipStream_t s) {
+                           const Heads &hd, int T, int W, const RungTable &rt,
+                           const RungTable *rtp, const RopeFreq &rf, float rope_base, hipStream_t s) {
     if (backward_mfma_supported(dtype, D, W))
         return launch_backward_mfma(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials, BH,
-                                    hd, T, W, rt, rf, s);
+                                    hd, T, W, rt, rtp, rf, s);
     hipError_t e = launch_backward_generic(dtype, D, q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws,
-                                           partials, BH, hd, T, W, rt, s);
+                                           partials, BH, hd, T, W, rt, rtp, s);
     // R^T on dq and dk in place: gradients w.r.t. the unrotated q, k (R^T is linear, so
     // it also carries the group sum in dk)
     if (e == hipSuccess && rf.on) {

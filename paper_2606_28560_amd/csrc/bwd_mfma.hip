@@ -31,13 +31,17 @@ constexpr int kBwdB = 64;                // rows per workgroup
 constexpr int kStage = kBwdB + 16;       // staged rows
 
 // ---------------------------------------------------------------------------
-// INTERP: some rung has w != 0 (rows r0 and r1 both loaded per rung).
-template <bool INTERP>
+// INTERP: some rung has w != 0 (rows r0 and r1 both loaded per rung).  DEV: the rung
+// table is the one at rtp, built on the device (rt_arg unused).
+template <bool INTERP, bool DEV>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void bwd_dq_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const uint16_t *__restrict__ o, const float *__restrict__ lse, const uint16_t *__restrict__ dO,
     uint16_t *__restrict__ dq, float *__restrict__ delta_out, double *__restrict__ partials, int T,
-    int W, RungTable rt, RopeFreq rf, float tau, int tiles, Heads hd) {
+    int W, RungTable rt_arg, const RungTable *__restrict__ rtp, RopeFreq rf, float tau, int tiles,
+    Heads hd) {
+    const RungTable &rt = DEV ? *rtp : rt_arg;
+    const bool bad = DEV && rt.n < 0;  // a device alpha that is not finite and positive
     __shared__ __align__(16) uint16_t kr[kStage * kD];
     __shared__ __align__(16) uint16_t vr[kStage * kD];
     __shared__ double sfreq[32];
@@ -180,9 +184,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 
     if (rf.on) acc_rope_t(acc, i, sfreq + 8 * gq);  // gradient w.r.t. the unrotated q
     if (i < T) {
-        store_acc(dq + off + (size_t)i * kD, gq, acc, 1.f);
-        if (gq == 0) delta_out[(size_t)bh * T + i] = delta;
+        store_acc(dq + off + (size_t)i * kD, gq, acc, bad ? NAN : 1.f);
+        if (gq == 0) delta_out[(size_t)bh * T + i] = bad ? NAN : delta;
     }
+    if (bad) dal_q = NAN;
     // workgroup dalpha partial: wave sums, then the four waves in order
     double dal = (double)dal_q;
 #pragma unroll
@@ -197,13 +202,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 // kKG = 4 / NH key groups of 16 keys times NH head slots; a group of G query heads
 // takes G / NH passes (ONE_PASS: G == NH, no pass loop), and the head slots' dk, dv
 // are summed through LDS at the end.
-template <bool INTERP, int NH, bool ONE_PASS>
+template <bool INTERP, int NH, bool ONE_PASS, bool DEV>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void bwd_dkdv_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const float *__restrict__ lse, const uint16_t *__restrict__ dO, const float *__restrict__ delta_in,
     uint16_t *__restrict__ dk, uint16_t *__restrict__ dv, const double *__restrict__ partials,
-    int n_partials, float *__restrict__ dalpha, int T, int W, RungTable rt, RopeFreq rf, float tau,
-    int tiles, Heads hd) {
+    int n_partials, float *__restrict__ dalpha, int T, int W, RungTable rt_arg,
+    const RungTable *__restrict__ rtp, RopeFreq rf, float tau, int tiles, Heads hd) {
+    const RungTable &rt = DEV ? *rtp : rt_arg;
     constexpr int kKG = 4 / NH;          // key groups of 16 per workgroup
     constexpr int kKeys = 16 * kKG;      // keys per workgroup
     constexpr int kSt = kKeys + 16;      // staged query rows per head slot
@@ -480,8 +486,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     if (hs == 0) {
         if (rf.on) acc_rope_t(adk, j_key, sfreq + 8 * gq);  // gradient w.r.t. the unrotated k
         if (j_key < T) {
-            store_acc(dk + kvoff + (size_t)j_key * kD, gq, adk, 1.f);
-            store_acc(dv + kvoff + (size_t)j_key * kD, gq, adv, 1.f);
+            const float sc = DEV && rt.n < 0 ? NAN : 1.f;  // a device alpha not finite and positive
+            store_acc(dk + kvoff + (size_t)j_key * kD, gq, adk, sc);
+            store_acc(dv + kvoff + (size_t)j_key * kD, gq, adv, sc);
         }
     }
 }
@@ -495,39 +502,44 @@ static hipError_t launch_dkdv(bool interp, const void *q, const void *k, const v
                               const float *lse, const void *dO, const float *delta_ws, void *dk,
                               void *dv, const double *partials, int n_partials, float *dalpha,
                               int BH, const Heads &hd, int T, int W, const RungTable &rt,
-                              const RopeFreq &rf, float tau, hipStream_t s) {
+                              const RungTable *rtp, const RopeFreq &rf, float tau, hipStream_t s) {
     constexpr int keys = 64 / NH;
     const int tiles = (T + keys - 1) / keys;
     const bool one = hd.G == NH;
-    auto kern = interp ? (one ? bwd_dkdv_bf16_d64_kernel<true, NH, true> : bwd_dkdv_bf16_d64_kernel<true, NH, false>)
-                       : (one ? bwd_dkdv_bf16_d64_kernel<false, NH, true> : bwd_dkdv_bf16_d64_kernel<false, NH, false>);
+    auto kern = rtp ? (one ? bwd_dkdv_bf16_d64_kernel<true, NH, true, true>
+                           : bwd_dkdv_bf16_d64_kernel<true, NH, false, true>)
+              : interp ? (one ? bwd_dkdv_bf16_d64_kernel<true, NH, true, false>
+                              : bwd_dkdv_bf16_d64_kernel<true, NH, false, false>)
+                       : (one ? bwd_dkdv_bf16_d64_kernel<false, NH, true, false>
+                              : bwd_dkdv_bf16_d64_kernel<false, NH, false, false>);
     return launch(kBwdDkDv, kern, dim3(tiles * (BH / hd.G)), dim3(256), 0, s, q, k, v, lse, dO,
-                  delta_ws, dk, dv, partials, n_partials, dalpha, T, W, rt, rf, tau, tiles, hd);
+                  delta_ws, dk, dv, partials, n_partials, dalpha, T, W, rt, rtp, rf, tau, tiles, hd);
 }
 
 hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, const void *o,
                                 const float *lse, const void *dO, void *dq, void *dk, void *dv,
                                 float *dalpha, float *delta_ws, double *partials, int BH,
                                 const Heads &hd, int T, int W, const RungTable &rt,
-                                const RopeFreq &rf, hipStream_t s) {
+                                const RungTable *rtp, const RopeFreq &rf, hipStream_t s) {
     const int tiles = (T + kBwdB - 1) / kBwdB;
     const float tau = 1.f / sqrtf(64.f);
     const int nb = tiles * BH;
-    bool interp = false;
-    for (int r = 0; r < rt.n; ++r) interp = interp || rt.w[r] != 0.f;
-    hipError_t e = launch(kBwdDq, interp ? bwd_dq_bf16_d64_kernel<true> : bwd_dq_bf16_d64_kernel<false>,
-                          dim3(nb), dim3(256), 0, s, q, k, v, o, lse, dO, dq, delta_ws, partials,
-                          T, W, rt, rf, tau, tiles, hd);
+    bool interp = rtp != nullptr;  // a device table may hold any weights
+    for (int r = 0; r < rt.n && !interp; ++r) interp = rt.w[r] != 0.f;
+    auto dqk = rtp ? bwd_dq_bf16_d64_kernel<true, true>
+                   : (interp ? bwd_dq_bf16_d64_kernel<true, false> : bwd_dq_bf16_d64_kernel<false, false>);
+    hipError_t e = launch(kBwdDq, dqk, dim3(nb), dim3(256), 0, s, q, k, v, o, lse, dO, dq, delta_ws,
+                          partials, T, W, rt, rtp, rf, tau, tiles, hd);
     if (e != hipSuccess) return e;
     // query heads per key/value head processed side by side in a workgroup
     if (hd.G % 4 == 0)
         return launch_dkdv<4>(interp, q, k, v, lse, dO, delta_ws, dk, dv, partials, nb, dalpha, BH,
-                              hd, T, W, rt, rf, tau, s);
+                              hd, T, W, rt, rtp, rf, tau, s);
     if (hd.G % 2 == 0)
         return launch_dkdv<2>(interp, q, k, v, lse, dO, delta_ws, dk, dv, partials, nb, dalpha, BH,
-                              hd, T, W, rt, rf, tau, s);
+                              hd, T, W, rt, rtp, rf, tau, s);
     return launch_dkdv<1>(interp, q, k, v, lse, dO, delta_ws, dk, dv, partials, nb, dalpha, BH, hd,
-                          T, W, rt, rf, tau, s);
+                          T, W, rt, rtp, rf, tau, s);
 }
 
 }  // namespace fibattn

@@ -10,14 +10,49 @@ constexpr int kMaxRungs = 32;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-// Rung table passed by value in the kernel arguments: the offsets every query of a
-// launch shares (floor of the distance, blend weight, base value), increasing d.
+// Rung table: the offsets every query of a launch shares (floor of the distance,
+// blend weight, base value), increasing d.  Passed by value in the kernel arguments,
+// or built on the device from a device-resident alpha (rung_table_fill).  n < 0 marks
+// a table built from an alpha that is not finite and positive: kernels then write NaN.
 struct RungTable {
     int n;
     int d0[kMaxRungs];
     float w[kMaxRungs];
     int f[kMaxRungs];
 };
+
+// A validated base table (strictly increasing, >= 1, K <= kMaxRungs) by value.
+struct BaseTable {
+    int K;
+    int f[kMaxRungs];
+};
+
+// Section 2 rung rules for a validated base: d_k = fl32(alpha * f_k) (one float32
+// multiply), a rung with d_k <= W coincides with the window and is dropped (the
+// attended set is a union), equal distances are one entry; w = d - floor(d) is exact.
+// Returns false (and an empty table with n = -1) when alpha is not finite and
+// positive or a distance overflows int.
+__host__ __device__ inline bool rung_table_fill(float alpha, const BaseTable &b, int W, RungTable *rt) {
+    for (int a = 0; a < kMaxRungs; ++a) { rt->d0[a] = 0; rt->w[a] = 0.f; rt->f[a] = 0; }
+    rt->n = -1;
+    if (!(alpha > 0.f) || !(alpha < INFINITY)) return false;
+    int n = 0;
+    float last = -1.f;
+    for (int a = 0; a < b.K; ++a) {
+        const float d = alpha * (float)b.f[a];
+        if (!(d <= 2147483520.f)) { rt->n = -1; return false; }
+        if (!(d > (float)W)) continue;     // coincides with the window
+        if (n > 0 && d == last) continue;  // equal distances are one entry
+        const float fl = floorf(d);
+        rt->d0[n] = (int)fl;
+        rt->w[n] = d - fl;
+        rt->f[n] = b.f[a];
+        last = d;
+        ++n;
+    }
+    rt->n = n;
+    return true;
+}
 
 // Grouped key/value heads (Section 3 "Model and training": 8 query heads share 2
 // key/value heads): query head h of batch b reads key/value head h / G of that batch.

@@ -16,17 +16,20 @@
 
 namespace fibattn {
 
-template <typename S, int D>
+// DEV: the rung table is the one at rtp, built on the device (rt_arg unused).
+template <typename S, int D, bool DEV>
 __global__ __launch_bounds__(256) void fwd_kernel(const S *__restrict__ q, const S *__restrict__ k,
                                                   const S *__restrict__ v, S *__restrict__ o,
                                                   float *__restrict__ lse, int T, int W,
-                                                  RungTable rt, float scale_log2, Heads hd) {
+                                                  RungTable rt_arg, const RungTable *__restrict__ rtp,
+                                                  float scale_log2, Heads hd) {
+    const RungTable &rt = DEV ? *rtp : rt_arg;
     constexpr int VN = Vec<S>::N;
     constexpr int LPQ = D / VN;
     constexpr int QPB = 256 / LPQ;
     extern __shared__ float smem[];
 
-    const int cap = W + 1 + rt.n;
+    const int cap = W + 1 + (DEV ? kMaxRungs : rt.n);  // LDS logits per query
     const int g = threadIdx.x / LPQ;
     const int sub = threadIdx.x % LPQ;
     const int i = blockIdx.x * QPB + g;
@@ -99,35 +102,38 @@ __global__ __launch_bounds__(256) void fwd_kernel(const S *__restrict__ q, const
                 for (int c = 0; c < VN; ++c) acc[c] = fmaf(p1, vv[c], acc[c]);
             }
         }
-        const float inv = 1.f / l;
+        const bool bad = DEV && rt.n < 0;  // a device alpha that is not finite and positive
+        const float inv = bad ? NAN : 1.f / l;
 #pragma unroll
         for (int c = 0; c < VN; ++c) acc[c] *= inv;
         Vec<S>::store(o + off + (size_t)i * D + col, acc);
-        if (sub == 0) lse[(size_t)blockIdx.y * T + i] = (m + log2f(l)) * kLn2;
+        if (sub == 0) lse[(size_t)blockIdx.y * T + i] = bad ? NAN : (m + log2f(l)) * kLn2;
     }
 }
 
 template <typename S, int D>
 static hipError_t launch_fwd_t(const void *q, const void *k, const void *v, void *o, float *lse,
                                int BH, const Heads &hd, int T, int W, const RungTable &rt,
-                               hipStream_t s) {
+                               const RungTable *rtp, hipStream_t s) {
     constexpr int LPQ = D / Vec<S>::N;
     constexpr int QPB = 256 / LPQ;
     dim3 grid((T + QPB - 1) / QPB, BH);
-    const size_t lds = sizeof(float) * QPB * (size_t)(W + 1 + rt.n);
+    const size_t lds = sizeof(float) * QPB * (size_t)(W + 1 + (rtp ? kMaxRungs : rt.n));
     const float scale_log2 = kLog2e / sqrtf((float)D);
-    return launch(kForward, fwd_kernel<S, D>, grid, dim3(256), (unsigned)lds, s, (const S *)q,
-                  (const S *)k, (const S *)v, (S *)o, lse, T, W, rt, scale_log2, hd);
+    return launch(kForward, rtp ? fwd_kernel<S, D, true> : fwd_kernel<S, D, false>, grid, dim3(256),
+                  (unsigned)lds, s, (const S *)q, (const S *)k, (const S *)v, (S *)o, lse, T, W, rt,
+                  rtp, scale_log2, hd);
 }
 
 hipError_t launch_forward(int dtype, int D, const void *q, const void *k, const void *v, void *o,
                           float *lse, int BH, const Heads &hd, int T, int W, const RungTable &rt,
-                          hipStream_t s) {
-    if (forward_mfma_supported(dtype, D, W)) return launch_forward_mfma(q, k, v, o, lse, BH, hd, T, W, rt, s);
-    if (dtype == 0 && D == 32) return launch_fwd_t<float, 32>(q, k, v, o, lse, BH, hd, T, W, rt, s);
-    if (dtype == 0 && D == 64) return launch_fwd_t<float, 64>(q, k, v, o, lse, BH, hd, T, W, rt, s);
-    if (dtype == 1 && D == 32) return launch_fwd_t<uint16_t, 32>(q, k, v, o, lse, BH, hd, T, W, rt, s);
-    if (dtype == 1 && D == 64) return launch_fwd_t<uint16_t, 64>(q, k, v, o, lse, BH, hd, T, W, rt, s);
+                          const RungTable *rtp, hipStream_t s) {
+    if (forward_mfma_supported(dtype, D, W))
+        return launch_forward_mfma(q, k, v, o, lse, BH, hd, T, W, rt, rtp, s);
+    if (dtype == 0 && D == 32) return launch_fwd_t<float, 32>(q, k, v, o, lse, BH, hd, T, W, rt, rtp, s);
+    if (dtype == 0 && D == 64) return launch_fwd_t<float, 64>(q, k, v, o, lse, BH, hd, T, W, rt, rtp, s);
+    if (dtype == 1 && D == 32) return launch_fwd_t<uint16_t, 32>(q, k, v, o, lse, BH, hd, T, W, rt, rtp, s);
+    if (dtype == 1 && D == 64) return launch_fwd_t<uint16_t, 64>(q, k, v, o, lse, BH, hd, T, W, rt, rtp, s);
     return hipErrorInvalidValue;
 }
 

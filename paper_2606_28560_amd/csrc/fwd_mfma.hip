@@ -24,12 +24,14 @@ constexpr int kFwdBQ = 64;                 // queries per workgroup
 constexpr int kBandRows = kFwdBQ + 16;     // staged band rows [T0-16, T0+64)
 constexpr float kSlack = 8.f;              // log2 units a logit may exceed the running reference
 
-// INTERP: some rung has w != 0, so the second row r1 is read.
-template <bool INTERP>
+// INTERP: some rung has w != 0, so the second row r1 is read.  DEV: the rung table
+// is the one at rtp, built on the device (rt_arg unused).
+template <bool INTERP, bool DEV>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void fwd_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
-    uint16_t *__restrict__ o, float *__restrict__ lse, int T, int W, RungTable rt, float sl2,
-    int tiles, Heads hd) {
+    uint16_t *__restrict__ o, float *__restrict__ lse, int T, int W, RungTable rt_arg,
+    const RungTable *__restrict__ rtp, float sl2, int tiles, Heads hd) {
+    const RungTable &rt = DEV ? *rtp : rt_arg;
     constexpr int RB = INTERP ? 1 : 2;  // rungs per load batch; two batches in flight
     constexpr int NS = INTERP ? 2 : 1;  // rows per rung (r0, and r1 when interpolating)
     __shared__ __align__(16) uint16_t kr[kBandRows * kD];
@@ -181,8 +183,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     }
 
     if (i < T) {
-        store_acc(o + off + (size_t)i * kD, gq, acc, 1.f / l);
-        if (gq == 0) lse[(size_t)bh * T + i] = (m + log2f(l)) * kLn2;
+        const bool bad = DEV && rt.n < 0;  // a device alpha that is not finite and positive
+        store_acc(o + off + (size_t)i * kD, gq, acc, bad ? NAN : 1.f / l);
+        if (gq == 0) lse[(size_t)bh * T + i] = bad ? NAN : (m + log2f(l)) * kLn2;
     }
 }
 
@@ -196,11 +199,13 @@ bool forward_mfma_supported(int dtype, int D, int W) { return dtype == 1 && D ==
 
 hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void *o, float *lse,
                                int BH, const Heads &hd, int T, int W, const RungTable &rt,
-                               hipStream_t s) {
+                               const RungTable *rtp, hipStream_t s) {
     const int tiles = (T + kFwdBQ - 1) / kFwdBQ;
     const float sl2 = kLog2e / sqrtf(64.f);
-    return launch(kForward, any_interp(rt) ? fwd_bf16_d64_kernel<true> : fwd_bf16_d64_kernel<false>,
-                  dim3(tiles * BH), dim3(256), 0, s, q, k, v, o, lse, T, W, rt, sl2, tiles, hd);
+    auto kern = rtp ? fwd_bf16_d64_kernel<true, true>
+                    : (any_interp(rt) ? fwd_bf16_d64_kernel<true, false> : fwd_bf16_d64_kernel<false, false>);
+    return launch(kForward, kern, dim3(tiles * BH), dim3(256), 0, s, q, k, v, o, lse, T, W, rt, rtp,
+                  sl2, tiles, hd);
 }
 
 }  // namespace fibattn

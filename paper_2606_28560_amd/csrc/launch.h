@@ -9,7 +9,8 @@
 
 namespace fibattn {
 
-enum KernelId { kRope = 0, kForward = 1, kBwdDq = 2, kBwdDkDv = 3, kDalphaReduce = 4, kNumKernels = 5 };
+enum KernelId { kRope = 0, kForward = 1, kBwdDq = 2, kBwdDkDv = 3, kDalphaReduce = 4, kAlpha = 5,
+                kNumKernels = 6 };
 
 // The start/stop event pair for the next launch of kernel `id` while kernel timing is
 // active for it; false otherwise.
@@ -30,10 +31,11 @@ hipError_t launch(int id, void (*kernel)(P...), dim3 grid, dim3 block, unsigned 
 }
 
 // dtype: 0 float32, 1 bfloat16.  All launchers return hipGetLastError() of their launches.
-// BH = batch * query heads; k, v (and dk, dv) hold BH / hd.G heads.
+// BH = batch * query heads; k, v (and dk, dv) hold BH / hd.G heads.  rtp != nullptr:
+// the rung table is the device-resident one at rtp (rt unused).
 hipError_t launch_forward(int dtype, int D, const void *q, const void *k, const void *v, void *o,
                           float *lse, int BH, const Heads &hd, int T, int W, const RungTable &rt,
-                          hipStream_t s);
+                          const RungTable *rtp, hipStream_t s);
 
 // Number of dalpha partials the dq kernel writes (one per workgroup).
 size_t bwd_num_partials(int dtype, int D, int BH, int T);
@@ -41,23 +43,30 @@ size_t bwd_num_partials(int dtype, int D, int BH, int T);
 hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const void *v,
                            const void *o, const float *lse, const void *dO, void *dq, void *dk,
                            void *dv, float *dalpha, float *delta_ws, double *partials, int BH,
-                           const Heads &hd, int T, int W, const RungTable &rt, const RopeFreq &rf,
-                           float rope_base, hipStream_t s);
+                           const Heads &hd, int T, int W, const RungTable &rt,
+                           const RungTable *rtp, const RopeFreq &rf, float rope_base, hipStream_t s);
 
 // bfloat16, d_head = 64, W <= 16: matrix-core band + VALU rungs (fwd_mfma.hip, bwd_mfma.hip).
 bool forward_mfma_supported(int dtype, int D, int W);
 hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void *o, float *lse,
                                int BH, const Heads &hd, int T, int W, const RungTable &rt,
-                               hipStream_t s);
+                               const RungTable *rtp, hipStream_t s);
 bool backward_mfma_supported(int dtype, int D, int W);
 size_t bwd_mfma_num_partials(int BH, int T);
 hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, const void *o,
                                 const float *lse, const void *dO, void *dq, void *dk, void *dv,
                                 float *dalpha, float *delta_ws, double *partials, int BH,
                                 const Heads &hd, int T, int W, const RungTable &rt,
-                                const RopeFreq &rf, hipStream_t s);
+                                const RungTable *rtp, const RopeFreq &rf, hipStream_t s);
 
 RopeFreq make_rope_freq(double rope_base, int D);  // on = 0 when rope_base <= 0
+
+// Device-resident alpha: builds the rung table from *alpha (one thread) into *out.
+hipError_t launch_rung_table(const float *alpha, const BaseTable &b, int W, RungTable *out,
+                             hipStream_t s);
+// alpha_l = 0.5 + sigmoid(theta_l); dtheta_l = dalpha_l sigmoid(theta_l) (1 - sigmoid(theta_l)).
+hipError_t launch_alpha_from_theta(const float *theta, float *alpha, int n, hipStream_t s);
+hipError_t launch_dtheta(const float *theta, const float *dalpha, float *dtheta, int n, hipStream_t s);
 
 // RoPE of one tensor (x1 == nullptr) or of two same-shaped tensors in one launch.
 hipError_t launch_rope(int dtype, int D, const void *x0, void *y0, const void *x1, void *y1, int BH,

@@ -19,9 +19,11 @@ LIB_PATH = os.path.join(_HERE, "libfibattn.so")
 FIBATTN_FP32, FIBATTN_BF16 = 0, 1
 MAX_RUNGS = 32
 MAX_WINDOW = 128
-KERNEL_IDS = {"rope": 0, "forward": 1, "bwd_dq": 2, "bwd_dkdv": 3, "dalpha_reduce": 4}
+KERNEL_IDS = {"rope": 0, "forward": 1, "bwd_dq": 2, "bwd_dkdv": 3, "dalpha_reduce": 4, "alpha": 5}
 EXPORTED = ("fibattn_rung_table", "fibattn_forward", "fibattn_backward_workspace_bytes",
-            "fibattn_backward", "fibattn_forward_gqa", "fibattn_backward_gqa", "fibattn_rope",
+            "fibattn_backward", "fibattn_forward_gqa", "fibattn_backward_gqa",
+            "fibattn_device_table_bytes", "fibattn_device_table", "fibattn_forward_dt",
+            "fibattn_backward_dt", "fibattn_alpha_from_theta", "fibattn_dtheta", "fibattn_rope",
             "fibattn_rope_qk", "fibattn_status_string", "fibattn_timing_begin", "fibattn_timing_end")
 
 
@@ -60,6 +62,19 @@ def lib():
     L.fibattn_backward_gqa.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                        i, i, i, i, i, i, ip, i, f, f, i, vp]
     L.fibattn_backward_gqa.restype = i
+    L.fibattn_device_table_bytes.argtypes = []
+    L.fibattn_device_table_bytes.restype = sz
+    L.fibattn_device_table.argtypes = [vp, ip, i, i, vp, vp]
+    L.fibattn_device_table.restype = i
+    L.fibattn_forward_dt.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, vp, i, vp]
+    L.fibattn_forward_dt.restype = i
+    L.fibattn_backward_dt.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+                                      i, i, i, i, i, i, vp, f, i, vp]
+    L.fibattn_backward_dt.restype = i
+    L.fibattn_alpha_from_theta.argtypes = [vp, vp, i, vp]
+    L.fibattn_alpha_from_theta.restype = i
+    L.fibattn_dtheta.argtypes = [vp, vp, vp, i, vp]
+    L.fibattn_dtheta.restype = i
     L.fibattn_rope.argtypes = [vp, vp, i, i, i, i, f, i, i, vp]
     L.fibattn_rope.restype = i
     L.fibattn_rope_qk.argtypes = [vp, vp, vp, vp, i, i, i, i, f, i, vp]
@@ -209,6 +224,101 @@ def fibattn_backward(q, k, v, o, lse, dO, W: int, base, alpha: float, *, dq=None
         st = lib().fibattn_backward_gqa(*ptrs, B, H, Hkv, *tail)
         _check("fibattn_backward_gqa", st)
     return dq, dk, dv, dalpha
+
+
+# ---- device-resident alpha ---------------------------------------------------------
+
+def fibattn_device_table(alpha, base, W: int, *, table=None, stream=None):
+    """Rung table of a device alpha (a 1-element float32 tensor, or one element of a
+    per-layer array) built on the device; returns the table buffer (uint8 tensor)."""
+    import torch
+
+    if alpha.device.type != "cuda" or alpha.dtype != torch.float32 or alpha.numel() < 1:
+        raise ValueError("alpha: a float32 device tensor")
+    nb = int(lib().fibattn_device_table_bytes())
+    if table is None:
+        table = torch.empty(nb, device=alpha.device, dtype=torch.uint8)
+    if table.numel() < nb or not table.is_contiguous():
+        raise ValueError(f"table: {nb} contiguous bytes")
+    b, bp = _base_array(base)
+    st = lib().fibattn_device_table(alpha.data_ptr(), bp, b.size, int(W), table.data_ptr(), _stream(stream))
+    _check("fibattn_device_table", st)
+    return table
+
+
+def fibattn_forward_dt(q, k, v, W: int, table, *, o=None, lse=None, stream=None):
+    """As fibattn_forward, with the rung table built on the device."""
+    import torch
+
+    B, H, T, D = q.shape
+    Hkv = _kv_heads(q, k)
+    _check_tensor("q", q, q.shape, q.dtype)
+    for n_, t in (("k", k), ("v", v)):
+        _check_tensor(n_, t, (B, Hkv, T, D), q.dtype)
+    o = torch.empty_like(q) if o is None else o
+    lse = torch.empty((B, H, T), device=q.device, dtype=torch.float32) if lse is None else lse
+    _check_tensor("o", o, q.shape, q.dtype)
+    _check_tensor("lse", lse, (B, H, T), torch.float32)
+    st = lib().fibattn_forward_dt(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
+                                  B, H, Hkv, T, D, int(W), table.data_ptr(), _dtype_code(q), _stream(stream))
+    _check("fibattn_forward_dt", st)
+    return o, lse
+
+
+def fibattn_backward_dt(q, k, v, o, lse, dO, W: int, table, *, dq=None, dk=None, dv=None,
+                        dalpha=None, workspace=None, rope_base: float = 0.0, stream=None):
+    """As fibattn_backward, with the rung table built on the device."""
+    import torch
+
+    B, H, T, D = q.shape
+    Hkv = _kv_heads(q, k)
+    kvs = (B, Hkv, T, D)
+    for n_, t, sh in (("q", q, q.shape), ("k", k, kvs), ("v", v, kvs), ("o", o, q.shape),
+                      ("dO", dO, q.shape)):
+        _check_tensor(n_, t, sh, q.dtype)
+    _check_tensor("lse", lse, (B, H, T), torch.float32)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    for n_, t, sh in (("dq", dq, q.shape), ("dk", dk, kvs), ("dv", dv, kvs)):
+        _check_tensor(n_, t, sh, q.dtype)
+    if dalpha is None:
+        dalpha = torch.empty(1, device=q.device, dtype=torch.float32)
+    need = fibattn_backward_workspace_bytes(B, H, T, D, W, 0)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), device=q.device, dtype=torch.uint8)
+    st = lib().fibattn_backward_dt(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
+                                   dO.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                                   dalpha.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                                   B, H, Hkv, T, D, int(W), table.data_ptr(), ctypes.c_float(rope_base),
+                                   _dtype_code(q), _stream(stream))
+    _check("fibattn_backward_dt", st)
+    return dq, dk, dv, dalpha
+
+
+def fibattn_alpha_from_theta(theta, *, alpha=None, stream=None):
+    """alpha = 0.5 + sigmoid(theta) elementwise (float32 device tensors)."""
+    import torch
+
+    if theta.device.type != "cuda" or theta.dtype != torch.float32 or not theta.is_contiguous():
+        raise ValueError("theta: a contiguous float32 device tensor")
+    alpha = torch.empty_like(theta) if alpha is None else alpha
+    st = lib().fibattn_alpha_from_theta(theta.data_ptr(), alpha.data_ptr(), theta.numel(), _stream(stream))
+    _check("fibattn_alpha_from_theta", st)
+    return alpha
+
+
+def fibattn_dtheta(theta, dalpha, *, dtheta=None, stream=None):
+    """dtheta = dalpha * sigmoid(theta) (1 - sigmoid(theta)) elementwise."""
+    import torch
+
+    if dalpha.shape != theta.shape or dalpha.dtype != torch.float32 or dalpha.device != theta.device:
+        raise ValueError("dalpha: float32, shaped like theta, same device")
+    dtheta = torch.empty_like(theta) if dtheta is None else dtheta
+    st = lib().fibattn_dtheta(theta.data_ptr(), dalpha.data_ptr(), dtheta.data_ptr(), theta.numel(),
+                              _stream(stream))
+    _check("fibattn_dtheta", st)
+    return dtheta
 
 
 def fibattn_rope(x, rope_base: float = 10000.0, transpose: bool = False, *, out=None, stream=None):

@@ -123,5 +123,17 @@ def test_invalid_arguments_return_codes_without_gpu():
         assert L.fibattn_forward_gqa(16, 16, 16, 16, 16, 1, 8, hkv, 8, 64, 8, b, 15, one, 1, None) == 1
         assert L.fibattn_backward_gqa(16, 16, 16, 16, 16, 16, 16, 16, 16, 16, 16, 1 << 30,
                                       1, 8, hkv, 8, 64, 8, b, 15, one, zero, 1, None) == 1
+    # device alpha: the base table is checked on the host, pointers before any launch
+    bad = (ctypes.c_int32 * 3)(5, 3, 8)
+    assert L.fibattn_device_table(16, bad, 3, 8, 16, None) == 1
+    assert L.fibattn_device_table(None, b, 15, 8, 16, None) == 1
+    assert L.fibattn_device_table(16, b, 15, 8, 18, None) == 1  # misaligned table
+    assert L.fibattn_device_table_bytes() >= 4 + 3 * 4 * 32
+    assert L.fibattn_forward_dt(16, 16, 16, 16, 16, 1, 2, 2, 8, 64, 8, None, 1, None) == 1
+    assert L.fibattn_forward_dt(16, 16, 16, 16, 16, 1, 8, 3, 8, 64, 8, 16, 1, None) == 1
+    assert L.fibattn_backward_dt(16, 16, 16, 16, 16, 16, 16, 16, 16, 16, None, 0,
+                                 1, 1, 1, 8, 64, 8, 16, zero, 1, None) == 3
+    assert L.fibattn_alpha_from_theta(16, 16, 0, None) == 1
+    assert L.fibattn_dtheta(16, None, 16, 4, None) == 1
     for s in range(5):
         assert F.status_string(s)

@@ -1,0 +1,167 @@
+"""GPU: the device-resident alpha path (rung table built on the device from a device
+alpha, alpha = 0.5 + sigmoid(theta), dtheta), against the host table and the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_28560_amd import fibattn as F
+from paper_2606_28560_amd import inputs, schedules, workloads
+from tests.parity import compare, oracle_run
+
+pytestmark = pytest.mark.gpu
+
+FIB = schedules.FIB15
+POW2 = schedules.POW2_11
+
+
+def _table_fields(buf):
+    """(n, d0, w, f) of a device table read back (the library's layout: int n, then
+    int d0[32], float w[32], int f[32])."""
+    raw = buf.cpu().numpy()
+    n = int(raw[:4].view(np.int32)[0])
+    d0 = raw[4:132].view(np.int32)
+    w = raw[132:260].view(np.float32)
+    f = raw[260:388].view(np.int32)
+    return n, d0, w, f
+
+
+def _device_alphas():
+    out = [np.float32(a) for a in (0.5, 0.7310586, 1.0, 1.2333333, 1.5, 0.01, 3.0)]
+    out += list(schedules.alpha_linear_stagger(16)) + list(schedules.alpha_coprime_stagger(16))
+    out += list(schedules.alpha_from_theta(inputs.thetas(16, case=5)))
+    return out
+
+
+@pytest.mark.parametrize("base,W", [(FIB, 8), (FIB, 6), (FIB, 12), (POW2, 10), ([3, 7, 11, 40], 2)])
+def test_device_table_equals_host_table(base, W):
+    alphas = _device_alphas()
+    a_dev = torch.tensor(alphas, dtype=torch.float32, device="cuda")
+    for idx, a in enumerate(alphas):
+        buf = F.fibattn_device_table(a_dev[idx:idx + 1], base, W)
+        torch.cuda.synchronize()
+        n, d0, w, f = _table_fields(buf)
+        host = F.fibattn_rung_table(float(a), base, W)
+        assert n == len(host), (float(a), n, len(host))
+        for r, (hd0, hw, hf) in enumerate(host):
+            assert (int(d0[r]), float(w[r]), int(f[r])) == (hd0, hw, hf), (float(a), r)
+
+
+def _dev_run(x, W, base, alpha, rope=0.0, poison=True):
+    Q, K, V, G = (x[n].cuda().contiguous() for n in ("q", "k", "v", "dO"))
+    a_dev = torch.tensor([alpha], dtype=torch.float32, device="cuda")
+    table = F.fibattn_device_table(a_dev, base, W)
+    o = torch.empty_like(Q)
+    lse = torch.empty(Q.shape[:3], device="cuda", dtype=torch.float32)
+    dq, dk, dv = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
+    da = torch.empty(1, device="cuda", dtype=torch.float32)
+    if poison:
+        for t in (o, lse, dq, dk, dv, da):
+            t.fill_(float("nan"))
+    F.fibattn_forward_dt(Q, K, V, W, table, o=o, lse=lse)
+    F.fibattn_backward_dt(Q, K, V, o, lse, G, W, table, dq=dq, dk=dk, dv=dv, dalpha=da, rope_base=rope)
+    torch.cuda.synchronize()
+    res = {kk: vv.double().cpu().numpy() for kk, vv in
+           {"o": o, "lse": lse, "dq": dq, "dk": dk, "dv": dv}.items()}
+    res["dalpha"] = float(da.item())
+    return res
+
+
+DEV = [
+    # (B, H, H_kv, T, D, dtype, W, base, alpha)
+    (1, 2, 2, 300, 32, "fp32", 8, FIB, 0.7310586),
+    (2, 2, 2, 257, 64, "fp32", 6, POW2, 1.0),
+    (1, 3, 3, 333, 64, "bf16", 8, FIB, 1.0),
+    (2, 2, 2, 300, 64, "bf16", 10, FIB, 1.2333333),
+    (1, 8, 2, 290, 64, "bf16", 8, FIB, 0.9),
+    (1, 2, 1, 200, 64, "bf16", 20, POW2, 0.8),
+]
+
+
+@pytest.mark.parametrize("B,H,Hkv,T,D,dtype,W,base,alpha", DEV)
+def test_device_alpha_parity(B, H, Hkv, T, D, dtype, W, base, alpha):
+    idx = DEV.index((B, H, Hkv, T, D, dtype, W, base, alpha))
+    print(f"device alpha case {idx}: B{B} H{H}/{Hkv} T{T} D{D} {dtype} W{W} alpha={alpha}", flush=True)
+    x = inputs.attention_inputs(B, H, T, D, dtype, 400 + idx, 0, names=("q", "dO"))
+    x.update(inputs.attention_inputs(B, Hkv, T, D, dtype, 400 + idx, 0, names=("k", "v")))
+    got = _dev_run(x, W, base, alpha)
+    ref = oracle_run(x["q"], x["k"], x["v"], x["dO"], W, base, alpha)
+    compare(got, ref, dtype, f"device alpha case {idx}")
+
+
+@pytest.mark.parametrize("alpha", [float("nan"), 0.0, -1.0, float("inf")])
+def test_invalid_device_alpha_gives_nan(alpha):
+    x = inputs.attention_inputs(1, 2, 100, 64, "bf16", 450, 0)
+    got = _dev_run(x, 8, FIB, alpha, poison=False)
+    for name in ("o", "lse", "dq", "dk", "dv"):
+        assert np.all(np.isnan(got[name])), name
+    assert np.isnan(got["dalpha"])
+
+
+def test_alpha_from_theta_and_dtheta():
+    theta = inputs.thetas(64, case=7).astype(np.float32)
+    t_dev = torch.tensor(theta, device="cuda")
+    a = F.fibattn_alpha_from_theta(t_dev).cpu().numpy()
+    ref = (0.5 + 1.0 / (1.0 + np.exp(-theta.astype(np.float64))))
+    assert np.array_equal(a, ref.astype(np.float32))  # float64 sigmoid, one rounding
+    da = torch.linspace(-3.0, 5.0, 64, device="cuda", dtype=torch.float32)
+    dt = F.fibattn_dtheta(t_dev, da).cpu().numpy()
+    sg = 1.0 / (1.0 + np.exp(-theta.astype(np.float64)))
+    np.testing.assert_allclose(dt, da.cpu().numpy() * sg * (1 - sg), rtol=1e-6, atol=1e-7)
+
+
+def test_learned_alpha_step_in_a_graph():
+    # theta (device) -> alpha -> rung table -> RoPE -> forward -> backward -> dtheta,
+    # captured once and replayed with theta changed in place between replays: every
+    # replay follows the new theta with no host involvement
+    wl = workloads.workload("pow2_fib_learned16_T1024")
+    B, H, T, D, W = 2, 4, 256, 64, 10
+    x = inputs.attention_inputs(B, H, T, D, "bf16", 460, 0)
+    q, k, v, dO = (x[n].cuda() for n in ("q", "k", "v", "dO"))
+    theta = torch.tensor([0.3], device="cuda", dtype=torch.float32)
+    alpha = torch.empty_like(theta)
+    table = torch.empty(F.lib().fibattn_device_table_bytes(), device="cuda", dtype=torch.uint8)
+    qr, kr, o = torch.empty_like(q), torch.empty_like(k), torch.empty_like(q)
+    lse = torch.empty((B, H, T), device="cuda", dtype=torch.float32)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    da, dth = torch.empty(1, device="cuda"), torch.empty(1, device="cuda")
+    ws = torch.empty(F.fibattn_backward_workspace_bytes(B, H, T, D, W, 0), device="cuda", dtype=torch.uint8)
+    base = wl.calls[0].base
+
+    def step():
+        F.fibattn_alpha_from_theta(theta, alpha=alpha)
+        F.fibattn_device_table(alpha, base, W, table=table)
+        F.fibattn_rope_qk(q, k, 10000.0, q_out=qr, k_out=kr)
+        F.fibattn_forward_dt(qr, kr, v, W, table, o=o, lse=lse)
+        F.fibattn_backward_dt(qr, kr, v, o, lse, dO, W, table, dq=dq, dk=dk, dv=dv, dalpha=da,
+                              workspace=ws, rope_base=10000.0)
+        F.fibattn_dtheta(theta, da, dtheta=dth)
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()  # warm-up outside capture
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    torch.cuda.synchronize()
+    rq, rk = oracle.rope(x["q"]), oracle.rope(x["k"])
+    rq, rk = (inputs.round_to(r.astype(np.float32), "bf16").double().numpy() for r in (rq, rk))
+    for rep, th in enumerate((0.3, -0.8, 1.7)):
+        theta.fill_(th)
+        g.replay()
+        torch.cuda.synchronize()
+        a = float(alpha.item())
+        assert a == float(schedules.alpha_from_theta(np.float32(th)))
+        ro, rl = oracle.forward(rq, rk, x["v"], W, base, a)
+        rdq, rdk, rdv, rda, l1 = oracle.backward(rq, rk, x["v"], x["dO"], W, base, a)
+        rdq, rdk = oracle.rope(rdq, transpose=True), oracle.rope(rdk, transpose=True)
+        got = {kk: vv.double().cpu().numpy() for kk, vv in
+               {"o": o, "lse": lse, "dq": dq, "dk": dk, "dv": dv}.items()}
+        got["dalpha"] = float(da.item())
+        compare(got, {"o": ro, "lse": rl, "dq": rdq, "dk": rdk, "dv": rdv, "dalpha": rda, "l1": l1},
+                "bf16", f"graph replay {rep}")
+        sg = 1.0 / (1.0 + np.exp(-float(np.float32(th))))
+        assert abs(float(dth.item()) - got["dalpha"] * sg * (1 - sg)) <= 1e-5 * max(1.0, abs(got["dalpha"]))
