@@ -44,6 +44,7 @@ def parse_args():
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the oracle sample")
     p.add_argument("--no-t4096", action="store_true", help="skip the T=4096 figure")
     p.add_argument("--no-gqa", action="store_true", help="skip the grouped-heads figure")
+    p.add_argument("--no-learned-alpha", action="store_true", help="skip the device-alpha figure")
     p.add_argument("--no-integer-offsets", action="store_true",
                    help="skip the continuous vs rounded-offset stagger figure")
     p.add_argument("--copy-probe-mb", type=int, default=0,
@@ -310,6 +311,49 @@ def gqa_figure(steps: int, warmup: int, eager: bool, kv_heads: int = 2):
             "value": qh / (ms * 1e-3), "kernels_ms_per_step": kt}
 
 
+def learned_alpha_figure(steps: int, warmup: int, eager: bool, layer: int = 0):
+    """Learned-alpha layer of the pow2/fib workload (B=32, H=8, T=1024, W=10, Fibonacci
+    base, alpha = 0.5 + sigmoid(theta)) with theta resident on the device: theta ->
+    alpha -> rung table -> RoPE -> forward -> backward -> dtheta, against the same
+    layer with alpha passed from the host."""
+    import torch
+
+    from paper_2606_28560_amd import fibattn as F
+    from paper_2606_28560_amd import inputs, workloads
+
+    wl = workloads.workload("pow2_fib_learned16_T1024")
+    call = next(c for c in wl.calls if c.base_name == "fib15" and c.layer == layer)
+    theta = torch.tensor(inputs.thetas(16, case=5)[layer:layer + 1], dtype=torch.float32, device="cuda")
+    sets = [Step(wl, call, i) for i in range(2)]
+    dev = []
+    for st in sets:
+        st.theta, st.alpha = theta, torch.empty_like(theta)
+        st.table = torch.empty(F.lib().fibattn_device_table_bytes(), device="cuda", dtype=torch.uint8)
+        st.dtheta = torch.empty_like(theta)
+
+        def run_dev(st=st):
+            c = st.call
+            F.fibattn_alpha_from_theta(st.theta, alpha=st.alpha)
+            F.fibattn_device_table(st.alpha, c.base, c.W, table=st.table)
+            F.fibattn_rope_qk(st.q, st.k, ROPE_BASE, q_out=st.qr, k_out=st.kr)
+            F.fibattn_forward_dt(st.qr, st.kr, st.v, c.W, st.table, o=st.o, lse=st.lse)
+            F.fibattn_backward_dt(st.qr, st.kr, st.v, st.o, st.lse, st.dO, c.W, st.table, dq=st.dq,
+                                  dk=st.dk, dv=st.dv, dalpha=st.da, workspace=st.ws, rope_base=ROPE_BASE)
+            F.fibattn_dtheta(st.theta, st.da, dtheta=st.dtheta)
+        dev.append(run_dev)
+    out = {"workload": wl.name, "layer": layer, "alpha": float(call.alpha)}
+    for tag, fns in (("device_alpha", dev), ("host_alpha", sets)):
+        if eager:
+            run = lambda i, fns=fns: fns[i % len(fns)]()  # noqa: E731
+        else:
+            gs = [capture(fn) for fn in fns]
+            run = lambda i, gs=gs: gs[i % len(gs)].replay()  # noqa: E731
+        ms, _ = timed(run, steps, warmup)
+        out[tag + "_ms"] = ms
+        out[tag + "_value"] = wl.queries_heads / (ms * 1e-3)
+    return out
+
+
 def main():
     args = parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -392,6 +436,8 @@ def main():
         result["t4096"] = t4096_figure(max(5, args.steps // 4), 2, args.eager)
     if not args.no_gqa:
         result["gqa"] = gqa_figure(max(5, args.steps // 4), 2, args.eager)
+    if not args.no_learned_alpha:
+        result["learned_alpha"] = learned_alpha_figure(max(5, args.steps // 4), 2, args.eager)
     if not args.no_integer_offsets:
         result["integer_offsets"] = integer_offsets_figure(max(5, args.steps // 4), 2, args.eager)
     if args.copy_probe_mb:
