@@ -84,8 +84,9 @@ fibattn_status_t fibattn_rung_table(float alpha, const int32_t *base, int K, int
  *   o    : output, dtype, [B,H,T,d_head] (written)
  *   lse  : float32 [B,H,T] (written): natural-log log-sum-exp of the tau-scaled
  *          logits of each query, saved for the backward
- * Limits: d_head in {32, 64}; 0 <= W <= FIBATTN_MAX_WINDOW; 0 <= K <= FIBATTN_MAX_RUNGS;
- * alpha finite and > 0; B*H <= 65535.
+ * Limits: d_head in {32, 64, 128}; 0 <= W <= FIBATTN_MAX_WINDOW; 0 <= K <= FIBATTN_MAX_RUNGS;
+ * alpha finite and > 0; B*H <= 65535.  bfloat16 with d_head 64 and W <= 16 runs the
+ * matrix-core kernels; every other supported shape runs the generic kernels.
  */
 fibattn_status_t fibattn_forward(const void *q, const void *k, const void *v,
                                  void *o, float *lse,
@@ -193,7 +194,7 @@ fibattn_status_t fibattn_dtheta(const float *theta, const float *dalpha, float *
  * and sine rounded to float32.  transpose != 0 applies the inverse rotation R^T,
  * which carries gradients of rotated tensors back to the unrotated ones.
  *   x : input, dtype, [B,H,T,d_head];  y : output (may equal x), same layout.
- * Limits: d_head in {32, 64}; rope_base finite and > 1.
+ * Limits: d_head in {32, 64, 128}; rope_base finite and > 1.
  */
 fibattn_status_t fibattn_rope(const void *x, void *y, int B, int H, int T, int d_head,
                               float rope_base, int transpose,

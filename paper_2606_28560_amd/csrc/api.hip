@@ -42,7 +42,7 @@ fibattn_status_t check_common(int B, int H, int T, int d_head, int W, int K, fib
     if (dtype != FIBATTN_FP32 && dtype != FIBATTN_BF16) return FIBATTN_ERR_INVALID_ARG;
     if ((long long)B * H > 65535) return FIBATTN_ERR_UNSUPPORTED;
     if ((long long)B * H * T * d_head > (1ll << 40)) return FIBATTN_ERR_UNSUPPORTED;
-    if (d_head != 32 && d_head != 64) return FIBATTN_ERR_UNSUPPORTED;
+    if (d_head != 32 && d_head != 64 && d_head != 128) return FIBATTN_ERR_UNSUPPORTED;
     if (W > FIBATTN_MAX_WINDOW || K > FIBATTN_MAX_RUNGS) return FIBATTN_ERR_UNSUPPORTED;
     return FIBATTN_OK;
 }
@@ -244,7 +244,7 @@ fibattn_status_t fibattn_rope(const void *x, void *y, int B, int H, int T, int d
     if (!aligned16(x) || !aligned16(y)) return FIBATTN_ERR_INVALID_ARG;
     if (dtype != FIBATTN_FP32 && dtype != FIBATTN_BF16) return FIBATTN_ERR_INVALID_ARG;
     if (!(rope_base > 1.f) || !isfinite(rope_base)) return FIBATTN_ERR_INVALID_ARG;
-    if (d_head != 32 && d_head != 64) return FIBATTN_ERR_UNSUPPORTED;
+    if (d_head != 32 && d_head != 64 && d_head != 128) return FIBATTN_ERR_UNSUPPORTED;
     if ((long long)B * H > 65535ll * 16) return FIBATTN_ERR_UNSUPPORTED;
     hipError_t e = launch_rope((int)dtype, d_head, x, y, nullptr, nullptr, B * H, T, rope_base,
                                transpose, stream);
@@ -259,7 +259,7 @@ fibattn_status_t fibattn_rope_qk(const void *q, const void *k, void *q_out, void
         return FIBATTN_ERR_INVALID_ARG;
     if (dtype != FIBATTN_FP32 && dtype != FIBATTN_BF16) return FIBATTN_ERR_INVALID_ARG;
     if (!(rope_base > 1.f) || !isfinite(rope_base)) return FIBATTN_ERR_INVALID_ARG;
-    if (d_head != 32 && d_head != 64) return FIBATTN_ERR_UNSUPPORTED;
+    if (d_head != 32 && d_head != 64 && d_head != 128) return FIBATTN_ERR_UNSUPPORTED;
     if ((long long)B * H > 65535ll * 16) return FIBATTN_ERR_UNSUPPORTED;
     hipError_t e = launch_rope((int)dtype, d_head, q, q_out, k, k_out, B * H, T, rope_base, 0, stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;

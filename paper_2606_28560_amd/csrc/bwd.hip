@@ -265,6 +265,8 @@ size_t bwd_num_partials(int dtype, int D, int BH, int T) {
     if (dtype == 0 && D == 64) return num_partials_t<float, 64>(BH, T);
     if (dtype == 1 && D == 32) return num_partials_t<uint16_t, 32>(BH, T);
     if (dtype == 1 && D == 64) return num_partials_t<uint16_t, 64>(BH, T);
+    if (dtype == 0 && D == 128) return num_partials_t<float, 128>(BH, T);
+    if (dtype == 1 && D == 128) return num_partials_t<uint16_t, 128>(BH, T);
     return 0;
 }
 
@@ -301,6 +303,8 @@ static hipError_t launch_backward_generic(int dtype, int D, const void *q, const
     if (dtype == 0 && D == 64) FIBATTN_BWD(float, 64);
     if (dtype == 1 && D == 32) FIBATTN_BWD(uint16_t, 32);
     if (dtype == 1 && D == 64) FIBATTN_BWD(uint16_t, 64);
+    if (dtype == 0 && D == 128) FIBATTN_BWD(float, 128);
+    if (dtype == 1 && D == 128) FIBATTN_BWD(uint16_t, 128);
 #undef FIBATTN_BWD
     return hipErrorInvalidValue;
 }

@@ -134,6 +134,8 @@ hipError_t launch_forward(int dtype, int D, const void *q, const void *k, const 
     if (dtype == 0 && D == 64) return launch_fwd_t<float, 64>(q, k, v, o, lse, BH, hd, T, W, rt, rtp, s);
     if (dtype == 1 && D == 32) return launch_fwd_t<uint16_t, 32>(q, k, v, o, lse, BH, hd, T, W, rt, rtp, s);
     if (dtype == 1 && D == 64) return launch_fwd_t<uint16_t, 64>(q, k, v, o, lse, BH, hd, T, W, rt, rtp, s);
+    if (dtype == 0 && D == 128) return launch_fwd_t<float, 128>(q, k, v, o, lse, BH, hd, T, W, rt, rtp, s);
+    if (dtype == 1 && D == 128) return launch_fwd_t<uint16_t, 128>(q, k, v, o, lse, BH, hd, T, W, rt, rtp, s);
     return hipErrorInvalidValue;
 }
 

@@ -23,7 +23,7 @@ template <> __device__ __forceinline__ void st1<uint16_t>(uint16_t *p, float x) 
     *p = (uint16_t)f32_to_bf16(x);
 }
 
-// Generic kernel (float32 storage, d_head 32): one element pair per thread.
+// Generic kernel (any storage type and head size): one element pair per thread.
 template <typename S, int D>
 __global__ __launch_bounds__(256) void rope_kernel(const S *x, S *y, int BH, int T, double rope_base,
                                                    int transpose) {
@@ -126,6 +126,11 @@ static hipError_t launch_rope_generic(int dtype, int D, const void *x, void *y, 
                       transpose);
     if (dtype == 1 && D == 64)
         return launch(kRope, rope_kernel<uint16_t, 64>, grid, dim3(256), 0, s, x, y, BH, T, lb,
+                      transpose);
+    if (dtype == 0 && D == 128)
+        return launch(kRope, rope_kernel<float, 128>, grid, dim3(256), 0, s, x, y, BH, T, lb, transpose);
+    if (dtype == 1 && D == 128)
+        return launch(kRope, rope_kernel<uint16_t, 128>, grid, dim3(256), 0, s, x, y, BH, T, lb,
                       transpose);
     return hipErrorInvalidValue;
 }

@@ -98,7 +98,7 @@ def test_invalid_arguments_return_codes_without_gpu():
     assert L.fibattn_forward(None, None, None, None, None, 1, 1, 8, 64, 8, b, 15, one, 1, None) == 1
     # bad sizes
     assert L.fibattn_forward(16, 16, 16, 16, 16, 0, 1, 8, 64, 8, b, 15, one, 1, None) == 1
-    assert L.fibattn_forward(16, 16, 16, 16, 16, 1, 1, 8, 128, 8, b, 15, one, 1, None) == 2
+    assert L.fibattn_forward(16, 16, 16, 16, 16, 1, 1, 8, 96, 8, b, 15, one, 1, None) == 2
     assert L.fibattn_forward(16, 16, 16, 16, 16, 1, 1, 8, 64, 129, b, 15, one, 1, None) == 2
     assert L.fibattn_forward(16, 16, 16, 16, 16, 1, 1, 8, 64, 8, b, 15, one, 9, None) == 1
     # workspace

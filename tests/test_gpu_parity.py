@@ -161,6 +161,43 @@ def test_pipeline_with_rope(dtype, D, W, alpha):
             dtype, f"pipeline {dtype} D{D} W{W}")
 
 
+HEAD128 = [
+    # (B, H, H_kv, T, D, dtype, W, base, alpha): d_head = 128 runs the generic kernels
+    (1, 2, 2, 260, 128, "fp32", 8, FIB, 0.7310586),
+    (2, 2, 1, 200, 128, "bf16", 8, FIB, 1.0),
+    (1, 4, 4, 150, 128, "bf16", 12, POW2, 1.3),
+]
+
+
+@pytest.mark.parametrize("B,H,Hkv,T,D,dtype,W,base,alpha", HEAD128)
+def test_head_dim_128_parity(B, H, Hkv, T, D, dtype, W, base, alpha):
+    idx = HEAD128.index((B, H, Hkv, T, D, dtype, W, base, alpha))
+    print(f"d_head 128 case {idx}: B{B} H{H}/{Hkv} T{T} {dtype} W{W} alpha={alpha}", flush=True)
+    x = _gqa_inputs(B, H, Hkv, T, D, dtype, 70 + idx)
+    got = gpu_run(x["q"], x["k"], x["v"], x["dO"], W, base, alpha)
+    ref = oracle_run(x["q"], x["k"], x["v"], x["dO"], W, base, alpha)
+    compare(got, ref, dtype, f"d_head 128 case {idx}")
+
+
+def test_head_dim_128_rope_pipeline():
+    x = inputs.attention_inputs(1, 2, 130, 128, "bf16", 77, 0)
+    Q, K = F.fibattn_rope_qk(x["q"].cuda(), x["k"].cuda(), 10000.0)
+    V, G = x["v"].cuda(), x["dO"].cuda()
+    o, lse = F.fibattn_forward(Q, K, V, 8, FIB, 0.9)
+    dq, dk, dv, da = F.fibattn_backward(Q, K, V, o, lse, G, 8, FIB, 0.9, rope_base=10000.0)
+    torch.cuda.synchronize()
+    rq, rk = oracle.rope(x["q"]), oracle.rope(x["k"])
+    rq, rk = (inputs.round_to(r.astype(np.float32), "bf16").double().numpy() for r in (rq, rk))
+    ro, rl = oracle.forward(rq, rk, x["v"], 8, FIB, 0.9)
+    rdq, rdk, rdv, rda, l1 = oracle.backward(rq, rk, x["v"], x["dO"], 8, FIB, 0.9)
+    rdq, rdk = oracle.rope(rdq, transpose=True), oracle.rope(rdk, transpose=True)
+    got = {kk: vv.double().cpu().numpy() for kk, vv in
+           {"o": o, "lse": lse, "dq": dq, "dk": dk, "dv": dv}.items()}
+    got["dalpha"] = float(da.item())
+    compare(got, {"o": ro, "lse": rl, "dq": rdq, "dk": rdk, "dv": rdv, "dalpha": rda, "l1": l1},
+            "bf16", "d_head 128 pipeline")
+
+
 GQA = [
     # (B, H, H_kv, T, D, dtype, W, base, alpha): grouped key/value heads.  bf16 d64
     # W<=16 runs the matrix-core kernels, whose dk/dv workgroup takes 4, 2 or 1 query
