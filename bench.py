@@ -54,18 +54,19 @@ def parse_args():
 
 # HBM traffic per launch of the layer_60m_fixed_T1024 kernels, from two rocprofv3 --pmc
 # passes (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) over
-#   bench.py --eager --steps 10 --warmup 2 --no-cpu-baseline --no-t4096 --copy-probe-mb 256
+#   bench.py --eager --steps 10 --warmup 2 --no-cpu-baseline --no-t4096 --no-gqa
+#            --no-learned-alpha --no-integer-offsets --copy-probe-mb 256
 # each scaled by what the same counter reads for the plain 256 MiB device copy of that run.
 # They hold only for the kernel sources they were taken on (COUNTER_SOURCES_SHA).
-COUNTER_SOURCES_SHA = "48d5a1fc26296c3d0374fd8a9595362bd55b05fa28fe38d05e0ec492ba7577e9"
+COUNTER_SOURCES_SHA = "ccdbf9df8cd41856a2b84b9ede4f82056dddf8ab527b2301027070e577eed18e"
 COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
 COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
-    "forward": (12402.1, 8448.0),
-    "bwd_dq": (20779.1, 8480.1),
-    "bwd_dkdv": (17457.4, 16384.0),
-    "rope": (8212.2, 16384.0),
+    "forward": (12405.6, 8448.0),
+    "bwd_dq": (20775.7, 8480.1),
+    "bwd_dkdv": (18025.3, 16384.0),
+    "rope": (8220.3, 16384.0),
 }
-COPY_PROBE_KIB = (262144.0, 131093.1, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
+COPY_PROBE_KIB = (262144.0, 131092.2, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
 
 
 def kernel_sources_sha() -> str:
