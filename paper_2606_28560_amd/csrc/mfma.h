@@ -273,9 +273,18 @@ __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70)
 
 // Block index -> work item, keeping consecutive work items (the tiles of one
 // (batch, head)) on one XCD: workgroups are dispatched round-robin over 8 XCDs.
+// Within an XCD the first round places dispatch positions j, j + 32, j + 64, ...
+// on one CU (32 CUs per XCD).  Later tiles of a sequence carry more rungs (and
+// early key tiles more rung queries), so every other run of 32 positions is
+// reversed: a CU then holds tiles from both ends of the sequence rather than
+// four tiles at the same position.
 __device__ __forceinline__ int xcd_remap(int b, int nblocks) {
     if (nblocks & 7) return b;
-    return (b & 7) * (nblocks >> 3) + (b >> 3);
+    const int per = nblocks >> 3;
+    int j = b >> 3;
+    const int lo = j & ~31, hi = min(lo + 32, per);
+    if ((j >> 5) & 1) j = lo + hi - 1 - j;
+    return (b & 7) * per + j;
 }
 
 }  // namespace fibattn
