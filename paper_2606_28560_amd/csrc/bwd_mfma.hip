@@ -9,7 +9,9 @@
 //          copied to LDS with direct-to-LDS loads;
 //   rungs: per-row bf16 dot2 products for <q, k[r0]>, <q, k[r1]>, <dO, v[r0]>,
 //          <dO, v[r1]> (the r1 terms are needed for dalpha even when w = 0; then row
-//          r1 of a query is row r0 of the previous query, taken from its lanes),
+//          r1 of a query is row r0 of the previous query, taken from its lanes;
+//          with interpolation the rows of short rungs come from the staged rows,
+//          which then reach 32 rows below the tile),
 //          dq += tau dS ((1-w) k[r0] + w k[r1]) on the VALU,
 //          dalpha partial += f (tau dS <q, k[r1]-k[r0]> + p <dO, v[r1]-v[r0]>);
 //   writes dq, Delta_i = <dO_i, o_i> and one float64 dalpha partial per workgroup
@@ -28,7 +30,6 @@
 namespace fibattn {
 
 constexpr int kBwdB = 64;                // rows per workgroup
-constexpr int kStage = kBwdB + 16;       // staged rows
 
 // ---------------------------------------------------------------------------
 // INTERP: some rung has w != 0 (rows r0 and r1 both loaded per rung).  DEV: the rung
@@ -42,6 +43,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     Heads hd) {
     const RungTable &rt = DEV ? *rtp : rt_arg;
     const bool bad = DEV && rt.n < 0;  // a device alpha that is not finite and positive
+    // staged K, V rows [T0 - kLeadQ, T0 + 64): the band and, interpolating, the short rungs
+    constexpr int kLeadQ = INTERP ? 32 : 16;
+    constexpr int kStage = kBwdB + kLeadQ;
     __shared__ __align__(16) uint16_t kr[kStage * kD];
     __shared__ __align__(16) uint16_t vr[kStage * kD];
     __shared__ double sfreq[32];
@@ -79,38 +83,58 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 #pragma unroll
     for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && rt.d0[r] <= last) ? 1 : 0;
     nact = __builtin_amdgcn_readfirstlane(nact);  // wave-uniform: scalar branches
+    // rungs whose rows r0 and r1 for every query of the wave lie in the staged rows
+    int nlds = 0;
+#pragma unroll
+    for (int r = 0; r < kMaxRungs; ++r) nlds += (INTERP && r < rt.n && rt.d0[r] + 1 <= kLeadQ + 16 * wv) ? 1 : 0;
+    nlds = __builtin_amdgcn_readfirstlane(nlds);
     // x = {k0, v0, k1, v1}: rows r0 and r1 = r0 - 1 of K and V.  When every w == 0
     // only the first query of each 16-lane row (queries t0, t0+4, t0+8, t0+12) loads
     // its r1 rows here; fill_r1 takes the others from the previous query's lanes.
-    auto load_rung = [&](int r, Slice *x) {
-        const int R0 = min(max(i - rt.d0[r], 0), T - 1);
-        x[0] = load_row(K, R0, gq);
-        x[1] = load_row(V, R0, gq);
-        if (INTERP || (nq & 3) == 0) {
-            const int R1 = min(max(i - rt.d0[r] - 1, 0), T - 1);
-            x[2] = load_row(K, R1, gq);
-            x[3] = load_row(V, R1, gq);
+    // (rows of the first nlds rungs from LDS, the others from global memory; `which`
+    // selects 1 = global rungs only, 2 = LDS rungs only, 3 = both)
+    auto load_rung = [&](int r, Slice *x, int which) {
+        if (r < nlds) {
+            if (which & 2) {
+                const int L0 = 16 * wv + nq + kLeadQ - rt.d0[r];
+                x[0] = dma_slice(kr, L0, gq);
+                x[1] = dma_slice(vr, L0, gq);
+                if (INTERP || (nq & 3) == 0) {
+                    x[2] = dma_slice(kr, L0 - 1, gq);
+                    x[3] = dma_slice(vr, L0 - 1, gq);
+                }
+            }
+        } else if (which & 1) {
+            const int R0 = min(max(i - rt.d0[r], 0), T - 1);
+            x[0] = load_row(K, R0, gq);
+            x[1] = load_row(V, R0, gq);
+            if (INTERP || (nq & 3) == 0) {
+                const int R1 = min(max(i - rt.d0[r] - 1, 0), T - 1);
+                x[2] = load_row(K, R1, gq);
+                x[3] = load_row(V, R1, gq);
+            }
         }
     };
     Slice xA[4], xB[4];
-    if (0 < nact) load_rung(0, xA);  // in flight during the band phase
+    if (0 < nact) load_rung(0, xA, 1);  // in flight during the band phase
 
-    // band rows [T0-16, T0+64) of K and V, straight to LDS (rows outside [0, T) are
+    // rows [T0-kLeadQ, T0+64) of K and V, straight to LDS (rows outside [0, T) are
     // clamped copies: their keys are masked below)
-    dma_rows<kStage>(kr, K, T0 - 16, T);
-    dma_rows<kStage>(vr, V, T0 - 16, T);
+    dma_rows<kStage>(kr, K, T0 - kLeadQ, T);
+    dma_rows<kStage>(vr, V, T0 - kLeadQ, T);
     stage_freq(sfreq, rf);
     // Delta_i = <dO_i, o_i>, once every load of the prologue is in flight
     const float delta = quad_sum(dot_slice(gqq, oq));
     const float delta_m = __shfl(delta, 4 * nm, 64);
     wait_vmem();
     __syncthreads();
+    if (0 < nact) load_rung(0, xA, 2);
 
     // band (MFMA layout): keys [t0-16, t0+16)
     uint32_t cw[4];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
-        const int sr = 16 * wv + 16 * b + nm;  // staged row
+        const int sr = kLeadQ - 16 + 16 * wv + 16 * b + nm;  // staged row
         const f32x4 s = mfma_dot64(dma_slice(kr, sr, gm), qm, f32x4{0.f, 0.f, 0.f, 0.f});
         const f32x4 dp = mfma_dot64(dma_slice(vr, sr, gm), gmm, f32x4{0.f, 0.f, 0.f, 0.f});
         float c[4];
@@ -128,7 +152,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     Acc16 acc;
 #pragma unroll
     for (int c = 0; c < 4; ++c)
-        acc.c[c] = mfma(dma_operand_t(kr, c, nm, 16 * wv, gm), C, f32x4{0.f, 0.f, 0.f, 0.f});
+        acc.c[c] = mfma(dma_operand_t(kr, c, nm, kLeadQ - 16 + 16 * wv, gm), C, f32x4{0.f, 0.f, 0.f, 0.f});
     acc_to_quad(acc, lane);
 
     // rungs (quad layout), two batches in flight; r1 = -1 is the zero row
@@ -171,11 +195,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 #pragma unroll
     for (int rb = 0; rb < kMaxRungs; rb += 2) {
         if (rb < nact) {
-            if (rb + 1 < nact) load_rung(rb + 1, xB);
+            if (rb + 1 < nact) load_rung(rb + 1, xB, 3);
             fill_r1(xA);
             compute_rung(rb, xA);
             if (rb + 1 < nact) {
-                if (rb + 2 < nact) load_rung(rb + 2, xA);
+                if (rb + 2 < nact) load_rung(rb + 2, xA, 3);
                 fill_r1(xB);
                 compute_rung(rb + 1, xB);
             }

@@ -10,7 +10,11 @@
 //   - every rung is a contiguous shifted block: query t0+n reads rows t0+n-floor(d)
 //     and t0+n-floor(d)-1.  Those logits are per-row dot products (bf16 dot2, four
 //     lanes per row) blended in score space; the blended values are accumulated on
-//     the VALU in the same register layout as the matrix-core output.
+//     the VALU in the same register layout as the matrix-core output.  With
+//     interpolation the staged rows reach 32 rows below the tile, and the short
+//     rungs whose two rows lie there are read from LDS instead of the L2.  (With
+//     every w == 0 the wider stage does not pay: the first rung read from global
+//     memory would start late.)
 // Softmax runs in base 2: the band's maximum is the first running reference, then
 // rungs are taken a batch at a time (their key and value rows loaded together),
 // rescaling the running sum and weighted values only when a logit exceeds the
@@ -21,7 +25,6 @@
 namespace fibattn {
 
 constexpr int kFwdBQ = 64;                 // queries per workgroup
-constexpr int kBandRows = kFwdBQ + 16;     // staged band rows [T0-16, T0+64)
 constexpr float kSlack = 8.f;              // log2 units a logit may exceed the running reference
 
 // INTERP: some rung has w != 0, so the second row r1 is read.  DEV: the rung table
@@ -34,6 +37,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     const RungTable &rt = DEV ? *rtp : rt_arg;
     constexpr int RB = INTERP ? 1 : 2;  // rungs per load batch; two batches in flight
     constexpr int NS = INTERP ? 2 : 1;  // rows per rung (r0, and r1 when interpolating)
+    // staged rows [T0 - kLeadF, T0 + 64): the band and, interpolating, the short rungs
+    constexpr int kLeadF = INTERP ? 32 : 16;
+    constexpr int kBandRows = kFwdBQ + kLeadF;
     __shared__ __align__(16) uint16_t kr[kBandRows * kD];
     __shared__ __align__(16) uint16_t vr[kBandRows * kD];
 
@@ -57,32 +63,52 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
 #pragma unroll
     for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && rt.d0[r] <= last) ? 1 : 0;
     nact = __builtin_amdgcn_readfirstlane(nact);  // wave-uniform: scalar branches
+    // rungs whose rows (r0 and, interpolating, r1) for every query of the wave lie in
+    // the staged rows: a prefix of the table
+    int nlds = 0;
+#pragma unroll
+    for (int r = 0; r < kMaxRungs; ++r) nlds += (INTERP && r < rt.n && rt.d0[r] + NS - 1 <= kLeadF + 16 * wv) ? 1 : 0;
+    nlds = __builtin_amdgcn_readfirstlane(nlds);
 
     const int im = t0 + nm;  // query of this lane in the MFMA layout
     const int i = t0 + nq;   // ... in the quad layout
     const Slice qq = load_row(Q, min(i, T - 1), gq);
 
     // rung rows of a batch: kx[x*NS + s], vx[x*NS + s] = row r_s of rung rb + x
-    auto load_batch = [&](int rb, Slice *kx, Slice *vx) {
+    // (from LDS for the first nlds rungs, else from global memory; `which` selects
+    // 1 = global rungs only, 2 = LDS rungs only, 3 = both)
+    auto load_batch = [&](int rb, Slice *kx, Slice *vx, int which) {
 #pragma unroll
         for (int x = 0; x < RB; ++x) {
-            const int R0 = min(max(i - rt.d0[rb + x], 0), T - 1);
+            if (rb + x < nlds) {
+                if (which & 2) {
+                    const int L0 = 16 * wv + nq + kLeadF - rt.d0[rb + x];
 #pragma unroll
-            for (int sidx = 0; sidx < NS; ++sidx) {
-                const int R = max(R0 - sidx, 0);
-                kx[x * NS + sidx] = load_row(K, R, gq);
-                vx[x * NS + sidx] = load_row(V, R, gq);
+                    for (int sidx = 0; sidx < NS; ++sidx) {
+                        kx[x * NS + sidx] = dma_slice(kr, L0 - sidx, gq);
+                        vx[x * NS + sidx] = dma_slice(vr, L0 - sidx, gq);
+                    }
+                }
+            } else if (which & 1) {
+                const int R0 = min(max(i - rt.d0[rb + x], 0), T - 1);
+#pragma unroll
+                for (int sidx = 0; sidx < NS; ++sidx) {
+                    const int R = max(R0 - sidx, 0);
+                    kx[x * NS + sidx] = load_row(K, R, gq);
+                    vx[x * NS + sidx] = load_row(V, R, gq);
+                }
             }
         }
     };
     Slice kA[RB * NS], vA[RB * NS], kB[RB * NS], vB[RB * NS];
-    if (0 < nact) load_batch(0, kA, vA);  // in flight during the band phase
-    // band rows [T0-16, T0+64) of K and V, straight to LDS (rows outside [0, T) are
+    if (0 < nact) load_batch(0, kA, vA, 1);  // in flight during the band phase
+    // rows [T0-kLeadF, T0+64) of K and V, straight to LDS (rows outside [0, T) are
     // clamped copies: their keys are masked below)
-    dma_rows<kBandRows>(kr, K, T0 - 16, T);
-    dma_rows<kBandRows>(vr, V, T0 - 16, T);
+    dma_rows<kBandRows>(kr, K, T0 - kLeadF, T);
+    dma_rows<kBandRows>(vr, V, T0 - kLeadF, T);
     wait_vmem();
     __syncthreads();
+    if (0 < nact) load_batch(0, kA, vA, 2);
 
     // ---- window band (MFMA layout): logits (log2 units), maximum, probabilities ----
     const Slice qm = slice_from_quad(qq, lane);  // the wave's q rows in the MFMA layout
@@ -90,7 +116,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     f32x4 sb[2];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
-        const Slice kb = dma_slice(kr, 16 * wv + 16 * b + nm, gm);
+        const Slice kb = dma_slice(kr, kLeadF - 16 + 16 * wv + 16 * b + nm, gm);
         sb[b] = mfma_dot64(kb, qm, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -120,7 +146,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     Acc16 acc;
 #pragma unroll
     for (int c = 0; c < 4; ++c)
-        acc.c[c] = mfma(dma_operand_t(vr, c, nm, 16 * wv, gm), P, f32x4{0.f, 0.f, 0.f, 0.f});
+        acc.c[c] = mfma(dma_operand_t(vr, c, nm, kLeadF - 16 + 16 * wv, gm), P, f32x4{0.f, 0.f, 0.f, 0.f});
     // hand the band results to the quad layout
     acc_to_quad(acc, lane);
     m = to_quad(m, lane);
@@ -173,10 +199,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
 #pragma unroll
     for (int rb = 0; rb < kMaxRungs; rb += 2 * RB) {
         if (rb < nact) {
-            if (rb + RB < nact) load_batch(rb + RB, kB, vB);
+            if (rb + RB < nact) load_batch(rb + RB, kB, vB, 3);
             compute_batch(rb, kA, vA);
             if (rb + RB < nact) {
-                if (rb + 2 * RB < nact) load_batch(rb + 2 * RB, kA, vA);
+                if (rb + 2 * RB < nact) load_batch(rb + 2 * RB, kA, vA, 3);
                 compute_batch(rb + RB, kB, vB);
             }
         }
