@@ -45,6 +45,10 @@ SMALL = [
     (1, 1, 300, 64, "fp32", 128, FIB, 1.1),        # maximum window
     (1, 1, 700, 32, "fp32", 0, list(range(3, 99, 3)), 0.9),  # K = 32
     (1, 2, 200, 64, "bf16", 8, FIB, 0.01),         # tiny alpha: all rungs in the window
+    # 320 workgroups: 40 per XCD, so the reversed second run of the block order is
+    # a partial one (8 positions)
+    (1, 5, 4096, 64, "bf16", 8, FIB, 1.0),
+    (1, 5, 4096, 64, "bf16", 8, FIB, 0.9),
 ]
 
 
