@@ -70,10 +70,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     const int t0 = T0 + 16 * wv;
     const int im = t0 + nm, imc = min(im, T - 1);  // MFMA layout query
     const int i = t0 + nq, ic = min(i, T - 1);     // quad layout query
-    const Slice qm = load_row(Q, imc, gm);
-    const Slice gmm = load_row(G, imc, gm);
     const Slice qq = load_row(Q, ic, gq);
     const Slice gqq = load_row(G, ic, gq);
+    // the same rows in the MFMA layout, by lane shuffles rather than a second read
+    const Slice qm = slice_from_quad(qq, lane);
+    const Slice gmm = slice_from_quad(gqq, lane);
     const Slice oq = load_row(o + off, ic, gq);
     const float lse2 = L[ic] * kLog2e;
     const float lse2_m = L[imc] * kLog2e;
