@@ -58,15 +58,15 @@ def parse_args():
 #            --no-learned-alpha --no-integer-offsets --copy-probe-mb 256
 # each scaled by what the same counter reads for the plain 256 MiB device copy of that run.
 # They hold only for the kernel sources they were taken on (COUNTER_SOURCES_SHA).
-COUNTER_SOURCES_SHA = "b315f3f2d1880831103aa4e1bf27fa5c1e15fbd85f896b308ee017d5ef5ea76c"
+COUNTER_SOURCES_SHA = "d759f52a4deacbe137e4746492537acb53f30374c901898b47bef283d7b004cf"
 COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
 COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
-    "forward": (12403.6, 8448.0),
-    "bwd_dq": (20783.2, 8480.0),
-    "bwd_dkdv": (17895.0, 16384.0),
+    "forward": (12402.1, 8448.0),
+    "bwd_dq": (20772.7, 8480.0),
+    "bwd_dkdv": (17774.5, 16384.0),
     "rope": (8220.3, 16384.0),
 }
-COPY_PROBE_KIB = (262144.0, 131092.8, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
+COPY_PROBE_KIB = (262144.0, 131092.4, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
 
 
 def kernel_sources_sha() -> str:

@@ -23,6 +23,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef short v4i16 __attribute__((ext_vector_type(4)));
 
 constexpr int kD = 64;
 
@@ -251,22 +252,26 @@ __device__ __forceinline__ Slice dma_slice(const uint16_t *src, int rr, int g) {
     s.b = dma_chunk(src, rr, 4 + g);
     return s;
 }
-// Element (band row rr, dim d) of rows staged by dma_rows.
-__device__ __forceinline__ uint16_t dma_elem(const uint16_t *src, int rr, int d) {
-    return src[rr * kD + 8 * ((d >> 3) ^ (rr & 7)) + (d & 7)];
-}
 // A operand of a transposed-operand MFMA from rows staged by dma_rows: output dim
-// out_dim(c, n); k index 8g + j is staged row base + 4g + (j & 3) + 16 (j >> 2).
-__device__ __forceinline__ bf16x8 dma_operand_t(const uint16_t *src, int c, int n, int base, int g) {
-    const int d = out_dim(c, n);
-    uint32_t a[4];
+// out_dim(c, n) for lane n of each 16-lane group g; k index 8g + j is staged row
+// base + 4g + (j & 3) + 16 (j >> 2).  Two gfx950 LDS transpose reads
+// (ds_read_b64_tr_b16): in each 16-lane group, lane m points at 4 dims
+// (8 bytes) of one row, and lane n receives element n % 4 of the blocks read by
+// lanes n / 4, n / 4 + 4, n / 4 + 8 and n / 4 + 12.  So lane m reads row
+// k0 + m / 4, dims B + 8 (m % 4) .. + 3, and lane n gets dim B + 8 (n / 4) + n % 4 of
+// rows k0 .. k0 + 3: out_dim(c, n) with B = 32 [c >= 2] + 4 (c & 1).
+__device__ __forceinline__ bf16x8 dma_operand_t(const uint16_t *src, int c, int /*n*/, int base, int g) {
+    const int m = threadIdx.x & 15;
+    const int ch = (c < 2 ? 0 : 4) + (m & 3);  // 16-byte chunk holding the lane's 4 dims
+    const int off = 4 * (c & 1);
+    v4i16 t[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-        const int r = base + 16 * h + 4 * g;
-        a[2 * h] = (uint32_t)dma_elem(src, r, d) | ((uint32_t)dma_elem(src, r + 1, d) << 16);
-        a[2 * h + 1] = (uint32_t)dma_elem(src, r + 2, d) | ((uint32_t)dma_elem(src, r + 3, d) << 16);
+        const int r = base + 16 * h + 4 * g + (m >> 2);
+        t[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) v4i16 *)(src + r * kD + 8 * (ch ^ (r & 7)) + off));
     }
-    return as_bf8(make_uint4(a[0], a[1], a[2], a[3]));
+    return __builtin_bit_cast(bf16x8, t);
 }
 // Waits for this wave's outstanding vector-memory loads, direct-to-LDS ones included.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
