@@ -116,7 +116,7 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(
     __syncthreads();
 #pragma unroll
     for (int st = 128; st >= 1; st >>= 1) {
-        if (threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+        if ((int)threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
         __syncthreads();
     }
     if (threadIdx.x == 0) partials[(size_t)blockIdx.y * gridDim.x + blockIdx.x] = red[0];
@@ -248,7 +248,7 @@ __global__ __launch_bounds__(256) void dalpha_reduce_kernel(const double *__rest
     __syncthreads();
 #pragma unroll
     for (int st = 128; st >= 1; st >>= 1) {
-        if (threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+        if ((int)threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
         __syncthreads();
     }
     if (threadIdx.x == 0) *dalpha = (float)red[0];

@@ -273,7 +273,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         red[threadIdx.x] = s;
         __syncthreads();
         for (int st = 128; st >= 1; st >>= 1) {
-            if (threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+            if ((int)threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
             __syncthreads();
         }
         if (threadIdx.x == 0) *dalpha = (float)red[0];
