@@ -146,6 +146,41 @@ fibattn_status_t fibattn_backward_gqa(const void *q, const void *k, const void *
                                       fibattn_dtype_t dtype, hipStream_t stream);
 
 /*
+ * Tensors in any placement whose rows are contiguous, e.g. q, k, v taken straight out
+ * of a [B, T, H, d_head] or a packed [B, T, 3, H, d_head] projection output, without a
+ * copy.  A layout gives element strides: element (b, h, t, c) of a [B, heads, T,
+ * d_head] tensor is at  b*batch + h*head + t*pos + c  elements from its pointer.
+ *   layouts (host array, read during the call):
+ *     fibattn_forward_strided : 4 entries, for q, k, v, o
+ *     fibattn_backward_strided: 8 entries, for q, k, v, o, dO, dq, dk, dv
+ *   Requirements (else FIBATTN_ERR_INVALID_ARG): batch, head, pos >= 0 and multiples of
+ *   16 bytes (8 bf16 or 4 float32 elements), so that every row is 16-byte aligned.
+ *   FIBATTN_ERR_UNSUPPORTED when a row of a head starts 2^31 bytes or more after the
+ *   head's first row.  lse and the workspace stay packed ([B,H,T] float32).  The caller
+ *   guarantees that no two output rows overlap each other or an input row (not
+ *   checked).  Otherwise exactly fibattn_forward_gqa / fibattn_backward_gqa; the
+ *   packed entry points are these with layouts (H*T*d, T*d, d) (heads H or H_kv).
+ */
+typedef struct {
+    int64_t batch, head, pos;
+} fibattn_layout_t;
+
+fibattn_status_t fibattn_forward_strided(const void *q, const void *k, const void *v,
+                                         void *o, float *lse, const fibattn_layout_t *layouts,
+                                         int B, int H, int H_kv, int T, int d_head, int W,
+                                         const int32_t *base, int K, float alpha,
+                                         fibattn_dtype_t dtype, hipStream_t stream);
+
+fibattn_status_t fibattn_backward_strided(const void *q, const void *k, const void *v,
+                                          const void *o, const float *lse, const void *dO,
+                                          void *dq, void *dk, void *dv, float *dalpha,
+                                          void *workspace, size_t workspace_bytes,
+                                          const fibattn_layout_t *layouts,
+                                          int B, int H, int H_kv, int T, int d_head, int W,
+                                          const int32_t *base, int K, float alpha, float rope_base,
+                                          fibattn_dtype_t dtype, hipStream_t stream);
+
+/*
  * Device-resident alpha (Section 2, "The per-layer scalar": alpha = 0.5 + sigmoid(theta)
  * with theta learned per layer), so that a training step never reads alpha on the host.
  *

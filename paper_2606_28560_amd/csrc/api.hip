@@ -49,6 +49,25 @@ fibattn_status_t check_common(int B, int H, int T, int d_head, int W, int K, fib
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Every tensor packed [B, heads, T, d].
+Layouts packed_layouts(int H, int H_kv, int T, int D) {
+    const Layout lq = Layout::packed(H, T, D), lk = Layout::packed(H_kv, T, D);
+    return {lq, lk, lk, lq, lq, lq, lk, lk};
+}
+
+// A caller's placement of one tensor: non-negative strides that keep every row 16-byte
+// aligned, and row offsets within a head below 2^31 bytes (the kernels address rows
+// with 32-bit offsets from the head's first row).
+fibattn_status_t check_layout(const fibattn_layout_t &l, int T, int d_head, fibattn_dtype_t dtype,
+                              Layout *out) {
+    const long long es = dtype == FIBATTN_BF16 ? 2 : 4;
+    if (l.batch < 0 || l.head < 0 || l.pos < 0) return FIBATTN_ERR_INVALID_ARG;
+    if ((l.batch * es) % 16 || (l.head * es) % 16 || (l.pos * es) % 16) return FIBATTN_ERR_INVALID_ARG;
+    if (((long long)(T - 1) * l.pos + d_head) * es >= (1ll << 31)) return FIBATTN_ERR_UNSUPPORTED;
+    *out = {l.batch, l.head, l.pos};
+    return FIBATTN_OK;
+}
+
 // ---- kernel timing -------------------------------------------------------
 struct Timing {
     int id = -1;
@@ -84,10 +103,10 @@ fibattn_status_t fibattn_rung_table(float alpha, const int32_t *base, int K, int
     return FIBATTN_OK;
 }
 
-fibattn_status_t fibattn_forward_gqa(const void *q, const void *k, const void *v, void *o,
-                                     float *lse, int B, int H, int H_kv, int T, int d_head, int W,
-                                     const int32_t *base, int K, float alpha, fibattn_dtype_t dtype,
-                                     hipStream_t stream) {
+static fibattn_status_t forward_impl(const void *q, const void *k, const void *v, void *o, float *lse,
+                                     const Layouts &lay, int B, int H, int H_kv, int T, int d_head,
+                                     int W, const int32_t *base, int K, float alpha,
+                                     fibattn_dtype_t dtype, hipStream_t stream) {
     fibattn_status_t st = check_common(B, H, T, d_head, W, K, dtype);
     if (st != FIBATTN_OK) return st;
     if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
@@ -99,8 +118,32 @@ fibattn_status_t fibattn_forward_gqa(const void *q, const void *k, const void *v
     if (st != FIBATTN_OK) return st;
     const Heads hd{H, H / H_kv};
     hipError_t e = launch_forward((int)dtype, d_head, q, k, v, o, lse, B * H, hd, T, W, rt, nullptr,
-                                  stream);
+                                  lay, stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
+fibattn_status_t fibattn_forward_gqa(const void *q, const void *k, const void *v, void *o,
+                                     float *lse, int B, int H, int H_kv, int T, int d_head, int W,
+                                     const int32_t *base, int K, float alpha, fibattn_dtype_t dtype,
+                                     hipStream_t stream) {
+    if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
+    return forward_impl(q, k, v, o, lse, packed_layouts(H, H_kv, T, d_head), B, H, H_kv, T, d_head, W,
+                        base, K, alpha, dtype, stream);
+}
+
+fibattn_status_t fibattn_forward_strided(const void *q, const void *k, const void *v, void *o,
+                                         float *lse, const fibattn_layout_t *layouts, int B, int H,
+                                         int H_kv, int T, int d_head, int W, const int32_t *base,
+                                         int K, float alpha, fibattn_dtype_t dtype,
+                                         hipStream_t stream) {
+    if (!layouts || T < 1) return FIBATTN_ERR_INVALID_ARG;
+    Layouts lay = packed_layouts(H, H_kv > 0 ? H_kv : 1, T, d_head);
+    Layout *dst[4] = {&lay.q, &lay.k, &lay.v, &lay.o};
+    for (int a = 0; a < 4; ++a) {
+        const fibattn_status_t st = check_layout(layouts[a], T, d_head, dtype, dst[a]);
+        if (st != FIBATTN_OK) return st;
+    }
+    return forward_impl(q, k, v, o, lse, lay, B, H, H_kv, T, d_head, W, base, K, alpha, dtype, stream);
 }
 
 fibattn_status_t fibattn_forward(const void *q, const void *k, const void *v, void *o, float *lse,
@@ -121,12 +164,13 @@ size_t fibattn_backward_workspace_bytes(int B, int H, int T, int d_head, int W, 
     return align256(sizeof(float) * (size_t)B * H * T) + align256(sizeof(double) * np);
 }
 
-fibattn_status_t fibattn_backward_gqa(const void *q, const void *k, const void *v, const void *o,
+static fibattn_status_t backward_impl(const void *q, const void *k, const void *v, const void *o,
                                       const float *lse, const void *dO, void *dq, void *dk,
                                       void *dv, float *dalpha, void *workspace,
-                                      size_t workspace_bytes, int B, int H, int H_kv, int T,
-                                      int d_head, int W, const int32_t *base, int K, float alpha,
-                                      float rope_base, fibattn_dtype_t dtype, hipStream_t stream) {
+                                      size_t workspace_bytes, const Layouts &lay, int B, int H,
+                                      int H_kv, int T, int d_head, int W, const int32_t *base,
+                                      int K, float alpha, float rope_base, fibattn_dtype_t dtype,
+                                      hipStream_t stream) {
     fibattn_status_t st = check_common(B, H, T, d_head, W, K, dtype);
     if (st != FIBATTN_OK) return st;
     if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
@@ -148,8 +192,38 @@ fibattn_status_t fibattn_backward_gqa(const void *q, const void *k, const void *
     const Heads hd{H, H / H_kv};
     hipError_t e = launch_backward((int)dtype, d_head, q, k, v, o, lse, dO, dq, dk, dv, dalpha,
                                    delta_ws, partials, B * H, hd, T, W, rt, nullptr, rf, rope_base,
-                                   stream);
+                                   lay, stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
+fibattn_status_t fibattn_backward_gqa(const void *q, const void *k, const void *v, const void *o,
+                                      const float *lse, const void *dO, void *dq, void *dk,
+                                      void *dv, float *dalpha, void *workspace,
+                                      size_t workspace_bytes, int B, int H, int H_kv, int T,
+                                      int d_head, int W, const int32_t *base, int K, float alpha,
+                                      float rope_base, fibattn_dtype_t dtype, hipStream_t stream) {
+    if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
+    return backward_impl(q, k, v, o, lse, dO, dq, dk, dv, dalpha, workspace, workspace_bytes,
+                         packed_layouts(H, H_kv, T, d_head), B, H, H_kv, T, d_head, W, base, K, alpha,
+                         rope_base, dtype, stream);
+}
+
+fibattn_status_t fibattn_backward_strided(const void *q, const void *k, const void *v, const void *o,
+                                          const float *lse, const void *dO, void *dq, void *dk,
+                                          void *dv, float *dalpha, void *workspace,
+                                          size_t workspace_bytes, const fibattn_layout_t *layouts,
+                                          int B, int H, int H_kv, int T, int d_head, int W,
+                                          const int32_t *base, int K, float alpha, float rope_base,
+                                          fibattn_dtype_t dtype, hipStream_t stream) {
+    if (!layouts || T < 1) return FIBATTN_ERR_INVALID_ARG;
+    Layouts lay = packed_layouts(H, H_kv > 0 ? H_kv : 1, T, d_head);
+    Layout *dst[8] = {&lay.q, &lay.k, &lay.v, &lay.o, &lay.g, &lay.dq, &lay.dk, &lay.dv};
+    for (int a = 0; a < 8; ++a) {
+        const fibattn_status_t st = check_layout(layouts[a], T, d_head, dtype, dst[a]);
+        if (st != FIBATTN_OK) return st;
+    }
+    return backward_impl(q, k, v, o, lse, dO, dq, dk, dv, dalpha, workspace, workspace_bytes, lay, B, H,
+                         H_kv, T, d_head, W, base, K, alpha, rope_base, dtype, stream);
 }
 
 fibattn_status_t fibattn_backward(const void *q, const void *k, const void *v, const void *o,
@@ -191,7 +265,7 @@ fibattn_status_t fibattn_forward_dt(const void *q, const void *k, const void *v,
     memset(&unused, 0, sizeof(unused));
     const Heads hd{H, H / H_kv};
     hipError_t e = launch_forward((int)dtype, d_head, q, k, v, o, lse, B * H, hd, T, W, unused,
-                                  (const RungTable *)table, stream);
+                                  (const RungTable *)table, packed_layouts(H, H_kv, T, d_head), stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
 }
 
@@ -220,7 +294,8 @@ fibattn_status_t fibattn_backward_dt(const void *q, const void *k, const void *v
     const Heads hd{H, H / H_kv};
     hipError_t e = launch_backward((int)dtype, d_head, q, k, v, o, lse, dO, dq, dk, dv, dalpha,
                                    delta_ws, partials, B * H, hd, T, W, unused,
-                                   (const RungTable *)table, rf, rope_base, stream);
+                                   (const RungTable *)table, rf, rope_base,
+                                   packed_layouts(H, H_kv, T, d_head), stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
 }
 
@@ -246,8 +321,9 @@ fibattn_status_t fibattn_rope(const void *x, void *y, int B, int H, int T, int d
     if (!(rope_base > 1.f) || !isfinite(rope_base)) return FIBATTN_ERR_INVALID_ARG;
     if (d_head != 32 && d_head != 64 && d_head != 128) return FIBATTN_ERR_UNSUPPORTED;
     if ((long long)B * H > 65535ll * 16) return FIBATTN_ERR_UNSUPPORTED;
-    hipError_t e = launch_rope((int)dtype, d_head, x, y, nullptr, nullptr, B * H, T, rope_base,
-                               transpose, stream);
+    const Layout l = Layout::packed(H, T, d_head);
+    hipError_t e = launch_rope((int)dtype, d_head, x, y, l, l, nullptr, nullptr, l, l, B * H, H, T,
+                               rope_base, transpose, stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
 }
 
@@ -261,7 +337,9 @@ fibattn_status_t fibattn_rope_qk(const void *q, const void *k, void *q_out, void
     if (!(rope_base > 1.f) || !isfinite(rope_base)) return FIBATTN_ERR_INVALID_ARG;
     if (d_head != 32 && d_head != 64 && d_head != 128) return FIBATTN_ERR_UNSUPPORTED;
     if ((long long)B * H > 65535ll * 16) return FIBATTN_ERR_UNSUPPORTED;
-    hipError_t e = launch_rope((int)dtype, d_head, q, q_out, k, k_out, B * H, T, rope_base, 0, stream);
+    const Layout l = Layout::packed(H, T, d_head);
+    hipError_t e = launch_rope((int)dtype, d_head, q, q_out, l, l, k, k_out, l, l, B * H, H, T, rope_base,
+                               0, stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
 }
 

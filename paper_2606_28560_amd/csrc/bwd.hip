@@ -31,7 +31,7 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(
     const S *__restrict__ q, const S *__restrict__ k, const S *__restrict__ v,
     const S *__restrict__ o, const float *__restrict__ lse, const S *__restrict__ dO,
     S *__restrict__ dq, float *__restrict__ delta_out, double *__restrict__ partials, int T,
-    int W, RungTable rt_arg, const RungTable *__restrict__ rtp, float tau, Heads hd) {
+    int W, RungTable rt_arg, const RungTable *__restrict__ rtp, float tau, Heads hd, Layouts lay) {
     const RungTable &rt = DEV ? *rtp : rt_arg;
     const bool bad = DEV && rt.n < 0;  // a device alpha that is not finite and positive
     constexpr int VN = Vec<S>::N;
@@ -42,20 +42,20 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(
     const int g = threadIdx.x / LPQ;
     const int sub = threadIdx.x % LPQ;
     const int i = blockIdx.x * QPB + g;
-    const size_t off = (size_t)blockIdx.y * T * D;
-    const size_t kvoff = (size_t)hd.kv_of(blockIdx.y) * T * D;
-    const S *Q = q + off;
-    const S *K = k + kvoff;
-    const S *V = v + kvoff;
+    const int bk = hd.kv_of(blockIdx.y);
+    const S *Q = q + lay.q.head(blockIdx.y, hd.H);
+    const S *K = k + lay.k.head(bk, hd.kv_heads());
+    const S *V = v + lay.v.head(bk, hd.kv_heads());
+    const long long sq = lay.q.st, sk = lay.k.st, sv = lay.v.st;  // row strides
     const int col = sub * VN;
     const float sl2 = tau * kLog2e;
 
     double dal = 0.0;
     if (i < T) {
         float qv[VN], gv[VN], kv[VN], vv[VN], acc[VN];
-        Vec<S>::load(Q + (size_t)i * D + col, qv);
-        Vec<S>::load(dO + off + (size_t)i * D + col, gv);
-        Vec<S>::load(o + off + (size_t)i * D + col, kv);
+        Vec<S>::load(Q + i * sq + col, qv);
+        Vec<S>::load(dO + lay.g.head(blockIdx.y, hd.H) + i * lay.g.st + col, gv);
+        Vec<S>::load(o + lay.o.head(blockIdx.y, hd.H) + i * lay.o.st + col, kv);
         const float delta = group_sum<LPQ>(dot<VN>(gv, kv));
         if (sub == 0) delta_out[(size_t)blockIdx.y * T + i] = bad ? NAN : delta;
         const float lse2 = lse[(size_t)blockIdx.y * T + i] * kLog2e;
@@ -64,9 +64,8 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(
 
         const int wmax = min(W, i);
         for (int d = 0; d <= wmax; ++d) {
-            const size_t row = (size_t)(i - d) * D + col;
-            Vec<S>::load(K + row, kv);
-            Vec<S>::load(V + row, vv);
+            Vec<S>::load(K + (i - d) * sk + col, kv);
+            Vec<S>::load(V + (i - d) * sv + col, vv);
             const float s = group_sum<LPQ>(dot<VN>(qv, kv));
             const float dP = group_sum<LPQ>(dot<VN>(gv, vv));
             const float p = exp2f(s * sl2 - lse2);
@@ -80,11 +79,11 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(
             if (!(d0 < i || (d0 == i && w == 0.f))) break;
             const int r0 = i - d0;
             float k1[VN], v1[VN];
-            Vec<S>::load(K + (size_t)r0 * D + col, kv);
-            Vec<S>::load(V + (size_t)r0 * D + col, vv);
+            Vec<S>::load(K + r0 * sk + col, kv);
+            Vec<S>::load(V + r0 * sv + col, vv);
             if (r0 >= 1) {
-                Vec<S>::load(K + (size_t)(r0 - 1) * D + col, k1);
-                Vec<S>::load(V + (size_t)(r0 - 1) * D + col, v1);
+                Vec<S>::load(K + (r0 - 1) * sk + col, k1);
+                Vec<S>::load(V + (r0 - 1) * sv + col, v1);
             } else {
 #pragma unroll
                 for (int x = 0; x < VN; ++x) { k1[x] = 0.f; v1[x] = 0.f; }
@@ -110,7 +109,7 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(
             for (int x = 0; x < VN; ++x) acc[x] = NAN;
             dal = NAN;
         }
-        Vec<S>::store(dq + off + (size_t)i * D + col, acc);
+        Vec<S>::store(dq + lay.dq.head(blockIdx.y, hd.H) + i * lay.dq.st + col, acc);
     }
     red[threadIdx.x] = (sub == 0 && i < T) ? dal : 0.0;
     __syncthreads();
@@ -130,7 +129,7 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(
     const S *__restrict__ q, const S *__restrict__ k, const S *__restrict__ v,
     const float *__restrict__ lse, const S *__restrict__ dO, const float *__restrict__ delta_in,
     S *__restrict__ dk, S *__restrict__ dv, int T, int W, RungTable rt_arg,
-    const RungTable *__restrict__ rtp, float tau, Heads hd) {
+    const RungTable *__restrict__ rtp, float tau, Heads hd, Layouts lay) {
     const RungTable &rt = DEV ? *rtp : rt_arg;
     constexpr int VN = Vec<S>::N;
     constexpr int LPQ = D / VN;
@@ -140,32 +139,32 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(
     const int sub = threadIdx.x % LPQ;
     const int j = blockIdx.x * QPB + g;
     if (j >= T) return;  // whole lane groups leave together; no block barrier below
-    const size_t kvoff = (size_t)blockIdx.y * T * D;  // blockIdx.y: batch * key/value head
-    const S *K = k + kvoff;
-    const S *V = v + kvoff;
+    const int bk = blockIdx.y;  // batch * key/value heads + key/value head
+    const S *K = k + lay.k.head(bk, hd.kv_heads());
+    const S *V = v + lay.v.head(bk, hd.kv_heads());
+    const long long sq = lay.q.st, sk = lay.k.st, sv = lay.v.st, sg = lay.g.st;  // row strides
     const int col = sub * VN;
     const float sl2 = tau * kLog2e;
 
     float kj[VN], vj[VN], adk[VN], adv[VN], qv[VN], gv[VN];
-    Vec<S>::load(K + (size_t)j * D + col, kj);
-    Vec<S>::load(V + (size_t)j * D + col, vj);
+    Vec<S>::load(K + j * sk + col, kj);
+    Vec<S>::load(V + j * sv + col, vj);
 #pragma unroll
     for (int c = 0; c < VN; ++c) { adk[c] = 0.f; adv[c] = 0.f; }
 
     // every query head of the group reads this key row; their terms add up
     for (int hg = 0; hg < hd.G; ++hg) {
         const int bh = hd.q_of(blockIdx.y, hg);
-        const size_t off = (size_t)bh * T * D;
-        const S *Q = q + off;
-        const S *G = dO + off;
+        const S *Q = q + lay.q.head(bh, hd.H);
+        const S *G = dO + lay.g.head(bh, hd.H);
         const float *L = lse + (size_t)bh * T;
         const float *Dl = delta_in + (size_t)bh * T;
 
         // window: queries i = j .. j+W read row j with weight 1
         const int imax = min(T - 1, j + W);
         for (int i = j; i <= imax; ++i) {
-            Vec<S>::load(Q + (size_t)i * D + col, qv);
-            Vec<S>::load(G + (size_t)i * D + col, gv);
+            Vec<S>::load(Q + i * sq + col, qv);
+            Vec<S>::load(G + i * sg + col, gv);
             const float s = group_sum<LPQ>(dot<VN>(qv, kj));
             const float dP = group_sum<LPQ>(dot<VN>(gv, vj));
             const float p = exp2f(s * sl2 - L[i] * kLog2e);
@@ -185,13 +184,13 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(
             float kn[VN], vn[VN];
             // query i0 reads row j as r0 (weight 1-w) and row j-1 as r1; included iff w <= j
             if (w == 0.f || j >= 1) {
-                Vec<S>::load(Q + (size_t)i0 * D + col, qv);
-                Vec<S>::load(G + (size_t)i0 * D + col, gv);
+                Vec<S>::load(Q + i0 * sq + col, qv);
+                Vec<S>::load(G + i0 * sg + col, gv);
                 float s = (1.f - w) * dot<VN>(qv, kj);
                 float dP = (1.f - w) * dot<VN>(gv, vj);
                 if (w != 0.f) {
-                    Vec<S>::load(K + (size_t)(j - 1) * D + col, kn);
-                    Vec<S>::load(V + (size_t)(j - 1) * D + col, vn);
+                    Vec<S>::load(K + (j - 1) * sk + col, kn);
+                    Vec<S>::load(V + (j - 1) * sv + col, vn);
                     s = fmaf(w, dot<VN>(qv, kn), s);
                     dP = fmaf(w, dot<VN>(gv, vn), dP);
                 }
@@ -209,10 +208,10 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(
             // query i0+1 reads row j+1 as r0 and row j as r1 (weight w); always included
             const int i1 = i0 + 1;
             if (w != 0.f && i1 < T) {
-                Vec<S>::load(Q + (size_t)i1 * D + col, qv);
-                Vec<S>::load(G + (size_t)i1 * D + col, gv);
-                Vec<S>::load(K + (size_t)(j + 1) * D + col, kn);
-                Vec<S>::load(V + (size_t)(j + 1) * D + col, vn);
+                Vec<S>::load(Q + i1 * sq + col, qv);
+                Vec<S>::load(G + i1 * sg + col, gv);
+                Vec<S>::load(K + (j + 1) * sk + col, kn);
+                Vec<S>::load(V + (j + 1) * sv + col, vn);
                 float s = fmaf(1.f - w, dot<VN>(qv, kn), w * dot<VN>(qv, kj));
                 float dP = fmaf(1.f - w, dot<VN>(gv, vn), w * dot<VN>(gv, vj));
                 s = group_sum<LPQ>(s);
@@ -232,8 +231,8 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(
 #pragma unroll
         for (int x = 0; x < VN; ++x) { adk[x] = NAN; adv[x] = NAN; }
     }
-    Vec<S>::store(dk + kvoff + (size_t)j * D + col, adk);
-    Vec<S>::store(dv + kvoff + (size_t)j * D + col, adv);
+    Vec<S>::store(dk + lay.dk.head(bk, hd.kv_heads()) + j * lay.dk.st + col, adk);
+    Vec<S>::store(dv + lay.dv.head(bk, hd.kv_heads()) + j * lay.dv.st + col, adv);
 }
 
 // ---------------------------------------------------------------------------
@@ -275,17 +274,17 @@ static hipError_t launch_bwd_t(const void *q, const void *k, const void *v, cons
                                const float *lse, const void *dO, void *dq, void *dk, void *dv,
                                float *dalpha, float *delta_ws, double *partials, int BH,
                                const Heads &hd, int T, int W, const RungTable &rt,
-                               const RungTable *rtp, hipStream_t s) {
+                               const RungTable *rtp, const Layouts &lay, hipStream_t s) {
     constexpr int QPB = 256 / (D / Vec<S>::N);
     const float tau = 1.f / sqrtf((float)D);
     dim3 grid((T + QPB - 1) / QPB, BH);
     hipError_t e = launch(kBwdDq, rtp ? bwd_dq_kernel<S, D, true> : bwd_dq_kernel<S, D, false>, grid,
                           dim3(256), 0, s, (const S *)q, (const S *)k, (const S *)v, (const S *)o,
-                          lse, (const S *)dO, (S *)dq, delta_ws, partials, T, W, rt, rtp, tau, hd);
+                          lse, (const S *)dO, (S *)dq, delta_ws, partials, T, W, rt, rtp, tau, hd, lay);
     if (e != hipSuccess) return e;
     e = launch(kBwdDkDv, rtp ? bwd_dkdv_kernel<S, D, true> : bwd_dkdv_kernel<S, D, false>,
                dim3(grid.x, BH / hd.G), dim3(256), 0, s, (const S *)q, (const S *)k, (const S *)v,
-               lse, (const S *)dO, delta_ws, (S *)dk, (S *)dv, T, W, rt, rtp, tau, hd);
+               lse, (const S *)dO, delta_ws, (S *)dk, (S *)dv, T, W, rt, rtp, tau, hd, lay);
     if (e != hipSuccess) return e;
     return launch(kDalphaReduce, dalpha_reduce_kernel, dim3(1), dim3(256), 0, s, partials,
                   (size_t)grid.x * grid.y, dalpha);
@@ -295,10 +294,11 @@ static hipError_t launch_backward_generic(int dtype, int D, const void *q, const
                                           const void *o, const float *lse, const void *dO, void *dq,
                                           void *dk, void *dv, float *dalpha, float *delta_ws,
                                           double *partials, int BH, const Heads &hd, int T, int W,
-                                          const RungTable &rt, const RungTable *rtp, hipStream_t s) {
+                                          const RungTable &rt, const RungTable *rtp, const Layouts &lay,
+                                          hipStream_t s) {
 #define FIBATTN_BWD(S_, D_)                                                                  \
     return launch_bwd_t<S_, D_>(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials, \
-                                BH, hd, T, W, rt, rtp, s)
+                                BH, hd, T, W, rt, rtp, lay, s)
     if (dtype == 0 && D == 32) FIBATTN_BWD(float, 32);
     if (dtype == 0 && D == 64) FIBATTN_BWD(float, 64);
     if (dtype == 1 && D == 32) FIBATTN_BWD(uint16_t, 32);
@@ -314,20 +314,25 @@ hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const
                            const void *o, const float *lse, const void *dO, void *dq, void *dk,
                            void *dv, float *dalpha, float *delta_ws, double *partials, int BH,
                            const Heads &hd, int T, int W, const RungTable &rt,
-                           const RungTable *rtp, const RopeFreq &rf, float rope_base, hipStream_t s) {
+                           const RungTable *rtp, const RopeFreq &rf, float rope_base,
+                           const Layouts &lay, hipStream_t s) {
     if (backward_mfma_supported(dtype, D, W))
         return launch_backward_mfma(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials, BH,
-                                    hd, T, W, rt, rtp, rf, s);
+                                    hd, T, W, rt, rtp, rf, lay, s);
     hipError_t e = launch_backward_generic(dtype, D, q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws,
-                                           partials, BH, hd, T, W, rt, rtp, s);
+                                           partials, BH, hd, T, W, rt, rtp, lay, s);
     // R^T on dq and dk in place: gradients w.r.t. the unrotated q, k (R^T is linear, so
     // it also carries the group sum in dk)
     if (e == hipSuccess && rf.on) {
         if (hd.G == 1) {
-            e = launch_rope(dtype, D, dq, dq, dk, dk, BH, T, rope_base, 1, s);
+            e = launch_rope(dtype, D, dq, dq, lay.dq, lay.dq, dk, dk, lay.dk, lay.dk, BH, hd.H, T,
+                            rope_base, 1, s);
         } else {
-            e = launch_rope(dtype, D, dq, dq, nullptr, nullptr, BH, T, rope_base, 1, s);
-            if (e == hipSuccess) e = launch_rope(dtype, D, dk, dk, nullptr, nullptr, BH / hd.G, T, rope_base, 1, s);
+            e = launch_rope(dtype, D, dq, dq, lay.dq, lay.dq, nullptr, nullptr, lay.dq, lay.dq, BH, hd.H,
+                            T, rope_base, 1, s);
+            if (e == hipSuccess)
+                e = launch_rope(dtype, D, dk, dk, lay.dk, lay.dk, nullptr, nullptr, lay.dk, lay.dk,
+                                BH / hd.G, hd.kv_heads(), T, rope_base, 1, s);
         }
     }
     return e;

@@ -33,14 +33,15 @@ constexpr int kBwdB = 64;                // rows per workgroup
 
 // ---------------------------------------------------------------------------
 // INTERP: some rung has w != 0 (rows r0 and r1 both loaded per rung).  DEV: the rung
-// table is the one at rtp, built on the device (rt_arg unused).
-template <bool INTERP, bool DEV>
+// table is the one at rtp, built on the device (rt_arg unused).  STRIDED: rows placed
+// by the layouts' position strides (else every row stride is 64, a constant).
+template <bool INTERP, bool DEV, bool STRIDED>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void bwd_dq_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const uint16_t *__restrict__ o, const float *__restrict__ lse, const uint16_t *__restrict__ dO,
     uint16_t *__restrict__ dq, float *__restrict__ delta_out, double *__restrict__ partials, int T,
     int W, RungTable rt_arg, const RungTable *__restrict__ rtp, RopeFreq rf, float tau, int tiles,
-    Heads hd) {
+    Heads hd, Layouts lay) {
     const RungTable &rt = DEV ? *rtp : rt_arg;
     const bool bad = DEV && rt.n < 0;  // a device alpha that is not finite and positive
     // staged K, V rows [T0 - kLeadQ, T0 + 64): the band and, interpolating, the short rungs
@@ -58,24 +59,27 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     const int blk = xcd_remap(blockIdx.x, gridDim.x);
     const int bh = blk / tiles;
     const int T0 = (blk % tiles) * kBwdB;
-    const size_t off = (size_t)bh * T * kD;
-    const size_t kvoff = (size_t)hd.kv_of(bh) * T * kD;
-    const uint16_t *Q = q + off;
-    const uint16_t *K = k + kvoff;
-    const uint16_t *V = v + kvoff;
-    const uint16_t *G = dO + off;
+    const int bk = hd.kv_of(bh);
+    const uint16_t *Q = q + head_at<STRIDED, kD>(lay.q, bh, hd.H, T);
+    const uint16_t *K = k + head_at<STRIDED, kD>(lay.k, bk, hd.kv_heads(), T);
+    const uint16_t *V = v + head_at<STRIDED, kD>(lay.v, bk, hd.kv_heads(), T);
+    const uint16_t *G = dO + head_at<STRIDED, kD>(lay.g, bh, hd.H, T);
+    // row strides
+    const int stq = STRIDED ? (int)lay.q.st : kD, stk = STRIDED ? (int)lay.k.st : kD;
+    const int stv = STRIDED ? (int)lay.v.st : kD, stg = STRIDED ? (int)lay.g.st : kD;
+    const int sto = STRIDED ? (int)lay.o.st : kD, stdq = STRIDED ? (int)lay.dq.st : kD;
     const float *L = lse + (size_t)bh * T;
     const float sl2 = tau * kLog2e;
 
     const int t0 = T0 + 16 * wv;
     const int im = t0 + nm, imc = min(im, T - 1);  // MFMA layout query
     const int i = t0 + nq, ic = min(i, T - 1);     // quad layout query
-    const Slice qq = load_row(Q, ic, gq);
-    const Slice gqq = load_row(G, ic, gq);
+    const Slice qq = load_row(Q, ic, gq, stq);
+    const Slice gqq = load_row(G, ic, gq, stg);
     // the same rows in the MFMA layout, by lane shuffles rather than a second read
     const Slice qm = slice_from_quad(qq, lane);
     const Slice gmm = slice_from_quad(gqq, lane);
-    const Slice oq = load_row(o + off, ic, gq);
+    const Slice oq = load_row(o + head_at<STRIDED, kD>(lay.o, bh, hd.H, T), ic, gq, sto);
     const float lse2 = L[ic] * kLog2e;
     const float lse2_m = L[imc] * kLog2e;
 
@@ -107,12 +111,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
             }
         } else if (which & 1) {
             const int R0 = min(max(i - rt.d0[r], 0), T - 1);
-            x[0] = load_row(K, R0, gq);
-            x[1] = load_row(V, R0, gq);
+            x[0] = load_row(K, R0, gq, stk);
+            x[1] = load_row(V, R0, gq, stv);
             if (INTERP || (nq & 3) == 0) {
                 const int R1 = min(max(i - rt.d0[r] - 1, 0), T - 1);
-                x[2] = load_row(K, R1, gq);
-                x[3] = load_row(V, R1, gq);
+                x[2] = load_row(K, R1, gq, stk);
+                x[3] = load_row(V, R1, gq, stv);
             }
         }
     };
@@ -121,8 +125,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 
     // rows [T0-kLeadQ, T0+64) of K and V, straight to LDS (rows outside [0, T) are
     // clamped copies: their keys are masked below)
-    dma_rows<kStage>(kr, K, T0 - kLeadQ, T);
-    dma_rows<kStage>(vr, V, T0 - kLeadQ, T);
+    dma_rows<kStage>(kr, K, T0 - kLeadQ, T, stk);
+    dma_rows<kStage>(vr, V, T0 - kLeadQ, T, stv);
     stage_freq(sfreq, rf);
     // Delta_i = <dO_i, o_i>, once every load of the prologue is in flight
     const float delta = quad_sum(dot_slice(gqq, oq));
@@ -209,7 +213,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 
     if (rf.on) acc_rope_t(acc, i, sfreq + 8 * gq);  // gradient w.r.t. the unrotated q
     if (i < T) {
-        store_acc(dq + off + (size_t)i * kD, gq, acc, bad ? NAN : 1.f);
+        store_acc(dq + head_at<STRIDED, kD>(lay.dq, bh, hd.H, T) + (size_t)i * stdq, gq, acc, bad ? NAN : 1.f);
         if (gq == 0) delta_out[(size_t)bh * T + i] = bad ? NAN : delta;
     }
     if (bad) dal_q = NAN;
@@ -227,13 +231,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 // kKG = 4 / NH key groups of 16 keys times NH head slots; a group of G query heads
 // takes G / NH passes (ONE_PASS: G == NH, no pass loop), and the head slots' dk, dv
 // are summed through LDS at the end.
-template <bool INTERP, int NH, bool ONE_PASS, bool DEV>
+template <bool INTERP, int NH, bool ONE_PASS, bool DEV, bool STRIDED>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void bwd_dkdv_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const float *__restrict__ lse, const uint16_t *__restrict__ dO, const float *__restrict__ delta_in,
     uint16_t *__restrict__ dk, uint16_t *__restrict__ dv, const double *__restrict__ partials,
     int n_partials, float *__restrict__ dalpha, int T, int W, RungTable rt_arg,
-    const RungTable *__restrict__ rtp, RopeFreq rf, float tau, int tiles, Heads hd) {
+    const RungTable *__restrict__ rtp, RopeFreq rf, float tau, int tiles, Heads hd, Layouts lay) {
     const RungTable &rt = DEV ? *rtp : rt_arg;
     constexpr int kKG = 4 / NH;          // key groups of 16 per workgroup
     constexpr int kKeys = 16 * kKG;      // keys per workgroup
@@ -257,9 +261,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     const int blk = xcd_remap(blockIdx.x, gridDim.x);
     const int bk = blk / tiles;                // batch * key/value heads + key/value head
     const int T0 = (blk % tiles) * kKeys;
-    const size_t kvoff = (size_t)bk * T * kD;
-    const uint16_t *K = k + kvoff;
-    const uint16_t *V = v + kvoff;
+    const uint16_t *K = k + head_at<STRIDED, kD>(lay.k, bk, hd.kv_heads(), T);
+    const uint16_t *V = v + head_at<STRIDED, kD>(lay.v, bk, hd.kv_heads(), T);
+    // row strides
+    const int stq = STRIDED ? (int)lay.q.st : kD, stg = STRIDED ? (int)lay.g.st : kD;
+    const int stk = STRIDED ? (int)lay.k.st : kD, stv = STRIDED ? (int)lay.v.st : kD;
+    const int stdk = STRIDED ? (int)lay.dk.st : kD, stdv = STRIDED ? (int)lay.dv.st : kD;
     const float sl2 = tau * kLog2e;
     uint16_t *qr = stage + hs * kSt * kD;            // this wave's head slot
     uint16_t *gr = stage + (NH + hs) * kSt * kD;
@@ -301,9 +308,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         int j = j_key;
         asm volatile("" : "+v"(j));
         const int bh = hd.q_of(bk, pass * NH + hs);  // this wave's query head
-        const size_t off = (size_t)bh * T * kD;
-        const uint16_t *Q = q + off;
-        const uint16_t *Gd = dO + off;
+        const uint16_t *Q = q + head_at<STRIDED, kD>(lay.q, bh, hd.H, T);
+        const uint16_t *Gd = dO + head_at<STRIDED, kD>(lay.g, bh, hd.H, T);
         const float *L = lse + (size_t)bh * T;
         const float *Dl = delta_in + (size_t)bh * T;
 
@@ -317,8 +323,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 #pragma unroll
             for (int y = 0; y < 2; ++y) {
                 const int ic = min(j + rt.d0[r] + y, T - 1);
-                ru.x[2 * y] = load_row(Q, ic, gq);
-                ru.x[2 * y + 1] = load_row(Gd, ic, gq);
+                ru.x[2 * y] = load_row(Q, ic, gq, stq);
+                ru.x[2 * y + 1] = load_row(Gd, ic, gq, stg);
                 ru.le[y] = L[ic] * kLog2e;
                 ru.de[y] = Dl[ic];
             }
@@ -332,8 +338,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 #pragma unroll
             for (int y = 0; y < 2; ++y) {
                 const int ic = min(j + rt.d0[rb + y], T - 1);
-                pr.x[2 * y] = load_row(Q, ic, gq);
-                pr.x[2 * y + 1] = load_row(Gd, ic, gq);
+                pr.x[2 * y] = load_row(Q, ic, gq, stq);
+                pr.x[2 * y + 1] = load_row(Gd, ic, gq, stg);
                 pr.le[y] = L[ic] * kLog2e;
                 pr.de[y] = Dl[ic];
             }
@@ -350,9 +356,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         // past the end are clamped copies, masked below)
 #pragma unroll 1
         for (int u = 0; u < NH; ++u) {
-            const size_t ou = (size_t)hd.q_of(bk, pass * NH + u) * T;
-            dma_rows<kSt>(stage + u * kSt * kD, q + ou * kD, T0, T);
-            dma_rows<kSt>(stage + (NH + u) * kSt * kD, dO + ou * kD, T0, T);
+            const int hu = hd.q_of(bk, pass * NH + u);
+            const size_t ou = (size_t)hu * T;
+            dma_rows<kSt>(stage + u * kSt * kD, q + head_at<STRIDED, kD>(lay.q, hu, hd.H, T), T0, T, stq);
+            dma_rows<kSt>(stage + (NH + u) * kSt * kD, dO + head_at<STRIDED, kD>(lay.g, hu, hd.H, T), T0, T, stg);
             for (int c = threadIdx.x; c < kSt; c += 256) {
                 const int row = T0 + c;
                 sl[u * kSt + c] = row < T ? lse[ou + row] * kLog2e : 0.f;
@@ -360,8 +367,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
             }
         }
         if (pass == 0) {
-            dma_rows<kOwn>(kown, K, T0 - kLead, T);  // rows outside [0, T) are clamped copies
-            dma_rows<kOwn>(vown, V, T0 - kLead, T);
+            dma_rows<kOwn>(kown, K, T0 - kLead, T, stk);  // rows outside [0, T): clamped copies
+            dma_rows<kOwn>(vown, V, T0 - kLead, T, stv);
             stage_freq(sfreq, rf);
         }
         wait_vmem();
@@ -512,8 +519,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         if (rf.on) acc_rope_t(adk, j_key, sfreq + 8 * gq);  // gradient w.r.t. the unrotated k
         if (j_key < T) {
             const float sc = DEV && rt.n < 0 ? NAN : 1.f;  // a device alpha not finite and positive
-            store_acc(dk + kvoff + (size_t)j_key * kD, gq, adk, sc);
-            store_acc(dv + kvoff + (size_t)j_key * kD, gq, adv, sc);
+            store_acc(dk + head_at<STRIDED, kD>(lay.dk, bk, hd.kv_heads(), T) + (size_t)j_key * stdk, gq, adk, sc);
+            store_acc(dv + head_at<STRIDED, kD>(lay.dv, bk, hd.kv_heads(), T) + (size_t)j_key * stdv, gq, adv, sc);
         }
     }
 }
@@ -527,44 +534,55 @@ static hipError_t launch_dkdv(bool interp, const void *q, const void *k, const v
                               const float *lse, const void *dO, const float *delta_ws, void *dk,
                               void *dv, const double *partials, int n_partials, float *dalpha,
                               int BH, const Heads &hd, int T, int W, const RungTable &rt,
-                              const RungTable *rtp, const RopeFreq &rf, float tau, hipStream_t s) {
+                              const RungTable *rtp, const RopeFreq &rf, float tau,
+                              const Layouts &lay, hipStream_t s) {
     constexpr int keys = 64 / NH;
     const int tiles = (T + keys - 1) / keys;
     const bool one = hd.G == NH;
-    auto kern = rtp ? (one ? bwd_dkdv_bf16_d64_kernel<true, NH, true, true>
-                           : bwd_dkdv_bf16_d64_kernel<true, NH, false, true>)
-              : interp ? (one ? bwd_dkdv_bf16_d64_kernel<true, NH, true, false>
-                              : bwd_dkdv_bf16_d64_kernel<true, NH, false, false>)
-                       : (one ? bwd_dkdv_bf16_d64_kernel<false, NH, true, false>
-                              : bwd_dkdv_bf16_d64_kernel<false, NH, false, false>);
+    const bool strided = lay.q.st != kD || lay.k.st != kD || lay.v.st != kD || lay.g.st != kD ||
+                         lay.dk.st != kD || lay.dv.st != kD;
+    if (rtp && strided) return hipErrorInvalidValue;  // device tables come with packed tensors
+#define FIBATTN_DKDV(I, S)                                                                     \
+    (one ? bwd_dkdv_bf16_d64_kernel<I, NH, true, false, S> : bwd_dkdv_bf16_d64_kernel<I, NH, false, false, S>)
+    auto kern = rtp ? (one ? bwd_dkdv_bf16_d64_kernel<true, NH, true, true, false>
+                           : bwd_dkdv_bf16_d64_kernel<true, NH, false, true, false>)
+              : strided ? (interp ? FIBATTN_DKDV(true, true) : FIBATTN_DKDV(false, true))
+                        : (interp ? FIBATTN_DKDV(true, false) : FIBATTN_DKDV(false, false));
+#undef FIBATTN_DKDV
     return launch(kBwdDkDv, kern, dim3(tiles * (BH / hd.G)), dim3(256), 0, s, q, k, v, lse, dO,
-                  delta_ws, dk, dv, partials, n_partials, dalpha, T, W, rt, rtp, rf, tau, tiles, hd);
+                  delta_ws, dk, dv, partials, n_partials, dalpha, T, W, rt, rtp, rf, tau, tiles, hd,
+                  lay);
 }
 
 hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, const void *o,
                                 const float *lse, const void *dO, void *dq, void *dk, void *dv,
                                 float *dalpha, float *delta_ws, double *partials, int BH,
                                 const Heads &hd, int T, int W, const RungTable &rt,
-                                const RungTable *rtp, const RopeFreq &rf, hipStream_t s) {
+                                const RungTable *rtp, const RopeFreq &rf, const Layouts &lay,
+                                hipStream_t s) {
     const int tiles = (T + kBwdB - 1) / kBwdB;
     const float tau = 1.f / sqrtf(64.f);
     const int nb = tiles * BH;
     bool interp = rtp != nullptr;  // a device table may hold any weights
     for (int r = 0; r < rt.n && !interp; ++r) interp = rt.w[r] != 0.f;
-    auto dqk = rtp ? bwd_dq_bf16_d64_kernel<true, true>
-                   : (interp ? bwd_dq_bf16_d64_kernel<true, false> : bwd_dq_bf16_d64_kernel<false, false>);
+    const bool strided = lay.q.st != kD || lay.k.st != kD || lay.v.st != kD || lay.o.st != kD ||
+                         lay.g.st != kD || lay.dq.st != kD;
+    if (rtp && strided) return hipErrorInvalidValue;  // device tables come with packed tensors
+    auto dqk = rtp ? bwd_dq_bf16_d64_kernel<true, true, false>
+             : strided ? (interp ? bwd_dq_bf16_d64_kernel<true, false, true> : bwd_dq_bf16_d64_kernel<false, false, true>)
+                       : (interp ? bwd_dq_bf16_d64_kernel<true, false, false> : bwd_dq_bf16_d64_kernel<false, false, false>);
     hipError_t e = launch(kBwdDq, dqk, dim3(nb), dim3(256), 0, s, q, k, v, o, lse, dO, dq, delta_ws,
-                          partials, T, W, rt, rtp, rf, tau, tiles, hd);
+                          partials, T, W, rt, rtp, rf, tau, tiles, hd, lay);
     if (e != hipSuccess) return e;
     // query heads per key/value head processed side by side in a workgroup
     if (hd.G % 4 == 0)
         return launch_dkdv<4>(interp, q, k, v, lse, dO, delta_ws, dk, dv, partials, nb, dalpha, BH,
-                              hd, T, W, rt, rtp, rf, tau, s);
+                              hd, T, W, rt, rtp, rf, tau, lay, s);
     if (hd.G % 2 == 0)
         return launch_dkdv<2>(interp, q, k, v, lse, dO, delta_ws, dk, dv, partials, nb, dalpha, BH,
-                              hd, T, W, rt, rtp, rf, tau, s);
+                              hd, T, W, rt, rtp, rf, tau, lay, s);
     return launch_dkdv<1>(interp, q, k, v, lse, dO, delta_ws, dk, dv, partials, nb, dalpha, BH, hd,
-                          T, W, rt, rtp, rf, tau, s);
+                          T, W, rt, rtp, rf, tau, lay, s);
 }
 
 }  // namespace fibattn

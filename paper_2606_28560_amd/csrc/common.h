@@ -66,6 +66,31 @@ struct Heads {
     __host__ __device__ int q_of(int bk, int g) const { return (bk / (H / G)) * H + (bk % (H / G)) * G + g; }
 };
 
+// Placement of a [B, heads, T, d] tensor whose rows (the d elements of one position
+// of one head) are contiguous: element (b, h, t, c) at b*sb + h*sh + t*st + c, in
+// elements.  The packed layout is (heads*T*d, T*d, d).
+struct Layout {
+    long long sb, sh, st;
+    __host__ __device__ static Layout packed(int heads, int T, int D) {
+        return {(long long)heads * T * D, (long long)T * D, (long long)D};
+    }
+    // element offset of row 0 of the flat head index bh = b * heads + h
+    __host__ __device__ long long head(int bh, int heads) const {
+        return (long long)(bh / heads) * sb + (long long)(bh % heads) * sh;
+    }
+};
+// Element offset of row 0 of head bh: from the layout when STRIDED, else packed
+// [*, T, D] (the layout is then not read, keeping its fields out of registers).
+template <bool STRIDED, int D>
+__device__ __forceinline__ long long head_at(const Layout &l, int bh, int heads, int T) {
+    return STRIDED ? l.head(bh, heads) : (long long)bh * T * D;
+}
+// The tensors of a launch: q, k, v, o, and for the backward dO, dq, dk, dv.  k, v,
+// dk, dv have the key/value head count.
+struct Layouts {
+    Layout q, k, v, o, g, dq, dk, dv;
+};
+
 // RoPE inverse frequencies base^(-2j/D) for j < D/2 <= 32, evaluated in float64 on
 // the host; `on` = 0 when no rotation is requested.
 struct RopeFreq {

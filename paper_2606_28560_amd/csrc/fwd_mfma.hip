@@ -28,12 +28,13 @@ constexpr int kFwdBQ = 64;                 // queries per workgroup
 constexpr float kSlack = 8.f;              // log2 units a logit may exceed the running reference
 
 // INTERP: some rung has w != 0, so the second row r1 is read.  DEV: the rung table
-// is the one at rtp, built on the device (rt_arg unused).
-template <bool INTERP, bool DEV>
+// is the one at rtp, built on the device (rt_arg unused).  STRIDED: rows are placed
+// by the layouts' position strides (else every row stride is 64, a constant).
+template <bool INTERP, bool DEV, bool STRIDED>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void fwd_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     uint16_t *__restrict__ o, float *__restrict__ lse, int T, int W, RungTable rt_arg,
-    const RungTable *__restrict__ rtp, float sl2, int tiles, Heads hd) {
+    const RungTable *__restrict__ rtp, float sl2, int tiles, Heads hd, Layouts lay) {
     const RungTable &rt = DEV ? *rtp : rt_arg;
     constexpr int RB = INTERP ? 1 : 2;  // rungs per load batch; two batches in flight
     constexpr int NS = INTERP ? 2 : 1;  // rows per rung (r0, and r1 when interpolating)
@@ -50,11 +51,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     const int blk = xcd_remap(blockIdx.x, gridDim.x);
     const int bh = blk / tiles;
     const int T0 = (blk % tiles) * kFwdBQ;
-    const size_t off = (size_t)bh * T * kD;
-    const size_t kvoff = (size_t)hd.kv_of(bh) * T * kD;
-    const uint16_t *Q = q + off;
-    const uint16_t *K = k + kvoff;
-    const uint16_t *V = v + kvoff;
+    const int bk = hd.kv_of(bh);
+    const uint16_t *Q = q + head_at<STRIDED, kD>(lay.q, bh, hd.H, T);
+    const uint16_t *K = k + head_at<STRIDED, kD>(lay.k, bk, hd.kv_heads(), T);
+    const uint16_t *V = v + head_at<STRIDED, kD>(lay.v, bk, hd.kv_heads(), T);
+    // row strides
+    const int stq = STRIDED ? (int)lay.q.st : kD, stk = STRIDED ? (int)lay.k.st : kD;
+    const int stv = STRIDED ? (int)lay.v.st : kD, sto = STRIDED ? (int)lay.o.st : kD;
 
     const int t0 = T0 + 16 * wv;
     const int last = t0 + 15;  // the wave's last query
@@ -72,7 +75,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
 
     const int im = t0 + nm;  // query of this lane in the MFMA layout
     const int i = t0 + nq;   // ... in the quad layout
-    const Slice qq = load_row(Q, min(i, T - 1), gq);
+    const Slice qq = load_row(Q, min(i, T - 1), gq, stq);
 
     // rung rows of a batch: kx[x*NS + s], vx[x*NS + s] = row r_s of rung rb + x
     // (from LDS for the first nlds rungs, else from global memory; `which` selects
@@ -94,8 +97,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
 #pragma unroll
                 for (int sidx = 0; sidx < NS; ++sidx) {
                     const int R = max(R0 - sidx, 0);
-                    kx[x * NS + sidx] = load_row(K, R, gq);
-                    vx[x * NS + sidx] = load_row(V, R, gq);
+                    kx[x * NS + sidx] = load_row(K, R, gq, stk);
+                    vx[x * NS + sidx] = load_row(V, R, gq, stv);
                 }
             }
         }
@@ -104,8 +107,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     if (0 < nact) load_batch(0, kA, vA, 1);  // in flight during the band phase
     // rows [T0-kLeadF, T0+64) of K and V, straight to LDS (rows outside [0, T) are
     // clamped copies: their keys are masked below)
-    dma_rows<kBandRows>(kr, K, T0 - kLeadF, T);
-    dma_rows<kBandRows>(vr, V, T0 - kLeadF, T);
+    dma_rows<kBandRows>(kr, K, T0 - kLeadF, T, stk);
+    dma_rows<kBandRows>(vr, V, T0 - kLeadF, T, stv);
     wait_vmem();
     __syncthreads();
     if (0 < nact) load_batch(0, kA, vA, 2);
@@ -210,7 +213,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
 
     if (i < T) {
         const bool bad = DEV && rt.n < 0;  // a device alpha that is not finite and positive
-        store_acc(o + off + (size_t)i * kD, gq, acc, bad ? NAN : 1.f / l);
+        store_acc(o + head_at<STRIDED, kD>(lay.o, bh, hd.H, T) + (size_t)i * sto, gq, acc, bad ? NAN : 1.f / l);
         if (gq == 0) lse[(size_t)bh * T + i] = bad ? NAN : (m + log2f(l)) * kLn2;
     }
 }
@@ -225,13 +228,18 @@ bool forward_mfma_supported(int dtype, int D, int W) { return dtype == 1 && D ==
 
 hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void *o, float *lse,
                                int BH, const Heads &hd, int T, int W, const RungTable &rt,
-                               const RungTable *rtp, hipStream_t s) {
+                               const RungTable *rtp, const Layouts &lay, hipStream_t s) {
     const int tiles = (T + kFwdBQ - 1) / kFwdBQ;
     const float sl2 = kLog2e / sqrtf(64.f);
-    auto kern = rtp ? fwd_bf16_d64_kernel<true, true>
-                    : (any_interp(rt) ? fwd_bf16_d64_kernel<true, false> : fwd_bf16_d64_kernel<false, false>);
+    // device tables come with packed tensors only
+    const bool strided = lay.q.st != kD || lay.k.st != kD || lay.v.st != kD || lay.o.st != kD;
+    if (rtp && strided) return hipErrorInvalidValue;
+    const bool interp = any_interp(rt);
+    auto kern = rtp ? fwd_bf16_d64_kernel<true, true, false>
+              : strided ? (interp ? fwd_bf16_d64_kernel<true, false, true> : fwd_bf16_d64_kernel<false, false, true>)
+                        : (interp ? fwd_bf16_d64_kernel<true, false, false> : fwd_bf16_d64_kernel<false, false, false>);
     return launch(kForward, kern, dim3(tiles * BH), dim3(256), 0, s, q, k, v, o, lse, T, W, rt, rtp,
-                  sl2, tiles, hd);
+                  sl2, tiles, hd, lay);
 }
 
 }  // namespace fibattn

@@ -35,7 +35,7 @@ hipError_t launch(int id, void (*kernel)(P...), dim3 grid, dim3 block, unsigned 
 // the rung table is the device-resident one at rtp (rt unused).
 hipError_t launch_forward(int dtype, int D, const void *q, const void *k, const void *v, void *o,
                           float *lse, int BH, const Heads &hd, int T, int W, const RungTable &rt,
-                          const RungTable *rtp, hipStream_t s);
+                          const RungTable *rtp, const Layouts &lay, hipStream_t s);
 
 // Number of dalpha partials the dq kernel writes (one per workgroup).
 size_t bwd_num_partials(int dtype, int D, int BH, int T);
@@ -44,20 +44,22 @@ hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const
                            const void *o, const float *lse, const void *dO, void *dq, void *dk,
                            void *dv, float *dalpha, float *delta_ws, double *partials, int BH,
                            const Heads &hd, int T, int W, const RungTable &rt,
-                           const RungTable *rtp, const RopeFreq &rf, float rope_base, hipStream_t s);
+                           const RungTable *rtp, const RopeFreq &rf, float rope_base,
+                           const Layouts &lay, hipStream_t s);
 
 // bfloat16, d_head = 64, W <= 16: matrix-core band + VALU rungs (fwd_mfma.hip, bwd_mfma.hip).
 bool forward_mfma_supported(int dtype, int D, int W);
 hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void *o, float *lse,
                                int BH, const Heads &hd, int T, int W, const RungTable &rt,
-                               const RungTable *rtp, hipStream_t s);
+                               const RungTable *rtp, const Layouts &lay, hipStream_t s);
 bool backward_mfma_supported(int dtype, int D, int W);
 size_t bwd_mfma_num_partials(int BH, int T);
 hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, const void *o,
                                 const float *lse, const void *dO, void *dq, void *dk, void *dv,
                                 float *dalpha, float *delta_ws, double *partials, int BH,
                                 const Heads &hd, int T, int W, const RungTable &rt,
-                                const RungTable *rtp, const RopeFreq &rf, hipStream_t s);
+                                const RungTable *rtp, const RopeFreq &rf, const Layouts &lay,
+                                hipStream_t s);
 
 RopeFreq make_rope_freq(double rope_base, int D);  // on = 0 when rope_base <= 0
 
@@ -68,8 +70,10 @@ hipError_t launch_rung_table(const float *alpha, const BaseTable &b, int W, Rung
 hipError_t launch_alpha_from_theta(const float *theta, float *alpha, int n, hipStream_t s);
 hipError_t launch_dtheta(const float *theta, const float *dalpha, float *dtheta, int n, hipStream_t s);
 
-// RoPE of one tensor (x1 == nullptr) or of two same-shaped tensors in one launch.
-hipError_t launch_rope(int dtype, int D, const void *x0, void *y0, const void *x1, void *y1, int BH,
+// RoPE of one tensor (x1 == nullptr) or of two same-shaped tensors in one launch:
+// BH = batch * heads rows; inputs and outputs placed by their layouts.
+hipError_t launch_rope(int dtype, int D, const void *x0, void *y0, const Layout &lx0, const Layout &ly0,
+                       const void *x1, void *y1, const Layout &lx1, const Layout &ly1, int BH, int heads,
                        int T, float rope_base, int transpose, hipStream_t s);
 
 }  // namespace fibattn

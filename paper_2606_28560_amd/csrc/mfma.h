@@ -41,10 +41,11 @@ __device__ __forceinline__ Slice load_slice(const uint16_t *row, int g) {
     return s;
 }
 
-// Slice g of row `row` of a [*, 64] bf16 matrix at a uniform base address: a 32-bit
-// byte offset from the base lets the loads use scalar-base addressing.
-__device__ __forceinline__ Slice load_row(const uint16_t *base, int row, int g) {
-    const uint32_t off = (uint32_t)row * 128u + (uint32_t)g * 16u;
+// Slice g of row `row` of rows `st` elements apart (64 contiguous bf16 each) at a
+// uniform base address: a 32-bit byte offset from the base lets the loads use
+// scalar-base addressing (the host keeps every row offset below 2^31 bytes).
+__device__ __forceinline__ Slice load_row(const uint16_t *base, int row, int g, int st) {
+    const uint32_t off = (uint32_t)row * (uint32_t)(2 * st) + (uint32_t)g * 16u;
     const char *p = reinterpret_cast<const char *>(base);
     Slice s;
     s.a = *reinterpret_cast<const uint4 *>(p + off);
@@ -223,14 +224,15 @@ __device__ __forceinline__ int out_dim(int c, int m) {
     return (c < 2 ? 0 : 32) + 8 * (m >> 2) + 4 * (c & 1) + (m & 3);
 }
 
-// Rows [r_begin, r_begin + NROWS) of a [*, 64] bf16 matrix copied to LDS with
-// direct-to-LDS loads (no registers; completion counts in vmcnt): row-major, 128-byte
+// Rows [r_begin, r_begin + NROWS) of rows `st` elements apart (64 contiguous bf16
+// each) copied to LDS with direct-to-LDS loads (no registers; completion counts in
+// vmcnt): row-major, 128-byte
 // rows whose 16-byte chunks are XOR-swizzled by the row (chunk c of band row r sits in
 // slot c ^ (r & 7)), so that lanes reading one chunk of consecutive rows spread over
 // the banks.  Rows outside [0, T) are clamped to a valid row: callers mask them.
 // Each wave moves 1 KB (8 rows) per instruction.  256 threads.
 template <int NROWS>
-__device__ __forceinline__ void dma_rows(uint16_t *dst, const uint16_t *X, int r_begin, int T) {
+__device__ __forceinline__ void dma_rows(uint16_t *dst, const uint16_t *X, int r_begin, int T, int st) {
     static_assert(NROWS % 8 == 0, "whole 1 KB blocks");
     const int lane = threadIdx.x & 63;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -239,7 +241,7 @@ __device__ __forceinline__ void dma_rows(uint16_t *dst, const uint16_t *X, int r
         const int rr = 8 * blk + (lane >> 3);
         const int ch = (lane & 7) ^ (rr & 7);
         const int row = min(max(r_begin + rr, 0), T - 1);
-        __builtin_amdgcn_global_load_lds(X + (size_t)row * kD + 8 * ch, dst + 512 * blk, 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(X + (size_t)row * st + 8 * ch, dst + 512 * blk, 16, 0, 0);
     }
 }
 // Chunk c (dims 8c..8c+7) of band row rr staged by dma_rows.

@@ -24,9 +24,10 @@ template <> __device__ __forceinline__ void st1<uint16_t>(uint16_t *p, float x) 
 }
 
 // Generic kernel (any storage type and head size): one element pair per thread.
+// BH = batch * heads rows of positions [0, T); x and y placed by lx and ly.
 template <typename S, int D>
 __global__ __launch_bounds__(256) void rope_kernel(const S *x, S *y, int BH, int T, double rope_base,
-                                                   int transpose) {
+                                                   int transpose, int heads, Layout lx, Layout ly) {
     constexpr int HALF = D / 2;
     __shared__ float cs[kRopeTP * HALF], sn[kRopeTP * HALF];
     const int t0 = blockIdx.x * kRopeTP;
@@ -49,12 +50,13 @@ __global__ __launch_bounds__(256) void rope_kernel(const S *x, S *y, int BH, int
         const int t = t0 + tt;
         const int bh = bh0 + rr;
         if (t >= T || bh >= BH) continue;
-        const size_t row = ((size_t)bh * T + t) * D;
+        const S *xr = x + lx.head(bh, heads) + (long long)t * lx.st;
+        S *yr = y + ly.head(bh, heads) + (long long)t * ly.st;
         const float c = cs[tt * HALF + jj], s = sn[tt * HALF + jj];
-        const float u = ld1<S>(x + row + jj);
-        const float w = ld1<S>(x + row + jj + HALF);
-        st1<S>(y + row + jj, u * c - w * s);
-        st1<S>(y + row + jj + HALF, w * c + u * s);
+        const float u = ld1<S>(xr + jj);
+        const float w = ld1<S>(xr + jj + HALF);
+        st1<S>(yr + jj, u * c - w * s);
+        st1<S>(yr + jj + HALF, w * c + u * s);
     }
 }
 
@@ -66,13 +68,20 @@ __global__ __launch_bounds__(256) void rope_kernel(const S *x, S *y, int BH, int
 constexpr int kRope64TP = 4;
 constexpr int kRope64RB = 16;
 
-// blockIdx.z selects the tensor: (x0 -> y0) or (x1 -> y1).
+// blockIdx.z selects the tensor: (x0 -> y0) or (x1 -> y1), each placed by its io
+// (STRIDED; else every tensor is packed [BH, T, 64]).
+struct RopeIO {
+    Layout x, y;
+};
+template <bool STRIDED>
 __global__ __launch_bounds__(256) void rope_bf16_d64_kernel(const uint16_t *x0, uint16_t *y0,
                                                             const uint16_t *x1, uint16_t *y1, int BH,
-                                                            int T, RopeFreq rf, int transpose) {
+                                                            int T, RopeFreq rf, int transpose,
+                                                            int heads, RopeIO io0, RopeIO io1) {
     __shared__ float cs[kRope64TP * 32], sn[kRope64TP * 32];
     const uint16_t *x = blockIdx.z ? x1 : x0;
     uint16_t *y = blockIdx.z ? y1 : y0;
+    const RopeIO &io = blockIdx.z ? io1 : io0;
     const int t0 = blockIdx.x * kRope64TP;
     const int g = threadIdx.x & 3;
     const int rr = threadIdx.x >> 2;  // 0..63
@@ -80,9 +89,12 @@ __global__ __launch_bounds__(256) void rope_bf16_d64_kernel(const uint16_t *x0, 
     const int t = t0 + tt;
     const int bh = blockIdx.y * kRope64RB + (rr >> 2);
     const bool live = t < T && bh < BH;
-    const size_t row = ((size_t)min(bh, BH - 1) * T + min(t, T - 1)) * 64;
-    const uint4 a = *reinterpret_cast<const uint4 *>(x + row + 8 * g);
-    const uint4 b = *reinterpret_cast<const uint4 *>(x + row + 32 + 8 * g);
+    const int bhc = min(bh, BH - 1), tc = min(t, T - 1);
+    const size_t packed = ((size_t)bhc * T + tc) * 64;
+    const uint16_t *xr = x + (STRIDED ? io.x.head(bhc, heads) + (long long)tc * io.x.st : packed);
+    uint16_t *yr = y + (STRIDED ? io.y.head(bhc, heads) + (long long)tc * io.y.st : packed);
+    const uint4 a = *reinterpret_cast<const uint4 *>(xr + 8 * g);
+    const uint4 b = *reinterpret_cast<const uint4 *>(xr + 32 + 8 * g);
     if (threadIdx.x < kRope64TP * 32) {
         float c, sv;
         rope_cs(t0 + (threadIdx.x >> 5), rf.inv[threadIdx.x & 31], c, sv);
@@ -103,8 +115,8 @@ __global__ __launch_bounds__(256) void rope_bf16_d64_kernel(const uint16_t *x0, 
         ow[w] = f32_to_bf16(u0 * c0 - v0 * s0) | (f32_to_bf16(u1 * c1 - v1 * s1) << 16);
         pw[w] = f32_to_bf16(v0 * c0 + u0 * s0) | (f32_to_bf16(v1 * c1 + u1 * s1) << 16);
     }
-    *reinterpret_cast<uint4 *>(y + row + 8 * g) = make_uint4(ow[0], ow[1], ow[2], ow[3]);
-    *reinterpret_cast<uint4 *>(y + row + 32 + 8 * g) = make_uint4(pw[0], pw[1], pw[2], pw[3]);
+    *reinterpret_cast<uint4 *>(yr + 8 * g) = make_uint4(ow[0], ow[1], ow[2], ow[3]);
+    *reinterpret_cast<uint4 *>(yr + 32 + 8 * g) = make_uint4(pw[0], pw[1], pw[2], pw[3]);
 }
 
 RopeFreq make_rope_freq(double rope_base, int D) {
@@ -115,39 +127,42 @@ RopeFreq make_rope_freq(double rope_base, int D) {
 }
 
 static hipError_t launch_rope_generic(int dtype, int D, const void *x, void *y, int BH, int T,
-                                      double lb, int transpose, hipStream_t s) {
+                                      double lb, int transpose, int heads, const Layout &lx,
+                                      const Layout &ly, hipStream_t s) {
     dim3 grid((T + kRopeTP - 1) / kRopeTP, (BH + kRopeRB - 1) / kRopeRB);
-    if (dtype == 0 && D == 32)
-        return launch(kRope, rope_kernel<float, 32>, grid, dim3(256), 0, s, x, y, BH, T, lb, transpose);
-    if (dtype == 0 && D == 64)
-        return launch(kRope, rope_kernel<float, 64>, grid, dim3(256), 0, s, x, y, BH, T, lb, transpose);
-    if (dtype == 1 && D == 32)
-        return launch(kRope, rope_kernel<uint16_t, 32>, grid, dim3(256), 0, s, x, y, BH, T, lb,
-                      transpose);
-    if (dtype == 1 && D == 64)
-        return launch(kRope, rope_kernel<uint16_t, 64>, grid, dim3(256), 0, s, x, y, BH, T, lb,
-                      transpose);
-    if (dtype == 0 && D == 128)
-        return launch(kRope, rope_kernel<float, 128>, grid, dim3(256), 0, s, x, y, BH, T, lb, transpose);
-    if (dtype == 1 && D == 128)
-        return launch(kRope, rope_kernel<uint16_t, 128>, grid, dim3(256), 0, s, x, y, BH, T, lb,
-                      transpose);
+#define FIBATTN_ROPE(S, DD)                                                                          \
+    if ((dtype == 0) == (sizeof(S) == 4) && D == DD)                                                  \
+        return launch(kRope, rope_kernel<S, DD>, grid, dim3(256), 0, s, x, y, BH, T, lb, transpose, \
+                      heads, lx, ly);
+    FIBATTN_ROPE(float, 32)
+    FIBATTN_ROPE(float, 64)
+    FIBATTN_ROPE(float, 128)
+    FIBATTN_ROPE(uint16_t, 32)
+    FIBATTN_ROPE(uint16_t, 64)
+    FIBATTN_ROPE(uint16_t, 128)
+#undef FIBATTN_ROPE
     return hipErrorInvalidValue;
 }
 
-// One launch for one tensor (x1 == nullptr) or two tensors of the same shape.
-hipError_t launch_rope(int dtype, int D, const void *x0, void *y0, const void *x1, void *y1, int BH,
+// One launch for one tensor (x1 == nullptr) or two tensors of the same shape; BH =
+// batch * heads rows; each input and output placed by its layout.
+hipError_t launch_rope(int dtype, int D, const void *x0, void *y0, const Layout &lx0, const Layout &ly0,
+                       const void *x1, void *y1, const Layout &lx1, const Layout &ly1, int BH, int heads,
                        int T, float rope_base, int transpose, hipStream_t s) {
     const double lb = (double)rope_base;
     if (dtype == 1 && D == 64) {
         const RopeFreq rf = make_rope_freq(lb, 64);
-        return launch(kRope, rope_bf16_d64_kernel,
+        const Layout p = Layout::packed(heads, T, 64);
+        auto same = [&](const Layout &l) { return l.sb == p.sb && l.sh == p.sh && l.st == p.st; };
+        const bool strided = !same(lx0) || !same(ly0) || (x1 && (!same(lx1) || !same(ly1)));
+        return launch(kRope, strided ? rope_bf16_d64_kernel<true> : rope_bf16_d64_kernel<false>,
                       dim3((T + kRope64TP - 1) / kRope64TP, (BH + kRope64RB - 1) / kRope64RB,
                            x1 ? 2 : 1),
-                      dim3(256), 0, s, x0, y0, x1, y1, BH, T, rf, transpose);
+                      dim3(256), 0, s, x0, y0, x1, y1, BH, T, rf, transpose, heads, RopeIO{lx0, ly0},
+                      RopeIO{lx1, ly1});
     }
-    hipError_t e = launch_rope_generic(dtype, D, x0, y0, BH, T, lb, transpose, s);
-    if (e == hipSuccess && x1) e = launch_rope_generic(dtype, D, x1, y1, BH, T, lb, transpose, s);
+    hipError_t e = launch_rope_generic(dtype, D, x0, y0, BH, T, lb, transpose, heads, lx0, ly0, s);
+    if (e == hipSuccess && x1) e = launch_rope_generic(dtype, D, x1, y1, BH, T, lb, transpose, heads, lx1, ly1, s);
     return e;
 }
 

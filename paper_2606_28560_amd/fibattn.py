@@ -22,6 +22,7 @@ MAX_WINDOW = 128
 KERNEL_IDS = {"rope": 0, "forward": 1, "bwd_dq": 2, "bwd_dkdv": 3, "dalpha_reduce": 4, "alpha": 5}
 EXPORTED = ("fibattn_rung_table", "fibattn_forward", "fibattn_backward_workspace_bytes",
             "fibattn_backward", "fibattn_forward_gqa", "fibattn_backward_gqa",
+            "fibattn_forward_strided", "fibattn_backward_strided",
             "fibattn_device_table_bytes", "fibattn_device_table", "fibattn_forward_dt",
             "fibattn_backward_dt", "fibattn_alpha_from_theta", "fibattn_dtheta", "fibattn_rope",
             "fibattn_rope_qk", "fibattn_status_string", "fibattn_timing_begin", "fibattn_timing_end")
@@ -62,6 +63,11 @@ def lib():
     L.fibattn_backward_gqa.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                        i, i, i, i, i, i, ip, i, f, f, i, vp]
     L.fibattn_backward_gqa.restype = i
+    L.fibattn_forward_strided.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, ip, i, f, i, vp]
+    L.fibattn_forward_strided.restype = i
+    L.fibattn_backward_strided.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp,
+                                           i, i, i, i, i, i, ip, i, f, f, i, vp]
+    L.fibattn_backward_strided.restype = i
     L.fibattn_device_table_bytes.argtypes = []
     L.fibattn_device_table_bytes.restype = sz
     L.fibattn_device_table.argtypes = [vp, ip, i, i, vp, vp]
@@ -120,10 +126,14 @@ def _stream(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def _check_tensor(name, t, shape, dtype):
+def _check_tensor(name, t, shape, dtype, strided=False):
+    """strided: any placement whose rows (last dimension) are contiguous."""
     if not t.is_cuda:
         raise ValueError(f"{name} must be a GPU tensor")
-    if not t.is_contiguous():
+    if strided:
+        if t.dim() != 4 or (t.shape[3] > 1 and t.stride(3) != 1):
+            raise ValueError(f"{name} must have contiguous rows (last-dimension stride 1)")
+    elif not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if tuple(t.shape) != tuple(shape):
         raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
@@ -152,27 +162,40 @@ def _kv_heads(q, k):
     return k.shape[1]
 
 
+def _layouts(*ts):
+    """fibattn_layout_t array of the tensors' (batch, head, position) element strides."""
+    arr = (ctypes.c_int64 * (3 * len(ts)))()
+    for a, t in enumerate(ts):
+        arr[3 * a], arr[3 * a + 1], arr[3 * a + 2] = t.stride(0), t.stride(1), t.stride(2)
+    return arr
+
+
 def fibattn_forward(q, k, v, W: int, base, alpha: float, *, o=None, lse=None, stream=None):
     """o, lse = forward of post-RoPE q, k and v (float32 or bfloat16).
 
-    q: [B,H,T,D]; k, v: [B,H_kv,T,D] with H_kv dividing H (H_kv < H: grouped heads)."""
+    q: [B,H,T,D]; k, v: [B,H_kv,T,D] with H_kv dividing H (H_kv < H: grouped heads).
+    q, k, v, o may be any views with contiguous rows (e.g. slices of a [B,T,3,H,D]
+    projection output, transposed); lse is packed [B,H,T]."""
     import torch
 
     B, H, T, D = q.shape
     Hkv = _kv_heads(q, k)
-    _check_tensor("q", q, q.shape, q.dtype)
+    _check_tensor("q", q, q.shape, q.dtype, strided=True)
     for n_, t in (("k", k), ("v", v)):
-        _check_tensor(n_, t, (B, Hkv, T, D), q.dtype)
+        _check_tensor(n_, t, (B, Hkv, T, D), q.dtype, strided=True)
     if o is None:
-        o = torch.empty_like(q)
+        o = torch.empty((B, H, T, D), device=q.device, dtype=q.dtype)
     if lse is None:
         lse = torch.empty((B, H, T), device=q.device, dtype=torch.float32)
-    _check_tensor("o", o, q.shape, q.dtype)
+    _check_tensor("o", o, q.shape, q.dtype, strided=True)
     _check_tensor("lse", lse, (B, H, T), torch.float32)
     b, bp = _base_array(base)
     ptrs = (q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr())
     tail = (T, D, int(W), bp, b.size, ctypes.c_float(alpha), _dtype_code(q), _stream(stream))
-    if Hkv == H:
+    if not all(t.is_contiguous() for t in (q, k, v, o)):
+        st = lib().fibattn_forward_strided(*ptrs, _layouts(q, k, v, o), B, H, Hkv, *tail)
+        _check("fibattn_forward_strided", st)
+    elif Hkv == H:
         st = lib().fibattn_forward(*ptrs, B, H, *tail)
         _check("fibattn_forward", st)
     else:
@@ -191,7 +214,7 @@ def fibattn_backward(q, k, v, o, lse, dO, W: int, base, alpha: float, *, dq=None
 
     k, v (and dk, dv) may have fewer heads than q (grouped heads; dk, dv then sum over
     each group).  rope_base > 0: dq, dk are returned w.r.t. the unrotated q, k (R^T
-    applied)."""
+    applied).  Every [B,*,T,D] tensor may be a view with contiguous rows; lse is packed."""
     import torch
 
     B, H, T, D = q.shape
@@ -199,13 +222,14 @@ def fibattn_backward(q, k, v, o, lse, dO, W: int, base, alpha: float, *, dq=None
     kvs = (B, Hkv, T, D)
     for n_, t, sh in (("q", q, q.shape), ("k", k, kvs), ("v", v, kvs), ("o", o, q.shape),
                       ("dO", dO, q.shape)):
-        _check_tensor(n_, t, sh, q.dtype)
+        _check_tensor(n_, t, sh, q.dtype, strided=True)
     _check_tensor("lse", lse, (B, H, T), torch.float32)
-    dq = torch.empty_like(q) if dq is None else dq
-    dk = torch.empty_like(k) if dk is None else dk
-    dv = torch.empty_like(v) if dv is None else dv
+    mk = lambda sh: torch.empty(sh, device=q.device, dtype=q.dtype)  # noqa: E731
+    dq = mk(tuple(q.shape)) if dq is None else dq
+    dk = mk(kvs) if dk is None else dk
+    dv = mk(kvs) if dv is None else dv
     for n_, t, sh in (("dq", dq, q.shape), ("dk", dk, kvs), ("dv", dv, kvs)):
-        _check_tensor(n_, t, sh, q.dtype)
+        _check_tensor(n_, t, sh, q.dtype, strided=True)
     if dalpha is None:
         dalpha = torch.empty(1, device=q.device, dtype=torch.float32)
     b, bp = _base_array(base)
@@ -217,7 +241,10 @@ def fibattn_backward(q, k, v, o, lse, dO, W: int, base, alpha: float, *, dq=None
             workspace.numel())
     tail = (T, D, int(W), bp, b.size, ctypes.c_float(alpha), ctypes.c_float(rope_base),
             _dtype_code(q), _stream(stream))
-    if Hkv == H:
+    if not all(t.is_contiguous() for t in (q, k, v, o, dO, dq, dk, dv)):
+        st = lib().fibattn_backward_strided(*ptrs, _layouts(q, k, v, o, dO, dq, dk, dv), B, H, Hkv, *tail)
+        _check("fibattn_backward_strided", st)
+    elif Hkv == H:
         st = lib().fibattn_backward(*ptrs, B, H, *tail)
         _check("fibattn_backward", st)
     else:

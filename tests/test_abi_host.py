@@ -137,3 +137,36 @@ def test_invalid_arguments_return_codes_without_gpu():
     assert L.fibattn_dtheta(16, None, 16, 4, None) == 1
     for s in range(5):
         assert F.status_string(s)
+
+
+def test_strided_layouts_are_checked_before_any_launch():
+    """Bad layouts return a status on the host.  Every call here fails validation
+    before any launch (the pointers are dummies)."""
+    L = F.lib()
+    b = (ctypes.c_int32 * 15)(*schedules.FIB15)
+    one, zero = ctypes.c_float(1.0), ctypes.c_float(0.0)
+
+    def lay(*rows):
+        arr = (ctypes.c_int64 * (3 * len(rows)))()
+        for a, r in enumerate(rows):
+            arr[3 * a:3 * a + 3] = r
+        return arr
+
+    good = (8 * 8 * 64, 8 * 64, 64)  # packed [B, 8, 8, 64]
+
+    def fwd(ls, T=8):
+        return L.fibattn_forward_strided(16, 16, 16, 16, 16, ls, 1, 8, 8, T, 64, 8, b, 15, one, 1, None)
+
+    assert fwd(None) == 1
+    assert fwd(lay(good, good, good, (-64, 64, 64))) == 1                # negative stride
+    assert fwd(lay(good, (8 * 8 * 64, 8 * 64, 60), good, good)) == 1     # rows not 16-byte aligned
+    assert fwd(lay(good, good, (8 * 8 * 64 + 4, 8 * 64, 64), good)) == 1  # batch stride misaligned
+    assert fwd(lay(good, good, (0, 0, 1 << 26), good), T=64) == 2        # row offsets >= 2^31 bytes
+
+    def bwd(ls):
+        return L.fibattn_backward_strided(16, 16, 16, 16, 16, 16, 16, 16, 16, 16, 16, 1 << 30, ls,
+                                          1, 8, 8, 8, 64, 8, b, 15, one, zero, 1, None)
+
+    assert bwd(None) == 1
+    assert bwd(lay(*([good] * 7 + [(0, 0, 12)]))) == 1                   # dv rows misaligned
+    assert bwd(lay(*([good] * 5 + [(0, -8, 64)] + [good] * 2))) == 1     # dq head stride negative

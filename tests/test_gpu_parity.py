@@ -286,3 +286,55 @@ def test_deterministic_and_stream_independent():
     for name in a:
         assert np.array_equal(a[name], b[name]), name
         assert np.array_equal(a[name], c[name]), name
+
+
+# ---- general strides: q, k, v, o, dO, dq, dk, dv as views with contiguous rows ----
+
+def _placed(x, how, slot=0):
+    """A device view of x ([B,H,T,D], CPU) with the same values in placement `how`:
+    "bthd" = a transposed [B,T,H,D] buffer; "qkv" = one slot of a [B,T,3,H,D] buffer
+    (a fused projection output); "packed" = contiguous."""
+    B, H, T, D = x.shape
+    if how == "packed":
+        return x.cuda().contiguous()
+    if how == "bthd":
+        buf = torch.empty((B, T, H, D), dtype=x.dtype, device="cuda")
+        buf.copy_(x.transpose(1, 2))
+        return buf.transpose(1, 2)
+    buf = torch.full((B, T, 3, H, D), float("nan"), dtype=x.dtype, device="cuda")
+    buf[:, :, slot].copy_(x.transpose(1, 2))
+    return buf[:, :, slot].transpose(1, 2)
+
+
+STRIDED = [
+    # (B, H, Hkv, T, D, dtype, W, alpha, placement of inputs, placement of outputs)
+    (2, 4, 4, 300, 64, "bf16", 8, 1.0, "bthd", "packed"),     # matrix-core kernels, integer
+    (2, 4, 4, 300, 64, "bf16", 8, 0.85, "qkv", "bthd"),       # interpolating, fused-qkv inputs
+    (1, 8, 2, 257, 64, "bf16", 8, 1.0, "bthd", "bthd"),       # grouped heads
+    (2, 3, 3, 200, 32, "fp32", 6, 0.7310586, "qkv", "bthd"),  # generic kernels
+    (1, 4, 2, 130, 128, "bf16", 10, 1.2, "bthd", "qkv"),      # d_head 128, outputs in a qkv buffer
+]
+
+
+@pytest.mark.parametrize("B,H,Hkv,T,D,dtype,W,alpha,pin,pout", STRIDED)
+@pytest.mark.parametrize("rope_base", [0.0, 10000.0])
+def test_strided_layouts(B, H, Hkv, T, D, dtype, W, alpha, pin, pout, rope_base):
+    x = _gqa_inputs(B, H, Hkv, T, D, dtype, 61 + D)
+    q, k, v, dO = (_placed(x[n], pin, s) for n, s in (("q", 0), ("k", 1), ("v", 2), ("dO", 0)))
+    o = _placed(torch.zeros((B, H, T, D), dtype=x["q"].dtype), pout, 0)
+    dq = _placed(torch.zeros((B, H, T, D), dtype=x["q"].dtype), pout, 0)
+    dk = _placed(torch.zeros((B, Hkv, T, D), dtype=x["q"].dtype), pout, 1)
+    dv = _placed(torch.zeros((B, Hkv, T, D), dtype=x["q"].dtype), pout, 2)
+    assert not (q.is_contiguous() and o.is_contiguous())
+    _, lse = F.fibattn_forward(q, k, v, W, FIB, alpha, o=o)
+    _, _, _, da = F.fibattn_backward(q, k, v, o, lse, dO, W, FIB, alpha, dq=dq, dk=dk, dv=dv,
+                                     rope_base=rope_base)
+    torch.cuda.synchronize()
+    ref = oracle_run(x["q"], x["k"], x["v"], x["dO"], W, FIB, alpha)
+    if rope_base:
+        ref["dq"] = oracle.rope(ref["dq"], rope_base, transpose=True)
+        ref["dk"] = oracle.rope(ref["dk"], rope_base, transpose=True)
+    got = {n_: t.double().cpu().numpy() for n_, t in (("o", o), ("lse", lse), ("dq", dq), ("dk", dk),
+                                                       ("dv", dv))}
+    got["dalpha"] = float(da.item())
+    compare(got, ref, dtype, f"strided {pin}->{pout} B{B} H{H}/{Hkv} T{T} D{D} {dtype}")
