@@ -58,15 +58,15 @@ def parse_args():
 #            --no-learned-alpha --no-integer-offsets --copy-probe-mb 256
 # each scaled by what the same counter reads for the plain 256 MiB device copy of that run.
 # They hold only for the kernel sources they were taken on (COUNTER_SOURCES_SHA).
-COUNTER_SOURCES_SHA = "a60f9c5d453cbe32909066ca0cf0150f6d6126275983044e9aae9278002cf9a8"
+COUNTER_SOURCES_SHA = "38e8c9c852332d25a0da04fe31a34e3b973c93a290661bc635f806fa34c75275"
 COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
 COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
-    "forward": (12402.1, 8448.0),
-    "bwd_dq": (20772.7, 8480.0),
-    "bwd_dkdv": (17778.6, 16384.0),
-    "rope": (8220.2, 16384.0),
+    "forward": (12403.1, 8448.0),
+    "bwd_dq": (20779.8, 8480.0),
+    "bwd_dkdv": (17811.2, 16384.0),
+    "rope": (8220.3, 16384.0),
 }
-COPY_PROBE_KIB = (262144.0, 131093.1, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
+COPY_PROBE_KIB = (262144.0, 131093.8, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
 
 
 def kernel_sources_sha() -> str:

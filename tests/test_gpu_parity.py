@@ -338,3 +338,8 @@ def test_strided_layouts(B, H, Hkv, T, D, dtype, W, alpha, pin, pout, rope_base)
                                                        ("dv", dv))}
     got["dalpha"] = float(da.item())
     compare(got, ref, dtype, f"strided {pin}->{pout} B{B} H{H}/{Hkv} T{T} D{D} {dtype}")
+    if pout == "qkv":
+        # the outputs wrote only their own slot: the NaN fill of the other two survives
+        for t, slot in ((o, 0), (dq, 0), (dk, 1), (dv, 2)):
+            others = [s_ for s_ in range(3) if s_ != slot]
+            assert torch.isnan(t._base[:, :, others].float()).all().item()
