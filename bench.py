@@ -331,6 +331,9 @@ def learned_alpha_figure(steps: int, warmup: int, eager: bool, layer: int = 0):
         st.theta, st.alpha = theta, torch.empty_like(theta)
         st.table = torch.empty(F.lib().fibattn_device_table_bytes(), device="cuda", dtype=torch.uint8)
         st.dtheta = torch.empty_like(theta)
+        # a device table's rung count is not known on the host: the workspace for K = 0
+        st.ws = torch.empty(F.fibattn_backward_workspace_bytes(wl.B, wl.H, wl.T, wl.D, call.W, 0),
+                            device="cuda", dtype=torch.uint8)
 
         def run_dev(st=st):
             c = st.call

@@ -94,7 +94,10 @@ fibattn_status_t fibattn_forward(const void *q, const void *k, const void *v,
                                  const int32_t *base, int K, float alpha,
                                  fibattn_dtype_t dtype, hipStream_t stream);
 
-/* Bytes of device workspace fibattn_backward needs for these sizes (0 for bad sizes). */
+/* Bytes of device workspace fibattn_backward needs for these sizes (0 for bad sizes):
+ * Delta (float32 [B,H,T]), the float64 dalpha partials and, when d_head = 64 and
+ * W <= 16, one 4-byte term per query and rung (K of them; pass K = 0 for a device
+ * table, whose rung count can be up to 32).  Its contents on entry are ignored. */
 size_t fibattn_backward_workspace_bytes(int B, int H, int T, int d_head, int W, int K);
 
 /*
@@ -190,7 +193,8 @@ fibattn_status_t fibattn_backward_strided(const void *q, const void *k, const vo
  * fibattn_device_table_bytes() bytes, 16-byte aligned.  The table is read by
  * fibattn_forward_dt / fibattn_backward_dt, which take it in place of (base, K, alpha)
  * and otherwise behave as fibattn_forward_gqa / fibattn_backward_gqa; W must be the
- * one the table was built with.  A table may hold any weights, so these calls always
+ * one the table was built with, and the backward's workspace is
+ * fibattn_backward_workspace_bytes(B, H, T, d_head, W, 0).  A table may hold any weights, so these calls always
  * run the interpolating kernels.  An alpha that is not finite and positive yields a
  * table that makes every output (o, lse, dq, dk, dv, dalpha) NaN.
  *

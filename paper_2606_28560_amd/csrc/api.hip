@@ -152,16 +152,33 @@ fibattn_status_t fibattn_forward(const void *q, const void *k, const void *v, vo
     return fibattn_forward_gqa(q, k, v, o, lse, B, H, H, T, d_head, W, base, K, alpha, dtype, stream);
 }
 
-size_t fibattn_backward_workspace_bytes(int B, int H, int T, int d_head, int W, int K) {
-    if (check_common(B, H, T, d_head, W, K, FIBATTN_FP32) != FIBATTN_OK) return 0;
-    // Delta (float32 [B,H,T]) then the per-workgroup dalpha partials (float64);
-    // sized for the larger of the two dtypes' partial counts.
+// Backward workspace: Delta (float32 [B,H,T]), then the per-workgroup dalpha partials
+// (float64; sized for the larger of the two dtypes' partial counts), then, for shapes
+// the matrix-core path may take (d_head 64, W <= 16), its per-(query, rung) terms:
+// one bfloat16 pair per query and plane, K planes (kMaxRungs for a device-resident table,
+// whose rung count the host does not know, passed as K = 0).
+struct WorkspaceLayout {
+    size_t partials, terms, total;
+    int planes;
+};
+
+static WorkspaceLayout workspace_layout(int B, int H, int T, int d_head, int W, int K) {
     size_t np = bwd_num_partials(0, d_head, B * H, T);
     size_t np1 = bwd_num_partials(1, d_head, B * H, T);
     size_t np2 = bwd_mfma_num_partials(B * H, T);
     if (np1 > np) np = np1;
     if (np2 > np) np = np2;
-    return align256(sizeof(float) * (size_t)B * H * T) + align256(sizeof(double) * np);
+    WorkspaceLayout l;
+    l.partials = align256(sizeof(float) * (size_t)B * H * T);
+    l.terms = l.partials + align256(sizeof(double) * np);
+    l.planes = backward_mfma_supported(1, d_head, W) ? (K > 0 ? K : kMaxRungs) : 0;
+    l.total = l.terms + align256(sizeof(uint32_t) * (size_t)l.planes * B * H * T);
+    return l;
+}
+
+size_t fibattn_backward_workspace_bytes(int B, int H, int T, int d_head, int W, int K) {
+    if (check_common(B, H, T, d_head, W, K, FIBATTN_FP32) != FIBATTN_OK) return 0;
+    return workspace_layout(B, H, T, d_head, W, K).total;
 }
 
 static fibattn_status_t backward_impl(const void *q, const void *k, const void *v, const void *o,
@@ -186,13 +203,15 @@ static fibattn_status_t backward_impl(const void *q, const void *k, const void *
     RungTable rt;
     st = build_table(alpha, base, K, W, &rt);
     if (st != FIBATTN_OK) return st;
+    const WorkspaceLayout wl = workspace_layout(B, H, T, d_head, W, K);
     float *delta_ws = (float *)workspace;
-    double *partials = (double *)((char *)workspace + align256(sizeof(float) * (size_t)B * H * T));
+    double *partials = (double *)((char *)workspace + wl.partials);
+    const RungTerms terms{(uint32_t *)((char *)workspace + wl.terms), wl.planes};
     const RopeFreq rf = make_rope_freq((double)rope_base, d_head);
     const Heads hd{H, H / H_kv};
     hipError_t e = launch_backward((int)dtype, d_head, q, k, v, o, lse, dO, dq, dk, dv, dalpha,
-                                   delta_ws, partials, B * H, hd, T, W, rt, nullptr, rf, rope_base,
-                                   lay, stream);
+                                   delta_ws, partials, terms, B * H, hd, T, W, rt, nullptr, rf,
+                                   rope_base, lay, stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
 }
 
@@ -288,12 +307,14 @@ fibattn_status_t fibattn_backward_dt(const void *q, const void *k, const void *v
         return FIBATTN_ERR_WORKSPACE;
     RungTable unused;
     memset(&unused, 0, sizeof(unused));
+    const WorkspaceLayout wl = workspace_layout(B, H, T, d_head, W, 0);
     float *delta_ws = (float *)workspace;
-    double *partials = (double *)((char *)workspace + align256(sizeof(float) * (size_t)B * H * T));
+    double *partials = (double *)((char *)workspace + wl.partials);
+    const RungTerms terms{(uint32_t *)((char *)workspace + wl.terms), wl.planes};
     const RopeFreq rf = make_rope_freq((double)rope_base, d_head);
     const Heads hd{H, H / H_kv};
     hipError_t e = launch_backward((int)dtype, d_head, q, k, v, o, lse, dO, dq, dk, dv, dalpha,
-                                   delta_ws, partials, B * H, hd, T, W, unused,
+                                   delta_ws, partials, terms, B * H, hd, T, W, unused,
                                    (const RungTable *)table, rf, rope_base,
                                    packed_layouts(H, H_kv, T, d_head), stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;

@@ -312,13 +312,13 @@ static hipError_t launch_backward_generic(int dtype, int D, const void *q, const
 
 hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const void *v,
                            const void *o, const float *lse, const void *dO, void *dq, void *dk,
-                           void *dv, float *dalpha, float *delta_ws, double *partials, int BH,
-                           const Heads &hd, int T, int W, const RungTable &rt,
-                           const RungTable *rtp, const RopeFreq &rf, float rope_base,
-                           const Layouts &lay, hipStream_t s) {
+                           void *dv, float *dalpha, float *delta_ws, double *partials,
+                           const RungTerms &terms, int BH, const Heads &hd, int T, int W,
+                           const RungTable &rt, const RungTable *rtp, const RopeFreq &rf,
+                           float rope_base, const Layouts &lay, hipStream_t s) {
     if (backward_mfma_supported(dtype, D, W))
-        return launch_backward_mfma(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials, BH,
-                                    hd, T, W, rt, rtp, rf, lay, s);
+        return launch_backward_mfma(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials,
+                                    terms, BH, hd, T, W, rt, rtp, rf, lay, s);
     hipError_t e = launch_backward_generic(dtype, D, q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws,
                                            partials, BH, hd, T, W, rt, rtp, lay, s);
     // R^T on dq and dk in place: gradients w.r.t. the unrotated q, k (R^T is linear, so

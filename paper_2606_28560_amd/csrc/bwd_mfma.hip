@@ -14,14 +14,18 @@
 //          which then reach 32 rows below the tile),
 //          dq += tau dS ((1-w) k[r0] + w k[r1]) on the VALU,
 //          dalpha partial += f (tau dS <q, k[r1]-k[r0]> + p <dO, v[r1]-v[r0]>);
-//   writes dq, Delta_i = <dO_i, o_i> and one float64 dalpha partial per workgroup
-//   (each query's terms in float32, then float64 across queries).
+//   writes dq, Delta_i = <dO_i, o_i>, one float64 dalpha partial per workgroup
+//   (each query's terms in float32, then float64 across queries) and, for every rung
+//   entry, the pair (tau dS, p) as bfloat16 (the rung terms, staged in LDS during the
+//   rung loop and copied out by each wave after it);
 // dk/dv kernel (key-stationary, 64 keys per workgroup, 16 per wave): the queries
 // that read key row j are j..j+W (window) and, for rung k, j+floor(d_k) (as row r0,
 // weight 1-w) and j+floor(d_k)+1 (as row r1, weight w):
 //   band:  S = Q.K^T and dP = dO.V^T tiles, dk^T += Q^T (tau dS), dv^T += dO^T P with
 //          the band's q and dO rows copied to LDS with direct-to-LDS loads;
-//   rungs: per-row dot2 products on the VALU;
+//   rungs: dk += (tau dS) q and dv += p dO with the dq kernel's rung terms, so a rung
+//          reads only the q and dO rows of its queries (bf16 dot2 accumulation, two
+//          rungs or one interpolated rung per batch, two batches in flight);
 //   each dk/dv row is written once; no atomics.  Workgroup 0 also sums the dalpha
 //   partials in a fixed order (float64), after the dq kernel has finished.
 #include "launch.h"
@@ -39,9 +43,9 @@ template <bool INTERP, bool DEV, bool STRIDED>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void bwd_dq_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const uint16_t *__restrict__ o, const float *__restrict__ lse, const uint16_t *__restrict__ dO,
-    uint16_t *__restrict__ dq, float *__restrict__ delta_out, double *__restrict__ partials, int T,
-    int W, RungTable rt_arg, const RungTable *__restrict__ rtp, RopeFreq rf, float tau, int tiles,
-    Heads hd, Layouts lay) {
+    uint16_t *__restrict__ dq, float *__restrict__ delta_out, double *__restrict__ partials,
+    RungTerms terms, int T, int W, RungTable rt_arg, const RungTable *__restrict__ rtp, RopeFreq rf,
+    float tau, int tiles, Heads hd, Layouts lay) {
     const RungTable &rt = DEV ? *rtp : rt_arg;
     const bool bad = DEV && rt.n < 0;  // a device alpha that is not finite and positive
     // staged K, V rows [T0 - kLeadQ, T0 + 64): the band and, interpolating, the short rungs
@@ -51,6 +55,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     __shared__ __align__(16) uint16_t vr[kStage * kD];
     __shared__ double sfreq[32];
     __shared__ double red[4];
+    // (tau dS, p) of every rung entry of the tile's queries, copied to terms.p at the end
+    // (stores inside the rung loop would hold up its loads: they share one counter)
+    __shared__ uint32_t sterm[kMaxRungs * kBwdB];
 
     const int lane = threadIdx.x & 63;
     const int wv = threadIdx.x >> 6;
@@ -177,6 +184,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         const float dP = (1.f - w) * p0 + w * p1;
         const float p = incl ? fast_exp2(sc * sl2 - lse2) : 0.f;
         const float cc = tau * p * (dP - delta);
+        // (tau dS, p) of this entry for the dk/dv kernel (zeros for an excluded entry)
+        if (gq == 0) sterm[r * kBwdB + 16 * wv + nq] = pack_bf16(cc, p);
         if (INTERP)
             acc_axpy2(acc, cc * (1.f - w), x[0], cc * w, x[2]);
         else
@@ -211,6 +220,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         }
     }
 
+    // this wave's rung terms, four rungs of its 16 queries per store (the entries were
+    // written to LDS by lanes of this wave; LDS accesses of a wave complete in order)
+    __builtin_amdgcn_wave_barrier();
+    for (int r0 = 0; r0 < nact; r0 += 4) {
+        const int r = r0 + (lane >> 4), qi = 16 * wv + (lane & 15);
+        if (r < nact && T0 + qi < T) terms.p[((size_t)bh * terms.planes + r) * T + T0 + qi] = sterm[r * kBwdB + qi];
+    }
+
     if (rf.on) acc_rope_t(acc, i, sfreq + 8 * gq);  // gradient w.r.t. the unrotated q
     if (i < T) {
         store_acc(dq + head_at<STRIDED, kD>(lay.dq, bh, hd.H, T) + (size_t)i * stdq, gq, acc, bad ? NAN : 1.f);
@@ -235,17 +252,16 @@ template <bool INTERP, int NH, bool ONE_PASS, bool DEV, bool STRIDED>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void bwd_dkdv_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const float *__restrict__ lse, const uint16_t *__restrict__ dO, const float *__restrict__ delta_in,
-    uint16_t *__restrict__ dk, uint16_t *__restrict__ dv, const double *__restrict__ partials,
-    int n_partials, float *__restrict__ dalpha, int T, int W, RungTable rt_arg,
+    RungTerms terms, uint16_t *__restrict__ dk, uint16_t *__restrict__ dv,
+    const double *__restrict__ partials, int n_partials, float *__restrict__ dalpha, int T, int W,
+    RungTable rt_arg,
     const RungTable *__restrict__ rtp, RopeFreq rf, float tau, int tiles, Heads hd, Layouts lay) {
     const RungTable &rt = DEV ? *rtp : rt_arg;
     constexpr int kKG = 4 / NH;          // key groups of 16 per workgroup
     constexpr int kKeys = 16 * kKG;      // keys per workgroup
     constexpr int kSt = kKeys + 16;      // staged query rows per head slot
-    // the tile's own K, V rows [T0 - kLead, T0 - kLead + kOwn): with interpolation also
-    // the neighbours j-1 and j+1 of every key j
-    constexpr int kLead = INTERP ? 4 : 0;
-    constexpr int kOwn = kKeys + (INTERP ? 8 : 0);
+    // the tile's own K, V rows [T0, T0 + kOwn) (the band's keys)
+    constexpr int kOwn = kKeys;
     __shared__ double sfreq[32];
     // q rows of every head slot, then their dO rows
     __shared__ __align__(16) uint16_t stage[2 * NH * kSt * kD];
@@ -290,7 +306,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     const int t0 = T0 + 16 * kg;
     const int jm = t0 + nm;      // MFMA layout key
     const int j_key = t0 + nq;   // quad layout key
-    const int jo = kLead + 16 * kg + nq;  // this key's row in kown / vown (quad layout)
 
     // rungs: some key of this wave has j + floor(d) < T for a prefix of the table
     int nact = 0;
@@ -310,74 +325,80 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         const int bh = hd.q_of(bk, pass * NH + hs);  // this wave's query head
         const uint16_t *Q = q + head_at<STRIDED, kD>(lay.q, bh, hd.H, T);
         const uint16_t *Gd = dO + head_at<STRIDED, kD>(lay.g, bh, hd.H, T);
-        const float *L = lse + (size_t)bh * T;
-        const float *Dl = delta_in + (size_t)bh * T;
-
-        // one interpolated rung: the rows (q, dO) of queries i0 = j + floor(d) and
-        // i0 + 1 with their lse (log2 units) and Delta
-        struct Rung {
-            Slice x[4];  // q0, g0 (query i0), q1, g1 (query i0 + 1)
-            float le[2], de[2];
+        const uint32_t *E = terms.p + (size_t)bh * terms.planes * T;  // this query head's terms
+        // Every rung entry's (tau dS, p) comes from the dq kernel, so a rung needs only the
+        // q and dO rows of the queries that read this key (the entry of a query that
+        // excludes the rung is zero).  The plane index is clamped to an active rung so a
+        // batch's second slot past the last active rung reads written terms (masked below).
+        // Integer offsets: query j + d0 of each of two rungs per batch.
+        struct Pair {
+            Slice x[4];     // q, dO of rung a's query; q, dO of rung b's query
+            uint32_t e[2];  // their (tau dS, p)
         };
-        auto load_rung = [&](int r, Rung &ru) {
+        auto load_pair = [&](int rb, Pair &pr) {
+#pragma unroll
+            for (int y = 0; y < 2; ++y) {
+                const int r = min(rb + y, nact - 1);
+                const int ic = min(j + rt.d0[r], T - 1);
+                pr.x[2 * y] = load_row(Q, ic, gq, stq);
+                pr.x[2 * y + 1] = load_row(Gd, ic, gq, stg);
+                pr.e[y] = E[(size_t)r * T + ic];
+            }
+        };
+        // Interpolated offsets: query i0 = j + floor(d) reads this key as row r0 (weight
+        // 1 - w) and query i0 + 1 reads it as row r1 (weight w).
+        struct Rung {
+            Slice x[4];     // q, dO of query i0; q, dO of query i0 + 1
+            uint32_t e[2];  // their (tau dS, p)
+        };
+        auto load_rung = [&](int r0, Rung &ru) {
+            const int r = min(r0, nact - 1);
 #pragma unroll
             for (int y = 0; y < 2; ++y) {
                 const int ic = min(j + rt.d0[r] + y, T - 1);
                 ru.x[2 * y] = load_row(Q, ic, gq, stq);
                 ru.x[2 * y + 1] = load_row(Gd, ic, gq, stg);
-                ru.le[y] = L[ic] * kLog2e;
-                ru.de[y] = Dl[ic];
+                ru.e[y] = E[(size_t)r * T + ic];
             }
         };
-        // two rungs' query rows (q, dO) with their lse (log2 units) and Delta
-        struct Pair {
-            Slice x[4];  // q0a, g0a, q0b, g0b
-            float le[2], de[2];
-        };
-        auto load_pair = [&](int rb, Pair &pr) {
-#pragma unroll
-            for (int y = 0; y < 2; ++y) {
-                const int ic = min(j + rt.d0[rb + y], T - 1);
-                pr.x[2 * y] = load_row(Q, ic, gq, stq);
-                pr.x[2 * y + 1] = load_row(Gd, ic, gq, stg);
-                pr.le[y] = L[ic] * kLog2e;
-                pr.de[y] = Dl[ic];
-            }
-        };
-        Pair pA;
-        Rung ru;
+        Pair pA, pB;
+        Rung rA, rB;
         if (0 < nact) {  // in flight during the band phase
-            if (INTERP) load_rung(0, ru);
+            if (INTERP) load_rung(0, rA);
             else load_pair(0, pA);
         }
-
         if (pass > 0) __syncthreads();  // every wave is done with the previous pass's rows
         // q and dO rows, lse and Delta of queries [T0, T0 + kSt) of every head slot (rows
         // past the end are clamped copies, masked below)
+        // (every copy is issued before the lse / Delta loads, whose LDS stores wait for
+        // all of this wave's loads)
 #pragma unroll 1
         for (int u = 0; u < NH; ++u) {
             const int hu = hd.q_of(bk, pass * NH + u);
-            const size_t ou = (size_t)hu * T;
             dma_rows<kSt>(stage + u * kSt * kD, q + head_at<STRIDED, kD>(lay.q, hu, hd.H, T), T0, T, stq);
             dma_rows<kSt>(stage + (NH + u) * kSt * kD, dO + head_at<STRIDED, kD>(lay.g, hu, hd.H, T), T0, T, stg);
+        }
+        if (pass == 0) {
+            dma_rows<kOwn>(kown, K, T0, T, stk);  // rows past the end: clamped copies
+            dma_rows<kOwn>(vown, V, T0, T, stv);
+            stage_freq(sfreq, rf);
+        }
+#pragma unroll 1
+        for (int u = 0; u < NH; ++u) {
+            const size_t ou = (size_t)hd.q_of(bk, pass * NH + u) * T;
             for (int c = threadIdx.x; c < kSt; c += 256) {
                 const int row = T0 + c;
                 sl[u * kSt + c] = row < T ? lse[ou + row] * kLog2e : 0.f;
                 sd[u * kSt + c] = row < T ? delta_in[ou + row] : 0.f;
             }
         }
-        if (pass == 0) {
-            dma_rows<kOwn>(kown, K, T0 - kLead, T, stk);  // rows outside [0, T): clamped copies
-            dma_rows<kOwn>(vown, V, T0 - kLead, T, stv);
-            stage_freq(sfreq, rf);
-        }
         wait_vmem();
         __syncthreads();
 
         // band (MFMA layout): queries [t0, t0 + 32) in two blocks
         {
-            const Slice km = dma_slice(kown, kLead + 16 * kg + nm, gm);
-            const Slice vm = dma_slice(vown, kLead + 16 * kg + nm, gm);
+            const Slice km = dma_slice(kown, 16 * kg + nm, gm);
+            const Slice vm = dma_slice(vown, 16 * kg + nm, gm);
             uint32_t cw[4], pw[4];
 #pragma unroll
             for (int b = 0; b < 2; ++b) {
@@ -416,68 +437,50 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         }
 
         if (!INTERP) {
-            const Slice ks = dma_slice(kown, jo, gq);
-            const Slice vs = dma_slice(vown, jo, gq);
-            // every w == 0: query j + d0 reads this row with weight 1; two rungs per batch
             auto compute_pair = [&](int rb, const Pair &pr) {
-                float cc[2], pp[2];
+                uint32_t e[2];
 #pragma unroll
                 for (int y = 0; y < 2; ++y) {
-                    const int i0 = j + rt.d0[rb + y];
-                    const bool in0 = rb + y < nact && j < T && i0 < T;
-                    const float sc = quad_sum(dot_slice(pr.x[2 * y], ks));
-                    const float dp = quad_sum(dot_slice(pr.x[2 * y + 1], vs));
-                    pp[y] = in0 ? fast_exp2(sc * sl2 - pr.le[y]) : 0.f;
-                    cc[y] = tau * pp[y] * (dp - pr.de[y]);
+                    const bool in = rb + y < nact && j < T && j + rt.d0[rb + y] < T;
+                    e[y] = in ? pr.e[y] : 0u;
                 }
-                acc_axpy2(adk, cc[0], pr.x[0], cc[1], pr.x[2]);
-                acc_axpy2(adv, pp[0], pr.x[1], pp[1], pr.x[3]);
+                // (tau dS_a, tau dS_b) and (p_a, p_b) as bfloat16 pairs
+                acc_axpy2_bf(adk, __builtin_amdgcn_perm(e[1], e[0], 0x05040100u), pr.x[0], pr.x[2]);
+                acc_axpy2_bf(adv, __builtin_amdgcn_perm(e[1], e[0], 0x07060302u), pr.x[1], pr.x[3]);
             };
-            // one pair in flight (register budget: four waves per SIMD)
+            // two batches in flight: load the next while accumulating the current
 #pragma unroll
-            for (int rb = 0; rb < kMaxRungs; rb += 2) {
+            for (int rb = 0; rb < kMaxRungs; rb += 4) {
                 if (rb < nact) {
-                    if (rb > 0) load_pair(rb, pA);
+                    if (rb + 2 < nact) load_pair(rb + 2, pB);
                     compute_pair(rb, pA);
+                    if (rb + 2 < nact) {
+                        if (rb + 4 < nact) load_pair(rb + 4, pA);
+                        compute_pair(rb + 2, pB);
+                    }
                 }
             }
         } else {
-            // query i0 = j + floor(d) reads this row as r0 (weight 1 - w) and row j-1
-            // as r1; query i0 + 1 reads row j+1 as r0 and this row as r1 (weight w).
-            // One rung in flight (register budget: four waves per SIMD); rows j-1, j,
-            // j+1 come from kown / vown.
             auto compute_rung = [&](int r, const Rung &ru) {
                 const float w = rt.w[r];
                 const int i0 = j + rt.d0[r];
-                const bool in0 = r < nact && j < T && i0 < T && (w == 0.f || j >= 1);
+                const bool in0 = r < nact && j < T && i0 < T;
                 const bool in1 = r < nact && j < T && i0 + 1 < T && w != 0.f;
-                float sa, sb, da, db;
-                {
-                    const Slice kj = dma_slice(kown, jo, gq);
-                    const Slice kl = dma_slice(kown, jo - 1, gq);
-                    const Slice kh = dma_slice(kown, jo + 1, gq);
-                    sa = quad_sum((1.f - w) * dot_slice(ru.x[0], kj) + w * dot_slice(ru.x[0], kl));
-                    sb = quad_sum((1.f - w) * dot_slice(ru.x[2], kh) + w * dot_slice(ru.x[2], kj));
-                }
-                {
-                    const Slice vj = dma_slice(vown, jo, gq);
-                    const Slice vl = dma_slice(vown, jo - 1, gq);
-                    const Slice vh = dma_slice(vown, jo + 1, gq);
-                    da = quad_sum((1.f - w) * dot_slice(ru.x[1], vj) + w * dot_slice(ru.x[1], vl));
-                    db = quad_sum((1.f - w) * dot_slice(ru.x[3], vh) + w * dot_slice(ru.x[3], vj));
-                }
-                const float pa = in0 ? fast_exp2(sa * sl2 - ru.le[0]) : 0.f;
-                const float ca = tau * pa * (da - ru.de[0]);
-                const float pb = in1 ? fast_exp2(sb * sl2 - ru.le[1]) : 0.f;
-                const float cb = tau * pb * (db - ru.de[1]);
-                acc_axpy2(adk, (1.f - w) * ca, ru.x[0], w * cb, ru.x[2]);
-                acc_axpy2(adv, (1.f - w) * pa, ru.x[1], w * pb, ru.x[3]);
+                const uint32_t ea = in0 ? ru.e[0] : 0u, eb = in1 ? ru.e[1] : 0u;
+                const float ca = (1.f - w) * bf16_lo(ea), pa = (1.f - w) * bf16_hi(ea);
+                const float cb = w * bf16_lo(eb), pb = w * bf16_hi(eb);
+                acc_axpy2(adk, ca, ru.x[0], cb, ru.x[2]);
+                acc_axpy2(adv, pa, ru.x[1], pb, ru.x[3]);
             };
 #pragma unroll
-            for (int r = 0; r < kMaxRungs; ++r) {
+            for (int r = 0; r < kMaxRungs; r += 2) {
                 if (r < nact) {
-                    if (r > 0) load_rung(r, ru);
-                    compute_rung(r, ru);
+                    if (r + 1 < nact) load_rung(r + 1, rB);
+                    compute_rung(r, rA);
+                    if (r + 1 < nact) {
+                        if (r + 2 < nact) load_rung(r + 2, rA);
+                        compute_rung(r + 1, rB);
+                    }
                 }
             }
         }
@@ -531,8 +534,9 @@ size_t bwd_mfma_num_partials(int BH, int T) { return (size_t)((T + kBwdB - 1) / 
 
 template <int NH>
 static hipError_t launch_dkdv(bool interp, const void *q, const void *k, const void *v,
-                              const float *lse, const void *dO, const float *delta_ws, void *dk,
-                              void *dv, const double *partials, int n_partials, float *dalpha,
+                              const float *lse, const void *dO, const float *delta_ws,
+                              const RungTerms &terms, void *dk, void *dv, const double *partials,
+                              int n_partials, float *dalpha,
                               int BH, const Heads &hd, int T, int W, const RungTable &rt,
                               const RungTable *rtp, const RopeFreq &rf, float tau,
                               const Layouts &lay, hipStream_t s) {
@@ -550,16 +554,16 @@ static hipError_t launch_dkdv(bool interp, const void *q, const void *k, const v
                         : (interp ? FIBATTN_DKDV(true, false) : FIBATTN_DKDV(false, false));
 #undef FIBATTN_DKDV
     return launch(kBwdDkDv, kern, dim3(tiles * (BH / hd.G)), dim3(256), 0, s, q, k, v, lse, dO,
-                  delta_ws, dk, dv, partials, n_partials, dalpha, T, W, rt, rtp, rf, tau, tiles, hd,
-                  lay);
+                  delta_ws, terms, dk, dv, partials, n_partials, dalpha, T, W, rt, rtp, rf, tau,
+                  tiles, hd, lay);
 }
 
 hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, const void *o,
                                 const float *lse, const void *dO, void *dq, void *dk, void *dv,
-                                float *dalpha, float *delta_ws, double *partials, int BH,
-                                const Heads &hd, int T, int W, const RungTable &rt,
-                                const RungTable *rtp, const RopeFreq &rf, const Layouts &lay,
-                                hipStream_t s) {
+                                float *dalpha, float *delta_ws, double *partials,
+                                const RungTerms &terms, int BH, const Heads &hd, int T, int W,
+                                const RungTable &rt, const RungTable *rtp, const RopeFreq &rf,
+                                const Layouts &lay, hipStream_t s) {
     const int tiles = (T + kBwdB - 1) / kBwdB;
     const float tau = 1.f / sqrtf(64.f);
     const int nb = tiles * BH;
@@ -572,16 +576,16 @@ hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, con
              : strided ? (interp ? bwd_dq_bf16_d64_kernel<true, false, true> : bwd_dq_bf16_d64_kernel<false, false, true>)
                        : (interp ? bwd_dq_bf16_d64_kernel<true, false, false> : bwd_dq_bf16_d64_kernel<false, false, false>);
     hipError_t e = launch(kBwdDq, dqk, dim3(nb), dim3(256), 0, s, q, k, v, o, lse, dO, dq, delta_ws,
-                          partials, T, W, rt, rtp, rf, tau, tiles, hd, lay);
+                          partials, terms, T, W, rt, rtp, rf, tau, tiles, hd, lay);
     if (e != hipSuccess) return e;
     // query heads per key/value head processed side by side in a workgroup
     if (hd.G % 4 == 0)
-        return launch_dkdv<4>(interp, q, k, v, lse, dO, delta_ws, dk, dv, partials, nb, dalpha, BH,
+        return launch_dkdv<4>(interp, q, k, v, lse, dO, delta_ws, terms, dk, dv, partials, nb, dalpha, BH,
                               hd, T, W, rt, rtp, rf, tau, lay, s);
     if (hd.G % 2 == 0)
-        return launch_dkdv<2>(interp, q, k, v, lse, dO, delta_ws, dk, dv, partials, nb, dalpha, BH,
+        return launch_dkdv<2>(interp, q, k, v, lse, dO, delta_ws, terms, dk, dv, partials, nb, dalpha, BH,
                               hd, T, W, rt, rtp, rf, tau, lay, s);
-    return launch_dkdv<1>(interp, q, k, v, lse, dO, delta_ws, dk, dv, partials, nb, dalpha, BH, hd,
+    return launch_dkdv<1>(interp, q, k, v, lse, dO, delta_ws, terms, dk, dv, partials, nb, dalpha, BH, hd,
                           T, W, rt, rtp, rf, tau, lay, s);
 }
 

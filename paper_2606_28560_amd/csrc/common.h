@@ -54,6 +54,16 @@ __host__ __device__ inline bool rung_table_fill(float alpha, const BaseTable &b,
     return true;
 }
 
+// Per-(query, rung) terms of the backward that the dq kernel of the matrix-core path
+// hands to its dk/dv kernel: for query i of flat head bh and rung r of the table, the
+// bfloat16 pair (tau dS, p) (tau dS in the low half) at index (bh * planes + r) * T + i
+// (planes >= the table's n).  The dk/dv accumulation rounds these weights to bfloat16
+// anyway.
+struct RungTerms {
+    uint32_t *p;
+    int planes;
+};
+
 // Grouped key/value heads (Section 3 "Model and training": 8 query heads share 2
 // key/value heads): query head h of batch b reads key/value head h / G of that batch.
 struct Heads {

@@ -42,10 +42,10 @@ size_t bwd_num_partials(int dtype, int D, int BH, int T);
 
 hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const void *v,
                            const void *o, const float *lse, const void *dO, void *dq, void *dk,
-                           void *dv, float *dalpha, float *delta_ws, double *partials, int BH,
-                           const Heads &hd, int T, int W, const RungTable &rt,
-                           const RungTable *rtp, const RopeFreq &rf, float rope_base,
-                           const Layouts &lay, hipStream_t s);
+                           void *dv, float *dalpha, float *delta_ws, double *partials,
+                           const RungTerms &terms, int BH, const Heads &hd, int T, int W,
+                           const RungTable &rt, const RungTable *rtp, const RopeFreq &rf,
+                           float rope_base, const Layouts &lay, hipStream_t s);
 
 // bfloat16, d_head = 64, W <= 16: matrix-core band + VALU rungs (fwd_mfma.hip, bwd_mfma.hip).
 bool forward_mfma_supported(int dtype, int D, int W);
@@ -56,10 +56,10 @@ bool backward_mfma_supported(int dtype, int D, int W);
 size_t bwd_mfma_num_partials(int BH, int T);
 hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, const void *o,
                                 const float *lse, const void *dO, void *dq, void *dk, void *dv,
-                                float *dalpha, float *delta_ws, double *partials, int BH,
-                                const Heads &hd, int T, int W, const RungTable &rt,
-                                const RungTable *rtp, const RopeFreq &rf, const Layouts &lay,
-                                hipStream_t s);
+                                float *dalpha, float *delta_ws, double *partials,
+                                const RungTerms &terms, int BH, const Heads &hd, int T, int W,
+                                const RungTable &rt, const RungTable *rtp, const RopeFreq &rf,
+                                const Layouts &lay, hipStream_t s);
 
 RopeFreq make_rope_freq(double rope_base, int D);  // on = 0 when rope_base <= 0
 

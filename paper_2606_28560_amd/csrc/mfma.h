@@ -130,9 +130,9 @@ __device__ __forceinline__ void acc_axpy(Acc16 &acc, float a, const Slice &x) {
 }
 
 // acc += a * x + b * y with one bf16 dot2 per dim: the pair (x_d, y_d) is packed
-// with v_perm and the weights (a, b) are rounded to bf16.
-__device__ __forceinline__ void acc_axpy2(Acc16 &acc, float a, const Slice &x, float b, const Slice &y) {
-    const bf16x2 ab = as_bf2(pack_bf16(a, b));
+// with v_perm; ab holds the bfloat16 weights (a in the low half).
+__device__ __forceinline__ void acc_axpy2_bf(Acc16 &acc, uint32_t abits, const Slice &x, const Slice &y) {
+    const bf16x2 ab = as_bf2(abits);
 #pragma unroll
     for (int w = 0; w < 8; ++w) {
         const uint32_t xu = word(x, w), yu = word(y, w);
@@ -143,6 +143,10 @@ __device__ __forceinline__ void acc_axpy2(Acc16 &acc, float a, const Slice &x, f
         acc.c[(d + 1) >> 2][(d + 1) & 3] =
             __builtin_amdgcn_fdot2_f32_bf16(as_bf2(hi), ab, acc.c[(d + 1) >> 2][(d + 1) & 3], false);
     }
+}
+// The same with float32 weights, rounded to bfloat16.
+__device__ __forceinline__ void acc_axpy2(Acc16 &acc, float a, const Slice &x, float b, const Slice &y) {
+    acc_axpy2_bf(acc, pack_bf16(a, b), x, y);
 }
 
 // Scaled store of the lane's slice as bf16 (two 16-byte stores).
