@@ -27,8 +27,9 @@ def to_gpu(t):
     return t.to("cuda").contiguous()
 
 
-def gpu_run(q, k, v, dO, W, base, alpha, backward=True, poison=True):
-    """Runs the HIP path on CPU tensors; returns float64 numpy results."""
+def gpu_run(q, k, v, dO, W, base, alpha, backward=True, poison=True, workspace=None):
+    """Runs the HIP path on CPU tensors; returns float64 numpy results.  `workspace`:
+    the backward's workspace (a uint8 device tensor), else the binding allocates one."""
     Q, K, V = to_gpu(q), to_gpu(k), to_gpu(v)
     o = torch.empty_like(Q)
     lse = torch.empty(Q.shape[:3], device="cuda", dtype=torch.float32)
@@ -43,7 +44,8 @@ def gpu_run(q, k, v, dO, W, base, alpha, backward=True, poison=True):
         if poison:
             for t in (dq, dk, dv, da):
                 t.fill_(float("nan"))
-        F.fibattn_backward(Q, K, V, o, lse, G, W, base, alpha, dq=dq, dk=dk, dv=dv, dalpha=da)
+        F.fibattn_backward(Q, K, V, o, lse, G, W, base, alpha, dq=dq, dk=dk, dv=dv, dalpha=da,
+                           workspace=workspace)
         out.update(dq=dq, dk=dk, dv=dv, dalpha=da)
     torch.cuda.synchronize()
     res = {kk: vv.double().cpu().numpy() for kk, vv in out.items()}

@@ -110,6 +110,15 @@ def test_invalid_arguments_return_codes_without_gpu():
                               1, 1, 8, 64, 8, b, 15, one, ctypes.c_float(0.5), 1, None) == 1
     assert L.fibattn_backward_workspace_bytes(1, 1, 8, 48, 8, 15) == 0
     assert L.fibattn_backward_workspace_bytes(8, 8, 1024, 64, 8, 15) > 8 * 8 * 1024 * 4
+    # the matrix-core shapes (d_head 64, W <= 16) add a 4-byte term per query and rung:
+    # K of them, or 32 (the most a table holds) for a device table (K = 0)
+    n = 8 * 8 * 1024
+    ws = L.fibattn_backward_workspace_bytes
+    assert ws(8, 8, 1024, 64, 8, 15) >= 4 * n + 8 * (n // 64) + 4 * 15 * n
+    assert ws(8, 8, 1024, 64, 8, 0) >= 4 * n + 8 * (n // 64) + 4 * 32 * n
+    assert ws(8, 8, 1024, 64, 8, 15) - ws(8, 8, 1024, 64, 8, 11) == 4 * 4 * n
+    assert ws(8, 8, 1024, 32, 8, 15) < 4 * n + 4 * 15 * n   # generic kernels: no terms
+    assert ws(8, 8, 1024, 64, 17, 15) < 4 * n + 4 * 15 * n
     # rope
     assert L.fibattn_rope(None, None, 1, 1, 8, 64, ctypes.c_float(1e4), 0, 1, None) == 1
     assert L.fibattn_rope(16, 16, 1, 1, 8, 64, ctypes.c_float(1.0), 0, 1, None) == 1

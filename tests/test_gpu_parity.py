@@ -234,6 +234,46 @@ def test_grouped_heads_parity(B, H, Hkv, T, D, dtype, W, base, alpha):
     compare(got, ref, dtype, f"gqa case {idx}")
 
 
+WS_CASES = [
+    # (B, H, H_kv, T, W, base, alpha), bf16 d_head 64: the matrix-core backward, whose
+    # dq kernel hands every rung entry's (tau dS, p) to dk/dv through the workspace
+    (2, 4, 4, 300, 8, FIB, 1.0),     # integer offsets, ragged tail
+    (1, 4, 4, 333, 8, FIB, 0.85),    # interpolated offsets
+    (1, 8, 2, 257, 10, POW2, 1.2),   # four query heads per key/value head in a workgroup
+    (1, 8, 1, 200, 8, FIB, 0.9),     # eight per key/value head: two passes
+    (1, 6, 2, 190, 6, FIB, 1.0),     # three per key/value head: one at a time
+]
+
+
+@pytest.mark.parametrize("B,H,Hkv,T,W,base,alpha", WS_CASES)
+def test_backward_ignores_workspace_contents(B, H, Hkv, T, W, base, alpha):
+    # The workspace is filled with all-ones bytes (NaN as float32, float64 and as
+    # bfloat16 pairs) before the call: a term the dk/dv kernel read without the dq
+    # kernel having written it would make dk or dv NaN.
+    idx = WS_CASES.index((B, H, Hkv, T, W, base, alpha))
+    print(f"workspace case {idx}: B{B} H{H} Hkv{Hkv} T{T} W{W} alpha={alpha}", flush=True)
+    x = _gqa_inputs(B, H, Hkv, T, 64, "bf16", 120 + idx)
+    need = F.fibattn_backward_workspace_bytes(B, H, T, 64, W, len(base))
+    ws = torch.full((need,), 0xFF, device="cuda", dtype=torch.uint8)
+    got = gpu_run(x["q"], x["k"], x["v"], x["dO"], W, base, alpha, workspace=ws)
+    ref = oracle_run(x["q"], x["k"], x["v"], x["dO"], W, base, alpha)
+    compare(got, ref, "bf16", f"workspace case {idx}")
+
+
+def test_workspace_reused_across_rung_tables():
+    # one workspace, sized for the longer base, serves three backward calls whose rung
+    # tables differ in length and distances (stale terms of an earlier call unused)
+    B, H, T = 1, 4, 400
+    ws = torch.empty(F.fibattn_backward_workspace_bytes(B, H, T, 64, 12, len(FIB)), device="cuda",
+                     dtype=torch.uint8)
+    for c, (W, base, alpha) in enumerate([(8, FIB, 1.3), (12, POW2, 0.9), (6, FIB[:9], 1.0)]):
+        print(f"reuse call {c}: W{W} K{len(base)} alpha={alpha}", flush=True)
+        x = _case_inputs(B, H, T, 64, "bf16", 60 + c)
+        got = gpu_run(x["q"], x["k"], x["v"], x["dO"], W, base, alpha, workspace=ws)
+        ref = oracle_run(x["q"], x["k"], x["v"], x["dO"], W, base, alpha)
+        compare(got, ref, "bf16", f"reuse call {c}")
+
+
 @pytest.mark.parametrize("alpha", [1.0, 0.7])
 def test_grouped_heads_full_size(alpha):
     # the 60M model's layer with its 2 key/value heads: B = 8, H = 8, T = 1024
