@@ -60,7 +60,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     __shared__ uint32_t sterm[kMaxRungs * kBwdB];
 
     const int lane = threadIdx.x & 63;
-    const int wv = threadIdx.x >> 6;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar work
     const int nm = lane & 15, gm = lane >> 4;  // MFMA layout
     const int nq = lane >> 2, gq = lane & 3;   // quad layout
     const int blk = xcd_remap(blockIdx.x, gridDim.x);
@@ -117,11 +117,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
                 }
             }
         } else if (which & 1) {
-            const int R0 = min(max(i - rt.d0[r], 0), T - 1);
+            // rows of the clamped query ic (a query past T is masked)
+            const int R0 = max(ic - rt.d0[r], 0);
             x[0] = load_row(K, R0, gq, stk);
             x[1] = load_row(V, R0, gq, stv);
             if (INTERP || (nq & 3) == 0) {
-                const int R1 = min(max(i - rt.d0[r] - 1, 0), T - 1);
+                const int R1 = max(ic - rt.d0[r] - 1, 0);
                 x[2] = load_row(K, R1, gq, stk);
                 x[3] = load_row(V, R1, gq, stv);
             }
@@ -168,20 +169,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     acc_to_quad(acc, lane);
 
     // rungs (quad layout), two batches in flight; r1 = -1 is the zero row
-    float dal_q = 0.f;  // this query's dalpha terms (float32; summed in float64 below)
+    float dal_q = 0.f;  // this lane's dalpha terms (float32; summed in float64 below)
     auto compute_rung = [&](int r, const Slice *x) {  // x = {k0, v0, k1, v1}
         const int d0 = rt.d0[r];
         const float w = rt.w[r];
-        const bool incl = r < nact && i < T && (d0 < i || (d0 == i && w == 0.f));
+        // with every w == 0 a rung is in the set of query i iff d0 <= i
+        const bool incl = r < nact && i < T && (INTERP ? (d0 < i || (d0 == i && w == 0.f)) : d0 <= i);
         const bool has1 = i - d0 - 1 >= 0;  // row r1 exists (else the zero row)
-        const float s0 = quad_sum(dot_slice(qq, x[0]));
-        const float s1r = quad_sum(dot_slice(qq, x[2]));
-        const float p0 = quad_sum(dot_slice(gqq, x[1]));
-        const float p1r = quad_sum(dot_slice(gqq, x[3]));
-        const float s1 = has1 ? s1r : 0.f;
-        const float p1 = has1 ? p1r : 0.f;
-        const float sc = (1.f - w) * s0 + w * s1;
-        const float dP = (1.f - w) * p0 + w * p1;
+        // this lane's parts of <q, k[r]>, <dO, v[r]> (four lanes per query)
+        const float s0l = dot_slice(qq, x[0]), p0l = dot_slice(gqq, x[1]);
+        const float s1a = dot_slice(qq, x[2]), p1a = dot_slice(gqq, x[3]);  // row r1 (or row 0)
+        const float s1l = has1 ? s1a : 0.f, p1l = has1 ? p1a : 0.f;
+        float sc, dP;
+        if (INTERP) {
+            sc = quad_sum((1.f - w) * s0l + w * s1l);
+            dP = quad_sum((1.f - w) * p0l + w * p1l);
+        } else {
+            sc = quad_sum(s0l);
+            dP = quad_sum(p0l);
+        }
         const float p = incl ? fast_exp2(sc * sl2 - lse2) : 0.f;
         const float cc = tau * p * (dP - delta);
         // (tau dS, p) of this entry for the dk/dv kernel (zeros for an excluded entry)
@@ -189,8 +195,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         if (INTERP)
             acc_axpy2(acc, cc * (1.f - w), x[0], cc * w, x[2]);
         else
-            acc_axpy(acc, cc, x[0]);
-        if (gq == 0 && incl) dal_q += (float)rt.f[r] * (cc * (s1 - s0) + p * (p1 - p0));
+            acc_axpy_bf(acc, cc, x[0]);
+        // dalpha: f (tau dS <q, k[r1] - k[r0]> + p <dO, v[r1] - v[r0]>) from this lane's
+        // parts; the wave and workgroup sums below add the four lanes of each query
+        dal_q += incl ? (float)rt.f[r] * (cc * (s1l - s0l) + p * (p1l - p0l)) : 0.f;
     };
     // with every w == 0, row r1 of query n is row r0 of query n - 1, four lanes below:
     // a DPP row shift, which leaves the loaded rows of each 16-lane row's first query
@@ -448,15 +456,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
                 acc_axpy2_bf(adk, __builtin_amdgcn_perm(e[1], e[0], 0x05040100u), pr.x[0], pr.x[2]);
                 acc_axpy2_bf(adv, __builtin_amdgcn_perm(e[1], e[0], 0x07060302u), pr.x[1], pr.x[3]);
             };
-            // two batches in flight: load the next while accumulating the current
+            // two batches in flight: load the next while accumulating the current (one in
+            // the instances that loop over head passes, whose registers hold more state)
+            if constexpr (ONE_PASS) {
 #pragma unroll
-            for (int rb = 0; rb < kMaxRungs; rb += 4) {
-                if (rb < nact) {
-                    if (rb + 2 < nact) load_pair(rb + 2, pB);
-                    compute_pair(rb, pA);
-                    if (rb + 2 < nact) {
-                        if (rb + 4 < nact) load_pair(rb + 4, pA);
-                        compute_pair(rb + 2, pB);
+                for (int rb = 0; rb < kMaxRungs; rb += 4) {
+                    if (rb < nact) {
+                        if (rb + 2 < nact) load_pair(rb + 2, pB);
+                        compute_pair(rb, pA);
+                        if (rb + 2 < nact) {
+                            if (rb + 4 < nact) load_pair(rb + 4, pA);
+                            compute_pair(rb + 2, pB);
+                        }
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int rb = 0; rb < kMaxRungs; rb += 2) {
+                    if (rb < nact) {
+                        if (rb > 0) load_pair(rb, pA);
+                        compute_pair(rb, pA);
                     }
                 }
             }
@@ -472,14 +491,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
                 acc_axpy2(adk, ca, ru.x[0], cb, ru.x[2]);
                 acc_axpy2(adv, pa, ru.x[1], pb, ru.x[3]);
             };
+            if constexpr (ONE_PASS) {
 #pragma unroll
-            for (int r = 0; r < kMaxRungs; r += 2) {
-                if (r < nact) {
-                    if (r + 1 < nact) load_rung(r + 1, rB);
-                    compute_rung(r, rA);
-                    if (r + 1 < nact) {
-                        if (r + 2 < nact) load_rung(r + 2, rA);
-                        compute_rung(r + 1, rB);
+                for (int r = 0; r < kMaxRungs; r += 2) {
+                    if (r < nact) {
+                        if (r + 1 < nact) load_rung(r + 1, rB);
+                        compute_rung(r, rA);
+                        if (r + 1 < nact) {
+                            if (r + 2 < nact) load_rung(r + 2, rA);
+                            compute_rung(r + 1, rB);
+                        }
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int r = 0; r < kMaxRungs; ++r) {
+                    if (r < nact) {
+                        if (r > 0) load_rung(r, rA);
+                        compute_rung(r, rA);
                     }
                 }
             }

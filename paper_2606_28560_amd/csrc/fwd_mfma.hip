@@ -45,7 +45,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     __shared__ __align__(16) uint16_t vr[kBandRows * kD];
 
     const int lane = threadIdx.x & 63;
-    const int wv = threadIdx.x >> 6;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar work
     const int nm = lane & 15, gm = lane >> 4;  // MFMA layout
     const int nq = lane >> 2, gq = lane & 3;   // quad layout
     const int blk = xcd_remap(blockIdx.x, gridDim.x);
@@ -75,7 +75,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
 
     const int im = t0 + nm;  // query of this lane in the MFMA layout
     const int i = t0 + nq;   // ... in the quad layout
-    const Slice qq = load_row(Q, min(i, T - 1), gq, stq);
+    const int ic = min(i, T - 1);
+    const Slice qq = load_row(Q, ic, gq, stq);
 
     // rung rows of a batch: kx[x*NS + s], vx[x*NS + s] = row r_s of rung rb + x
     // (from LDS for the first nlds rungs, else from global memory; `which` selects
@@ -93,7 +94,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
                     }
                 }
             } else if (which & 1) {
-                const int R0 = min(max(i - rt.d0[rb + x], 0), T - 1);
+                const int R0 = max(ic - rt.d0[rb + x], 0);  // a query past T is masked
 #pragma unroll
                 for (int sidx = 0; sidx < NS; ++sidx) {
                     const int R = max(R0 - sidx, 0);
@@ -164,7 +165,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
             const int r = rb + x;
             const int d0 = rt.d0[r];
             const float w = rt.w[r];
-            const bool incl = r < nact && (d0 < i || (d0 == i && w == 0.f));
+            // with every w == 0 a rung is in the set of query i iff d0 <= i
+            const bool incl = r < nact && (INTERP ? (d0 < i || (d0 == i && w == 0.f)) : d0 <= i);
             float part = dot_slice(qq, kx[x * NS]);
             if (INTERP) part = (1.f - w) * part + w * dot_slice(qq, kx[x * NS + 1]);
             part = quad_sum(part) * sl2;

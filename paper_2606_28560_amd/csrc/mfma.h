@@ -129,6 +129,20 @@ __device__ __forceinline__ void acc_axpy(Acc16 &acc, float a, const Slice &x) {
     }
 }
 
+// acc += a * x with bf16 dot2 products, no unpacking: the weight pairs (a, 0) and
+// (0, a) pick the low and the high element of each word (a rounded to bf16).
+__device__ __forceinline__ void acc_axpy_bf(Acc16 &acc, float a, const Slice &x) {
+    const uint32_t alo = pack_bf16(a, 0.f), ahi = alo << 16;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+        const uint32_t u = word(x, w);
+        const int d = 2 * w;
+        acc.c[d >> 2][d & 3] = __builtin_amdgcn_fdot2_f32_bf16(as_bf2(u), as_bf2(alo), acc.c[d >> 2][d & 3], false);
+        acc.c[(d + 1) >> 2][(d + 1) & 3] =
+            __builtin_amdgcn_fdot2_f32_bf16(as_bf2(u), as_bf2(ahi), acc.c[(d + 1) >> 2][(d + 1) & 3], false);
+    }
+}
+
 // acc += a * x + b * y with one bf16 dot2 per dim: the pair (x_d, y_d) is packed
 // with v_perm; ab holds the bfloat16 weights (a in the low half).
 __device__ __forceinline__ void acc_axpy2_bf(Acc16 &acc, uint32_t abits, const Slice &x, const Slice &y) {
