@@ -58,15 +58,15 @@ def parse_args():
 #            --no-learned-alpha --no-integer-offsets --copy-probe-mb 256
 # each scaled by what the same counter reads for the plain 256 MiB device copy of that run.
 # They hold only for the kernel sources they were taken on (COUNTER_SOURCES_SHA).
-COUNTER_SOURCES_SHA = "25ae0ca9f58ed6442a26b08e4c2922b95433494a8eccbc36a63f550b60e01b0e"
+COUNTER_SOURCES_SHA = "9e8da821d78b172b17d4c695df3124091e9d57dfbab5324d0678696a725b1497"
 COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
 COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
-    "forward": (12403.1, 8448.0),
-    "bwd_dq": (20781.4, 10416.2),
-    "bwd_dkdv": (18749.0, 16384.0),
+    "forward": (12388.1, 8448.0),
+    "bwd_dq": (20772.7, 10416.1),
+    "bwd_dkdv": (18826.6, 16384.0),
     "rope": (8220.3, 16384.0),
 }
-COPY_PROBE_KIB = (262144.0, 131094.2, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
+COPY_PROBE_KIB = (262144.0, 131092.7, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
 
 
 def kernel_sources_sha() -> str:
