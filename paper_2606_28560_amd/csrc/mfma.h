@@ -178,14 +178,25 @@ __device__ __forceinline__ void store_acc(uint16_t *row, int g, const Acc16 &acc
     *reinterpret_cast<uint4 *>(row + 32 + 8 * g) = b;
 }
 
+// cos and sin of the angle 2 pi t fr (fr: revolutions per position): t fr is reduced to
+// [-1/2, 1/2] in float64 and evaluated on the hardware sine and cosine units, whose
+// inputs are in revolutions (absolute error ~1e-6, far below the bf16 rounding of the
+// results these rotations feed).
+__device__ __forceinline__ void rope_cs_rev(int t, double fr, float &c, float &s) {
+    const double a = (double)t * fr;
+    const float r = (float)(a - rint(a));
+    s = __builtin_amdgcn_sinf(r);
+    c = __builtin_amdgcn_cosf(r);
+}
+
 // R^T (the inverse RoPE rotation) at position t on the lane's slice: slice positions
-// d and d + 8 hold the rotate-half pair (8g + d, 32 + 8g + d); inv8 points at the
-// eight inverse frequencies of lane group g.
-__device__ __forceinline__ void acc_rope_t(Acc16 &a, int t, const double *inv8) {
+// d and d + 8 hold the rotate-half pair (8g + d, 32 + 8g + d); rev8 points at the
+// eight frequencies (in revolutions per position) of lane group g.
+__device__ __forceinline__ void acc_rope_t(Acc16 &a, int t, const double *rev8) {
 #pragma unroll
     for (int d = 0; d < 8; ++d) {
         float c, s;
-        rope_cs(t, inv8[d], c, s);
+        rope_cs_rev(t, rev8[d], c, s);
         const float x = a.c[d >> 2][d & 3];
         const float y = a.c[2 + (d >> 2)][d & 3];
         a.c[d >> 2][d & 3] = x * c + y * s;
@@ -193,11 +204,12 @@ __device__ __forceinline__ void acc_rope_t(Acc16 &a, int t, const double *inv8) 
     }
 }
 
-// Stage the RoPE inverse frequencies in LDS (read by acc_rope_t after a barrier).
+// Stage the RoPE frequencies in LDS as revolutions per position (inverse frequency /
+// 2 pi; read by acc_rope_t after a barrier).
 __device__ __forceinline__ void stage_freq(double *dst, const RopeFreq &rf) {
     if (threadIdx.x == 0) {
 #pragma unroll
-        for (int j = 0; j < 32; ++j) dst[j] = rf.inv[j];
+        for (int j = 0; j < 32; ++j) dst[j] = rf.inv[j] * 0.15915494309189533576888376337251;
     }
 }
 
