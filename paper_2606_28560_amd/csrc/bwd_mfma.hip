@@ -334,6 +334,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         const uint16_t *Q = q + head_at<STRIDED, kD>(lay.q, bh, hd.H, T);
         const uint16_t *Gd = dO + head_at<STRIDED, kD>(lay.g, bh, hd.H, T);
         const uint32_t *E = terms.p + (size_t)bh * terms.planes * T;  // this query head's terms
+        // term of rung r, query ic: a 32-bit byte offset from the uniform base (planes * T
+        // entries of one head stay far below 2^30)
+        auto term = [&](int r, int ic) {
+            return *reinterpret_cast<const uint32_t *>(reinterpret_cast<const char *>(E) +
+                                                       4u * ((uint32_t)r * (uint32_t)T + (uint32_t)ic));
+        };
         // Every rung entry's (tau dS, p) comes from the dq kernel, so a rung needs only the
         // q and dO rows of the queries that read this key (the entry of a query that
         // excludes the rung is zero).  The plane index is clamped to an active rung so a
@@ -350,7 +356,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
                 const int ic = min(j + rt.d0[r], T - 1);
                 pr.x[2 * y] = load_row(Q, ic, gq, stq);
                 pr.x[2 * y + 1] = load_row(Gd, ic, gq, stg);
-                pr.e[y] = E[(size_t)r * T + ic];
+                pr.e[y] = term(r, ic);
             }
         };
         // Interpolated offsets: query i0 = j + floor(d) reads this key as row r0 (weight
@@ -366,7 +372,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
                 const int ic = min(j + rt.d0[r] + y, T - 1);
                 ru.x[2 * y] = load_row(Q, ic, gq, stq);
                 ru.x[2 * y + 1] = load_row(Gd, ic, gq, stg);
-                ru.e[y] = E[(size_t)r * T + ic];
+                ru.e[y] = term(r, ic);
             }
         };
         Pair pA, pB;
