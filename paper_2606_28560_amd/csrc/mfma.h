@@ -34,13 +34,6 @@ struct Slice {
     uint4 a, b;
 };
 
-__device__ __forceinline__ Slice load_slice(const uint16_t *row, int g) {
-    Slice s;
-    s.a = *reinterpret_cast<const uint4 *>(row + 8 * g);
-    s.b = *reinterpret_cast<const uint4 *>(row + 32 + 8 * g);
-    return s;
-}
-
 // Slice g of row `row` of rows `st` elements apart (64 contiguous bf16 each) at a
 // uniform base address: a 32-bit byte offset from the base lets the loads use
 // scalar-base addressing (the host keeps every row offset below 2^31 bytes).
@@ -53,15 +46,9 @@ __device__ __forceinline__ Slice load_row(const uint16_t *base, int row, int g, 
     return s;
 }
 
-// 2^x with the hardware instruction (no denormal rescaling; x <= 0 here).
+// 2^x with the hardware instruction (no denormal rescaling; here x <= 8, and results
+// below the float32 normal range are negligible weights).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-__device__ __forceinline__ Slice zero_slice() {
-    Slice s;
-    s.a = make_uint4(0, 0, 0, 0);
-    s.b = make_uint4(0, 0, 0, 0);
-    return s;
-}
 
 __device__ __forceinline__ uint32_t word(const Slice &s, int w) {
     switch (w) {
@@ -116,17 +103,6 @@ struct Acc16 {
 __device__ __forceinline__ void acc_zero(Acc16 &a) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) a.c[c] = f32x4{0.f, 0.f, 0.f, 0.f};
-}
-
-// acc += a * x (x one bf16 slice), float32 FMAs.
-__device__ __forceinline__ void acc_axpy(Acc16 &acc, float a, const Slice &x) {
-#pragma unroll
-    for (int w = 0; w < 8; ++w) {
-        const uint32_t u = word(x, w);
-        const int d = 2 * w;
-        acc.c[d >> 2][d & 3] = fmaf(a, bf16_lo(u), acc.c[d >> 2][d & 3]);
-        acc.c[(d + 1) >> 2][(d + 1) & 3] = fmaf(a, bf16_hi(u), acc.c[(d + 1) >> 2][(d + 1) & 3]);
-    }
 }
 
 // acc += a * x with bf16 dot2 products, no unpacking: the weight pairs (a, 0) and
