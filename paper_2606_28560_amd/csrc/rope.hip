@@ -60,12 +60,14 @@ __global__ __launch_bounds__(256) void rope_kernel(const S *x, S *y, int BH, int
     }
 }
 
-// bfloat16, d_head 64: a workgroup owns 4 positions of 16 (b, h) rows (64 rows).
+// bfloat16, d_head 64: a workgroup owns 8 positions of 16 (b, h) rows (128 rows; each
+// lane group of four handles two positions, t and t + 4, of one head, so two rows'
+// loads are in flight per lane: 10.7 -> 10.2 us for q and k of the 60M layer).
 // Lane group g of a row's four lanes holds dims [8g, 8g+8) and [32+8g, 32+8g+8),
 // i.e. the eight rotate-half pairs (j, j+32), j in [8g, 8g+8): two 16-byte loads
-// and stores per lane, reading 64 contiguous bytes per row per instruction.  The
-// loads are issued before the angles are evaluated.
-constexpr int kRope64TP = 4;
+// and stores per lane and row, reading 64 contiguous bytes per row per instruction.
+// The loads are issued before the angles are evaluated.
+constexpr int kRope64TP = 8;
 constexpr int kRope64RB = 16;
 
 // blockIdx.z selects the tensor: (x0 -> y0) or (x1 -> y1), each placed by its io
@@ -85,38 +87,47 @@ __global__ __launch_bounds__(256) void rope_bf16_d64_kernel(const uint16_t *x0, 
     const int t0 = blockIdx.x * kRope64TP;
     const int g = threadIdx.x & 3;
     const int rr = threadIdx.x >> 2;  // 0..63
-    const int tt = rr & (kRope64TP - 1);
-    const int t = t0 + tt;
     const int bh = blockIdx.y * kRope64RB + (rr >> 2);
-    const bool live = t < T && bh < BH;
-    const int bhc = min(bh, BH - 1), tc = min(t, T - 1);
-    const size_t packed = ((size_t)bhc * T + tc) * 64;
-    const uint16_t *xr = x + (STRIDED ? io.x.head(bhc, heads) + (long long)tc * io.x.st : packed);
-    uint16_t *yr = y + (STRIDED ? io.y.head(bhc, heads) + (long long)tc * io.y.st : packed);
-    const uint4 a = *reinterpret_cast<const uint4 *>(xr + 8 * g);
-    const uint4 b = *reinterpret_cast<const uint4 *>(xr + 32 + 8 * g);
-    if (threadIdx.x < kRope64TP * 32) {
+    const int bhc = min(bh, BH - 1);
+    uint4 a[2], b[2];
+    const uint16_t *xr[2];
+    uint16_t *yr[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {  // positions t0 + (rr & 3) and t0 + (rr & 3) + 4
+        const int tc = min(t0 + (rr & 3) + 4 * h, T - 1);
+        const size_t packed = ((size_t)bhc * T + tc) * 64;
+        xr[h] = x + (STRIDED ? io.x.head(bhc, heads) + (long long)tc * io.x.st : packed);
+        yr[h] = y + (STRIDED ? io.y.head(bhc, heads) + (long long)tc * io.y.st : packed);
+        a[h] = *reinterpret_cast<const uint4 *>(xr[h] + 8 * g);
+        b[h] = *reinterpret_cast<const uint4 *>(xr[h] + 32 + 8 * g);
+    }
+    {
         float c, sv;
         rope_cs(t0 + (threadIdx.x >> 5), rf.inv[threadIdx.x & 31], c, sv);
         cs[threadIdx.x] = c;
         sn[threadIdx.x] = transpose ? -sv : sv;
     }
     __syncthreads();
-    if (!live) return;
-    const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w};
-    uint32_t ow[4], pw[4];
-    const float *C = cs + tt * 32 + 8 * g;
-    const float *Sn = sn + tt * 32 + 8 * g;
+    if (bh >= BH) return;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-        const float u0 = bf16_lo(aw[w]), u1 = bf16_hi(aw[w]);
-        const float v0 = bf16_lo(bw[w]), v1 = bf16_hi(bw[w]);
-        const float c0 = C[2 * w], c1 = C[2 * w + 1], s0 = Sn[2 * w], s1 = Sn[2 * w + 1];
-        ow[w] = f32_to_bf16(u0 * c0 - v0 * s0) | (f32_to_bf16(u1 * c1 - v1 * s1) << 16);
-        pw[w] = f32_to_bf16(v0 * c0 + u0 * s0) | (f32_to_bf16(v1 * c1 + u1 * s1) << 16);
+    for (int h = 0; h < 2; ++h) {
+        const int tt = (rr & 3) + 4 * h;
+        if (t0 + tt >= T) continue;
+        const uint32_t aw[4] = {a[h].x, a[h].y, a[h].z, a[h].w}, bw[4] = {b[h].x, b[h].y, b[h].z, b[h].w};
+        uint32_t ow[4], pw[4];
+        const float *C = cs + tt * 32 + 8 * g;
+        const float *Sn = sn + tt * 32 + 8 * g;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const float u0 = bf16_lo(aw[w]), u1 = bf16_hi(aw[w]);
+            const float v0 = bf16_lo(bw[w]), v1 = bf16_hi(bw[w]);
+            const float c0 = C[2 * w], c1 = C[2 * w + 1], s0 = Sn[2 * w], s1 = Sn[2 * w + 1];
+            ow[w] = f32_to_bf16(u0 * c0 - v0 * s0) | (f32_to_bf16(u1 * c1 - v1 * s1) << 16);
+            pw[w] = f32_to_bf16(v0 * c0 + u0 * s0) | (f32_to_bf16(v1 * c1 + u1 * s1) << 16);
+        }
+        *reinterpret_cast<uint4 *>(yr[h] + 8 * g) = make_uint4(ow[0], ow[1], ow[2], ow[3]);
+        *reinterpret_cast<uint4 *>(yr[h] + 32 + 8 * g) = make_uint4(pw[0], pw[1], pw[2], pw[3]);
     }
-    *reinterpret_cast<uint4 *>(yr + 8 * g) = make_uint4(ow[0], ow[1], ow[2], ow[3]);
-    *reinterpret_cast<uint4 *>(yr + 32 + 8 * g) = make_uint4(pw[0], pw[1], pw[2], pw[3]);
 }
 
 RopeFreq make_rope_freq(double rope_base, int D) {
