@@ -8,10 +8,9 @@
 //          dS = P (dP - Delta), dq^T += K^T (tau dS)^T; the band's K and V rows are
 //          copied to LDS with direct-to-LDS loads;
 //   rungs: per-row bf16 dot2 products for <q, k[r0]>, <q, k[r1]>, <dO, v[r0]>,
-//          <dO, v[r1]> (the r1 terms are needed for dalpha even when w = 0; then row
-//          r1 of a query is row r0 of the previous query, taken from its lanes;
-//          with interpolation the rows of short rungs come from the staged rows,
-//          which then reach 32 rows below the tile),
+//          <dO, v[r1]> (the r1 terms are needed for dalpha even when w = 0; with
+//          interpolation the rows of short rungs come from the staged rows, which
+//          then reach 32 rows below the tile),
 //          dq += tau dS ((1-w) k[r0] + w k[r1]) on the VALU,
 //          dalpha partial += f (tau dS <q, k[r1]-k[r0]> + p <dO, v[r1]-v[r0]>);
 //   writes dq, Delta_i = <dO_i, o_i>, one float64 dalpha partial per workgroup
@@ -100,32 +99,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 #pragma unroll
     for (int r = 0; r < kMaxRungs; ++r) nlds += (INTERP && r < rt.n && rt.d0[r] + 1 <= kLeadQ + 16 * wv) ? 1 : 0;
     nlds = __builtin_amdgcn_readfirstlane(nlds);
-    // x = {k0, v0, k1, v1}: rows r0 and r1 = r0 - 1 of K and V.  When every w == 0
-    // only the first query of each 16-lane row (queries t0, t0+4, t0+8, t0+12) loads
-    // its r1 rows here; fill_r1 takes the others from the previous query's lanes.
-    // (rows of the first nlds rungs from LDS, the others from global memory; `which`
-    // selects 1 = global rungs only, 2 = LDS rungs only, 3 = both)
+    // x = {k0, v0, k1, v1}: rows r0 and r1 = r0 - 1 of K and V (r1 is needed for
+    // dalpha even when w == 0; then it is row r0 of the previous query, but loading it
+    // costs less than moving it across lanes).  Rows of the first nlds rungs come from
+    // LDS, the others from global memory; `which` selects 1 = global rungs only,
+    // 2 = LDS rungs only, 3 = both.
     auto load_rung = [&](int r, Slice *x, int which) {
         if (r < nlds) {
             if (which & 2) {
                 const int L0 = 16 * wv + nq + kLeadQ - rt.d0[r];
                 x[0] = dma_slice(kr, L0, gq);
                 x[1] = dma_slice(vr, L0, gq);
-                if (INTERP || (nq & 3) == 0) {
-                    x[2] = dma_slice(kr, L0 - 1, gq);
-                    x[3] = dma_slice(vr, L0 - 1, gq);
-                }
+                x[2] = dma_slice(kr, L0 - 1, gq);
+                x[3] = dma_slice(vr, L0 - 1, gq);
             }
         } else if (which & 1) {
             // rows of the clamped query ic (a query past T is masked)
             const int R0 = max(ic - rt.d0[r], 0);
+            const int R1 = max(ic - rt.d0[r] - 1, 0);
             x[0] = load_row(K, R0, gq, stk);
             x[1] = load_row(V, R0, gq, stv);
-            if (INTERP || (nq & 3) == 0) {
-                const int R1 = max(ic - rt.d0[r] - 1, 0);
-                x[2] = load_row(K, R1, gq, stk);
-                x[3] = load_row(V, R1, gq, stv);
-            }
+            x[2] = load_row(K, R1, gq, stk);
+            x[3] = load_row(V, R1, gq, stv);
         }
     };
     Slice xA[4], xB[4];
@@ -200,29 +195,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         // parts; the wave and workgroup sums below add the four lanes of each query
         dal_q += incl ? (float)rt.f[r] * (cc * (s1l - s0l) + p * (p1l - p0l)) : 0.f;
     };
-    // with every w == 0, row r1 of query n is row r0 of query n - 1, four lanes below:
-    // a DPP row shift, which leaves the loaded rows of each 16-lane row's first query
-    auto fill_r1 = [&](Slice *x) {
-        if (!INTERP) {
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                uint32_t *d = reinterpret_cast<uint32_t *>(&x[2 + h]);
-                const uint32_t *src = reinterpret_cast<const uint32_t *>(&x[h]);
-#pragma unroll
-                for (int u = 0; u < 8; ++u)
-                    d[u] = (uint32_t)__builtin_amdgcn_update_dpp((int)d[u], (int)src[u], 0x114, 0xF, 0xF, false);
-            }
-        }
-    };
 #pragma unroll
     for (int rb = 0; rb < kMaxRungs; rb += 2) {
         if (rb < nact) {
             if (rb + 1 < nact) load_rung(rb + 1, xB, 3);
-            fill_r1(xA);
             compute_rung(rb, xA);
             if (rb + 1 < nact) {
                 if (rb + 2 < nact) load_rung(rb + 2, xA, 3);
-                fill_r1(xB);
                 compute_rung(rb + 1, xB);
             }
         }
