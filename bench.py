@@ -58,15 +58,15 @@ def parse_args():
 #            --no-learned-alpha --no-integer-offsets --copy-probe-mb 256
 # each scaled by what the same counter reads for the plain 256 MiB device copy of that run.
 # They hold only for the kernel sources they were taken on (COUNTER_SOURCES_SHA).
-COUNTER_SOURCES_SHA = "1e3c54c457673ed4210582e81646500d74e90c5685d6039a413ec9da942adfb1"
+COUNTER_SOURCES_SHA = "31323547a54d69939999261942c488e08fa5b30d24456f38ce0820a0c52f429d"
 COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
 COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
     "forward": (12388.1, 8448.0),
-    "bwd_dq": (20789.6, 10416.2),
-    "bwd_dkdv": (18904.6, 16384.0),
-    "rope": (8220.3, 16384.0),
+    "bwd_dq": (20787.6, 10416.1),
+    "bwd_dkdv": (18940.0, 16384.0),
+    "rope": (8228.8, 16384.0),
 }
-COPY_PROBE_KIB = (262144.0, 131092.9, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
+COPY_PROBE_KIB = (262144.0, 131093.1, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
 
 
 def kernel_sources_sha() -> str:
