@@ -422,10 +422,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
             }
             acc_to_quad(bk_, lane);
             acc_to_quad(bv_, lane);
+            if (ONE_PASS || pass == 0) {  // the accumulators are still zero: no adds
+                adk = bk_;
+                adv = bv_;
+            } else {
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                adk.c[c] += bk_.c[c];
-                adv.c[c] += bv_.c[c];
+                for (int c = 0; c < 4; ++c) {
+                    adk.c[c] += bk_.c[c];
+                    adv.c[c] += bv_.c[c];
+                }
             }
         }
 
