@@ -300,6 +300,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && t0 + rt.d0[r] < T) ? 1 : 0;
     nact = __builtin_amdgcn_readfirstlane(nact);  // wave-uniform: scalar branches
 
+    // With several passes the table is staged before the pass loop: inside it the
+    // compiler hoists the table's products out of the loop and keeps them in scratch
+    // memory until the first pass stores them (behind a wait for every copy in flight).
+    if constexpr (!ONE_PASS) stage_freq(sfreq, rf);
     Acc16 adk, adv;
     acc_zero(adk);
     acc_zero(adv);
@@ -374,7 +378,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         if (pass == 0) {
             dma_rows<kOwn>(kown, K, T0, T, stk);  // rows past the end: clamped copies
             dma_rows<kOwn>(vown, V, T0, T, stv);
-            stage_freq(sfreq, rf);
+            if constexpr (ONE_PASS) stage_freq(sfreq, rf);
         }
 #pragma unroll 1
         for (int u = 0; u < NH; ++u) {
