@@ -62,6 +62,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar work
     const int nm = lane & 15, gm = lane >> 4;  // MFMA layout
     const int nq = lane >> 2, gq = lane & 3;   // quad layout
+    // Raised issue priority while the prologue's loads and row copies are issued (as
+    // in the forward); dk/dv keeps the default (measured slower at T = 4096).
+    __builtin_amdgcn_s_setprio(2);
     const int blk = xcd_remap(blockIdx.x, gridDim.x);
     const int bh = blk / tiles;
     const int T0 = (blk % tiles) * kBwdB;
@@ -130,6 +133,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     // clamped copies: their keys are masked below)
     dma_rows<kStage>(kr, K, T0 - kLeadQ, T, stk);
     dma_rows<kStage>(vr, V, T0 - kLeadQ, T, stv);
+    __builtin_amdgcn_s_setprio(0);
     stage_freq(sfreq, rf);
     // Delta_i = <dO_i, o_i>, once every load of the prologue is in flight
     const float delta = quad_sum(dot_slice(gqq, oq));

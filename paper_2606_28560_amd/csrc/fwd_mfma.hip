@@ -48,6 +48,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar work
     const int nm = lane & 15, gm = lane >> 4;  // MFMA layout
     const int nq = lane >> 2, gq = lane & 3;   // quad layout
+    // Raised issue priority while this wave sets up and issues its row copies, so a
+    // starting workgroup's loads are not queued behind resident waves' rung arithmetic.
+    __builtin_amdgcn_s_setprio(2);
     const int blk = xcd_remap(blockIdx.x, gridDim.x);
     const int bh = blk / tiles;
     const int T0 = (blk % tiles) * kFwdBQ;
@@ -110,6 +113,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     // clamped copies: their keys are masked below)
     dma_rows<kBandRows>(kr, K, T0 - kLeadF, T, stk);
     dma_rows<kBandRows>(vr, V, T0 - kLeadF, T, stv);
+    __builtin_amdgcn_s_setprio(0);
     wait_vmem();
     __syncthreads();
     if (0 < nact) load_batch(0, kA, vA, 2);
