@@ -85,7 +85,9 @@ fibattn_status_t fibattn_rung_table(float alpha, const int32_t *base, int K, int
  *   lse  : float32 [B,H,T] (written): natural-log log-sum-exp of the tau-scaled
  *          logits of each query, saved for the backward
  * Limits: d_head in {32, 64, 128}; 0 <= W <= FIBATTN_MAX_WINDOW; 0 <= K <= FIBATTN_MAX_RUNGS;
- * alpha finite and > 0; B*H <= 65535.  bfloat16 with d_head 64 and W <= 16 runs the
+ * alpha finite and > 0; B*H <= 65535; B*H*T*d_head <= 2^40; one head's rows,
+ * T*d_head elements, under 2^31 bytes (T < 2^24 for bfloat16 with d_head 64): else
+ * FIBATTN_ERR_UNSUPPORTED.  bfloat16 with d_head 64 and W <= 16 runs the
  * matrix-core kernels; every other supported shape runs the generic kernels.
  */
 fibattn_status_t fibattn_forward(const void *q, const void *k, const void *v,

@@ -42,6 +42,11 @@ fibattn_status_t check_common(int B, int H, int T, int d_head, int W, int K, fib
     if (dtype != FIBATTN_FP32 && dtype != FIBATTN_BF16) return FIBATTN_ERR_INVALID_ARG;
     if ((long long)B * H > 65535) return FIBATTN_ERR_UNSUPPORTED;
     if ((long long)B * H * T * d_head > (1ll << 40)) return FIBATTN_ERR_UNSUPPORTED;
+    // one packed head's rows below 2^31 bytes: the kernels address rows (and the
+    // backward's per-rung terms, 4 bytes per query and rung) with 32-bit offsets from
+    // the head's first row
+    const long long es = dtype == FIBATTN_BF16 ? 2 : 4;
+    if ((long long)T * d_head * es >= (1ll << 31)) return FIBATTN_ERR_UNSUPPORTED;
     if (d_head != 32 && d_head != 64 && d_head != 128) return FIBATTN_ERR_UNSUPPORTED;
     if (W > FIBATTN_MAX_WINDOW || K > FIBATTN_MAX_RUNGS) return FIBATTN_ERR_UNSUPPORTED;
     return FIBATTN_OK;
@@ -177,7 +182,9 @@ static WorkspaceLayout workspace_layout(int B, int H, int T, int d_head, int W, 
 }
 
 size_t fibattn_backward_workspace_bytes(int B, int H, int T, int d_head, int W, int K) {
-    if (check_common(B, H, T, d_head, W, K, FIBATTN_FP32) != FIBATTN_OK) return 0;
+    // the workspace does not depend on the storage type: checked here under the looser
+    // (bfloat16) size limits, the call itself then checks those of its own type
+    if (check_common(B, H, T, d_head, W, K, FIBATTN_BF16) != FIBATTN_OK) return 0;
     return workspace_layout(B, H, T, d_head, W, K).total;
 }
 
@@ -197,13 +204,11 @@ static fibattn_status_t backward_impl(const void *q, const void *k, const void *
     for (const void *p : ptrs)
         if (!aligned16(p)) return FIBATTN_ERR_INVALID_ARG;
     if (!(rope_base == 0.f || (rope_base > 1.f && isfinite(rope_base)))) return FIBATTN_ERR_INVALID_ARG;
-    if (!workspace || !aligned16(workspace) ||
-        workspace_bytes < fibattn_backward_workspace_bytes(B, H, T, d_head, W, K))
-        return FIBATTN_ERR_WORKSPACE;
+    const WorkspaceLayout wl = workspace_layout(B, H, T, d_head, W, K);
+    if (!workspace || !aligned16(workspace) || workspace_bytes < wl.total) return FIBATTN_ERR_WORKSPACE;
     RungTable rt;
     st = build_table(alpha, base, K, W, &rt);
     if (st != FIBATTN_OK) return st;
-    const WorkspaceLayout wl = workspace_layout(B, H, T, d_head, W, K);
     float *delta_ws = (float *)workspace;
     double *partials = (double *)((char *)workspace + wl.partials);
     const RungTerms terms{(uint32_t *)((char *)workspace + wl.terms), wl.planes};
@@ -302,12 +307,10 @@ fibattn_status_t fibattn_backward_dt(const void *q, const void *k, const void *v
     for (const void *p : ptrs)
         if (!aligned16(p)) return FIBATTN_ERR_INVALID_ARG;
     if (!(rope_base == 0.f || (rope_base > 1.f && isfinite(rope_base)))) return FIBATTN_ERR_INVALID_ARG;
-    if (!workspace || !aligned16(workspace) ||
-        workspace_bytes < fibattn_backward_workspace_bytes(B, H, T, d_head, W, 0))
-        return FIBATTN_ERR_WORKSPACE;
+    const WorkspaceLayout wl = workspace_layout(B, H, T, d_head, W, 0);
+    if (!workspace || !aligned16(workspace) || workspace_bytes < wl.total) return FIBATTN_ERR_WORKSPACE;
     RungTable unused;
     memset(&unused, 0, sizeof(unused));
-    const WorkspaceLayout wl = workspace_layout(B, H, T, d_head, W, 0);
     float *delta_ws = (float *)workspace;
     double *partials = (double *)((char *)workspace + wl.partials);
     const RungTerms terms{(uint32_t *)((char *)workspace + wl.terms), wl.planes};

@@ -101,6 +101,16 @@ def test_invalid_arguments_return_codes_without_gpu():
     assert L.fibattn_forward(16, 16, 16, 16, 16, 1, 1, 8, 96, 8, b, 15, one, 1, None) == 2
     assert L.fibattn_forward(16, 16, 16, 16, 16, 1, 1, 8, 64, 129, b, 15, one, 1, None) == 2
     assert L.fibattn_forward(16, 16, 16, 16, 16, 1, 1, 8, 64, 8, b, 15, one, 9, None) == 1
+    # one head's rows must stay below 2^31 bytes (32-bit row offsets in the kernels)
+    assert L.fibattn_forward(16, 16, 16, 16, 16, 1, 1, 1 << 24, 64, 8, b, 15, one, 1, None) == 2
+    assert L.fibattn_forward(16, 16, 16, 16, 16, 1, 1, 1 << 22, 128, 8, b, 15, one, 0, None) == 2
+    assert L.fibattn_backward_workspace_bytes(1, 1, 1 << 24, 64, 8, 15) == 0
+    assert L.fibattn_backward_workspace_bytes(1, 1, (1 << 24) - 1, 64, 8, 15) > 0
+    # the workspace size does not depend on the storage type: a bfloat16 shape beyond
+    # the float32 limit still gets its size, and the bfloat16 call checks against it
+    assert L.fibattn_backward_workspace_bytes(1, 1, 1 << 23, 64, 8, 15) > 4 * 15 * (1 << 23)
+    assert L.fibattn_backward(16, 16, 16, 16, 16, 16, 16, 16, 16, 16, 16, 256,
+                              1, 1, 1 << 23, 64, 8, b, 15, one, ctypes.c_float(0.0), 1, None) == 3
     # workspace
     zero = ctypes.c_float(0.0)
     assert L.fibattn_backward(16, 16, 16, 16, 16, 16, 16, 16, 16, 16, None, 0,
