@@ -58,15 +58,15 @@ def parse_args():
 #            --no-learned-alpha --no-integer-offsets --copy-probe-mb 256
 # each scaled by what the same counter reads for the plain 256 MiB device copy of that run.
 # They hold only for the kernel sources they were taken on (COUNTER_SOURCES_SHA).
-COUNTER_SOURCES_SHA = "58866e657c63dcb66420e41bda1f3d40973f4c428b0c94c5f526e0a99bb7dcb8"
+COUNTER_SOURCES_SHA = "8b8e424c556dbf5b0502cf05bbe01adc1c42b6bf2bcce09b4ab3d7a2d3d38ef7"
 COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
 COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
-    "forward": (12388.1, 8448.0),
-    "bwd_dq": (20787.6, 10416.1),
-    "bwd_dkdv": (18804.8, 16384.0),
+    "forward": (12387.6, 8448.0),
+    "bwd_dq": (20787.9, 10417.0),
+    "bwd_dkdv": (18885.5, 16384.0),
     "rope": (8228.8, 16384.0),
 }
-COPY_PROBE_KIB = (262144.0, 131093.2, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
+COPY_PROBE_KIB = (262144.0, 131092.6, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
 
 
 def kernel_sources_sha() -> str:
