@@ -214,6 +214,11 @@ GQA = [
     (1, 6, 2, 257, 64, "bf16", 8, FIB, 1.0),
     (1, 6, 2, 257, 64, "bf16", 12, FIB, 0.75),
     (1, 4, 2, 150, 64, "bf16", 20, FIB, 1.1),
+    # several passes per group over 16 tiles: G = 8 (two passes of four), both offset
+    # kinds, and G = 3 (three passes of one)
+    (1, 8, 1, 1024, 64, "bf16", 8, FIB, 1.0),
+    (1, 8, 1, 1024, 64, "bf16", 8, FIB, 0.9),
+    (1, 9, 3, 1024, 64, "bf16", 8, FIB, 1.0),
 ]
 
 
