@@ -12,6 +12,12 @@
 //   dL/dw  = tau dS_e <q_i, k[r1] - k[r0]> + p_e <dO_i, v[r1] - v[r0]>  (rung entries)
 //   dalpha = sum_{b,h,i,rungs} f_k dL/dw
 // The row -1 (reached only when w == 0) is a zero vector.
+// dalpha is a sum with heavy cancellation (its magnitude is a small fraction of the
+// sum of its terms' magnitudes), so it does not take Delta from the stored o (rounded
+// to the storage type) but from the entries themselves, Delta_i = sum_e p_e dP_e (the
+// same quantity, since o_i = sum_e p_e vhat_e): per query it accumulates
+// Xa = sum f p dP <q, k[r1]-k[r0]>, Xb = sum f p <dO, v[r1]-v[r0]>, Y = sum f p <q, k[r1]-k[r0]>
+// and the entries' sum of p dP, and adds tau (Xa - Delta Y) + Xb.
 //
 // Because every rung offset is shared, the queries that read key row j are again a
 // fixed set of shifted positions: j .. j+W through the window, and j + floor(d_k)
@@ -62,6 +68,7 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(
 #pragma unroll
         for (int c = 0; c < VN; ++c) acc[c] = 0.f;
 
+        double xa = 0.0, xb = 0.0, y = 0.0, dsum = 0.0;  // dalpha parts, Delta from the entries
         const int wmax = min(W, i);
         for (int d = 0; d <= wmax; ++d) {
             Vec<S>::load(K + (i - d) * sk + col, kv);
@@ -70,6 +77,7 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(
             const float dP = group_sum<LPQ>(dot<VN>(gv, vv));
             const float p = exp2f(s * sl2 - lse2);
             const float c = tau * p * (dP - delta);
+            dsum += (double)p * (double)dP;
 #pragma unroll
             for (int x = 0; x < VN; ++x) acc[x] = fmaf(c, kv[x], acc[x]);
         }
@@ -101,9 +109,13 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(
             const float c1 = c * w;
 #pragma unroll
             for (int x = 0; x < VN; ++x) acc[x] = fmaf(c0, kv[x], fmaf(c1, k1[x], acc[x]));
-            const float gw = c * (s1 - s0) + p * (dP1 - dP0);
-            dal += (double)rt.f[r] * (double)gw;
+            const double fp = (double)rt.f[r] * (double)p;
+            xa += fp * (double)dP * (double)(s1 - s0);
+            xb += fp * (double)(dP1 - dP0);
+            y += fp * (double)(s1 - s0);
+            dsum += (double)p * (double)dP;
         }
+        dal = (double)tau * (xa - dsum * y) + xb;
         if (bad) {
 #pragma unroll
             for (int x = 0; x < VN; ++x) acc[x] = NAN;

@@ -12,7 +12,9 @@
 //          interpolation the rows of short rungs come from the staged rows, which
 //          then reach 32 rows below the tile),
 //          dq += tau dS ((1-w) k[r0] + w k[r1]) on the VALU,
-//          dalpha partial += f (tau dS <q, k[r1]-k[r0]> + p <dO, v[r1]-v[r0]>);
+//          dalpha partial += f (tau dS <q, k[r1]-k[r0]> + p <dO, v[r1]-v[r0]>), where
+//          the dS of this sum uses Delta_i = sum_e p_e dP_e over the query's entries
+//          rather than the one from the stored (bf16) o;
 //   writes dq, Delta_i = <dO_i, o_i>, one float64 dalpha partial per workgroup
 //   (each query's terms in float32, then float64 across queries) and, for every rung
 //   entry, the pair (tau dS, p) as bfloat16 (the rung terms, staged in LDS during the
@@ -144,6 +146,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 
     // band (MFMA layout): keys [t0-16, t0+16)
     uint32_t cw[4];
+    float pdp = 0.f;  // this lane's part of the band's sum of p dP (Delta from the entries)
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
         const int sr = kLeadQ - 16 + 16 * wv + 16 * b + nm;  // staged row
@@ -156,6 +159,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
             const bool ok = key >= 0 && key <= im && im - key <= W;
             const float p = ok ? fast_exp2(s[e] * sl2 - lse2_m) : 0.f;
             c[e] = tau * p * (dp[e] - delta_m);
+            pdp = fmaf(p, dp[e], pdp);
         }
         cw[2 * b] = pack_bf16(c[0], c[1]);
         cw[2 * b + 1] = pack_bf16(c[2], c[3]);
@@ -166,9 +170,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     for (int c = 0; c < 4; ++c)
         acc.c[c] = mfma(dma_operand_t(kr, c, nm, kLeadQ - 16 + 16 * wv, gm), C, f32x4{0.f, 0.f, 0.f, 0.f});
     acc_to_quad(acc, lane);
+    // the query's band sum of p dP, on each of its four quad lanes
+    float dsum = to_quad(sum4(pdp), lane);
 
-    // rungs (quad layout), two batches in flight; r1 = -1 is the zero row
-    float dal_q = 0.f;  // this lane's dalpha terms (float32; summed in float64 below)
+    // rungs (quad layout), two batches in flight; r1 = -1 is the zero row.
+    // dalpha is a sum with heavy cancellation (|dalpha| is a small fraction of the sum
+    // of its terms' magnitudes), so its Delta is not the one from the stored o (rounded
+    // to bf16) but the entries' own Delta_i = sum_e p_e dP_e, known after the loop: the
+    // lane accumulates xa = sum f p dP ds, xb = sum f p dv and y = sum f p ds over its
+    // parts ds of <q, k[r1]-k[r0]> and dv of <dO, v[r1]-v[r0]>, and its dalpha terms are
+    // tau (xa - Delta y) + xb (float32 per lane; float64 across lanes below).
+    float xa = 0.f, xb = 0.f, y = 0.f;
     auto compute_rung = [&](int r, const Slice *x) {  // x = {k0, v0, k1, v1}
         const int d0 = rt.d0[r];
         const float w = rt.w[r];
@@ -196,8 +208,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         else
             acc_axpy_bf(acc, cc, x[0]);
         // dalpha: f (tau dS <q, k[r1] - k[r0]> + p <dO, v[r1] - v[r0]>) from this lane's
-        // parts; the wave and workgroup sums below add the four lanes of each query
-        dal_q += incl ? (float)rt.f[r] * (cc * (s1l - s0l) + p * (p1l - p0l)) : 0.f;
+        // parts (p = 0 for an excluded entry); the wave and workgroup sums below add the
+        // four lanes of each query
+        const float fp = (float)rt.f[r] * p, ds = s1l - s0l;
+        xa = fmaf(fp * dP, ds, xa);
+        xb = fmaf(fp, p1l - p0l, xb);
+        y = fmaf(fp, ds, y);
+        dsum = fmaf(p, dP, dsum);
     };
 #pragma unroll
     for (int rb = 0; rb < kMaxRungs; rb += 2) {
@@ -224,6 +241,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         store_acc(dq + head_at<STRIDED, kD>(lay.dq, bh, hd.H, T) + (size_t)i * stdq, gq, acc, bad ? NAN : 1.f);
         if (gq == 0) delta_out[(size_t)bh * T + i] = bad ? NAN : delta;
     }
+    float dal_q = fmaf(tau, fmaf(-dsum, y, xa), xb);
     if (bad) dal_q = NAN;
     // workgroup dalpha partial: wave sums, then the four waves in order
     double dal = (double)dal_q;

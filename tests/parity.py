@@ -7,7 +7,8 @@ Tolerances (written out here, used by every parity test):
     1e-5 bound is unattainable for any float32 implementation);
   * bfloat16 storage with float32 arithmetic: max |x - x_ref| <= 2e-2 * max |x_ref|
     per tensor for o, dq, dk, dv; lse (a float32 output) within 1e-3 absolute;
-    |dalpha - ref| <= 2e-2 * max(1, A).
+    |dalpha - ref| <= 2e-2 * max(1, |ref|) (relative to dalpha itself: a zero or
+    sign-flipped dalpha fails it).
 The oracle reads the very same rounded inputs, upcast to float64.
 """
 from __future__ import annotations
@@ -83,8 +84,10 @@ def compare(got, ref, dtype, label=""):
         assert err <= bound, f"{label} {name}: max abs err {err:.3e} > bound {bound:.3e}"
     if "dalpha" in got:
         err = abs(got["dalpha"] - ref["dalpha"])
-        A = max(1.0, ref["l1"])
-        bound = (TOL_FP32 if dtype == "fp32" else TOL_BF16_REL) * A
+        if dtype == "fp32":
+            bound = TOL_FP32 * max(1.0, ref["l1"])
+        else:
+            bound = TOL_BF16_REL * max(1.0, abs(ref["dalpha"]))
         report["dalpha"] = (err, bound)
         assert np.isfinite(got["dalpha"]), f"{label} dalpha not finite"
         assert err <= bound, f"{label} dalpha: {got['dalpha']} vs {ref['dalpha']} (err {err:.3e} > {bound:.3e})"

@@ -49,6 +49,17 @@ SMALL = [
     # a partial one (8 positions)
     (1, 5, 4096, 64, "bf16", 8, FIB, 1.0),
     (1, 5, 4096, 64, "bf16", 8, FIB, 0.9),
+    # the matrix-core kernels' window limit: their band tile reaches exactly 16 keys
+    # back (W = 16), one below the first W the generic kernels take (W = 17); W = 0 with
+    # alpha = 0.9 has a rung at d = 0.9 whose row r0 is the query itself
+    (1, 2, 300, 64, "bf16", 16, FIB, 1.0),
+    (1, 2, 300, 64, "bf16", 16, FIB, 0.7310586),
+    (2, 1, 333, 64, "bf16", 13, FIB, 1.0),
+    (2, 1, 333, 64, "bf16", 13, POW2, 1.3),
+    (1, 2, 257, 64, "bf16", 0, FIB, 1.0),
+    (1, 2, 257, 64, "bf16", 0, FIB, 0.9),
+    (1, 2, 290, 64, "bf16", 17, FIB, 1.0),
+    (1, 2, 290, 64, "bf16", 17, FIB, 1.2),
 ]
 
 
@@ -59,7 +70,10 @@ def test_small_parity(B, H, T, D, dtype, W, base, alpha):
     print(f"small case {idx}: B{B} H{H} T{T} D{D} {dtype} W{W} K{len(base)} alpha={alpha}", flush=True)
     got = gpu_run(x["q"], x["k"], x["v"], x["dO"], W, base, alpha)
     ref = oracle_run(x["q"], x["k"], x["v"], x["dO"], W, base, alpha)
-    compare(got, ref, dtype, f"case {idx}")
+    rep = compare(got, ref, dtype, f"case {idx}")
+    if "dalpha" in ref:
+        print(f"dalpha {got['dalpha']:.6g} ref {ref['dalpha']:.6g} L1 {ref['l1']:.4g}", flush=True)
+    print(rep, flush=True)
 
 
 def _full_calls(wl):
@@ -81,6 +95,8 @@ def test_full_size_parity(wl, ci):
     got = gpu_run(x["q"], x["k"], x["v"], x["dO"], call.W, call.base, call.alpha, backward=wl.backward)
     ref = oracle_run(x["q"], x["k"], x["v"], x["dO"], call.W, call.base, call.alpha, backward=wl.backward)
     rep = compare(got, ref, wl.dtype, f"{wl.name} call {ci}")
+    if "dalpha" in ref:
+        print(f"dalpha {got['dalpha']:.6g} ref {ref['dalpha']:.6g} L1 {ref['l1']:.4g}", flush=True)
     print(rep, flush=True)
 
 

@@ -83,8 +83,10 @@ def dense_autograd(q, k, v, dO, W, base, alpha):
     """Forward as one softmax over T window columns plus one column per rung, where the
     rung's key and value are (1 - w) S0 K + w S1 K with constant shift matrices S0, S1
     (S1 has no entry for row -1: zero padding).  w = w32 + (a - alpha) * f so that
-    autograd sees dw/da = f while the value is the float32 fraction.  Returns
-    (o, lse, dq, dk, dv, dalpha)."""
+    autograd sees dw/da = f while the value is the float32 fraction.  Each rung's weight
+    also carries a zero per-query offset leaf, whose gradient is the per-entry
+    dL/dw; the L1 mass sum |f dL/dw| is summed from those.  Returns
+    (o, lse, dq, dk, dv, dalpha, l1)."""
     B, H, T, D = q.shape
     tau = 1.0 / math.sqrt(D)
     Q = torch.tensor(q, dtype=torch.float64, requires_grad=True)
@@ -107,15 +109,19 @@ def dense_autograd(q, k, v, dO, W, base, alpha):
     S = S.masked_fill(~band, float("-inf"))
     cols = [S]
     vals = []
+    offs = []  # per-(b, h, query) weight offsets, one leaf per rung
     for f, d in rungs:
         d0 = math.floor(d)
         w32 = d - d0
-        w = w32 + (a - float(np.float32(alpha))) * f
+        wq = torch.zeros((B, H, T, 1), dtype=torch.float64, requires_grad=True)
+        offs.append((f, wq))
+        w = w32 + (a - float(np.float32(alpha))) * f + wq
         S0 = (rel == d0).to(torch.float64)
         S1 = (rel == d0 + 1).to(torch.float64)
-        G = (1 - w) * S0 + w * S1
-        Kk = G @ Kt
-        Vk = G @ V
+        K0, K1 = S0 @ Kt, S1 @ Kt
+        V0, V1 = S0 @ V, S1 @ V
+        Kk = (1 - w) * K0 + w * K1
+        Vk = (1 - w) * V0 + w * V1
         logit = tau * (Q * Kk).sum(-1, keepdim=True)
         incl = torch.tensor([d <= i for i in range(T)])[:, None]
         logit = logit.masked_fill(~incl, float("-inf"))
@@ -129,8 +135,9 @@ def dense_autograd(q, k, v, dO, W, base, alpha):
         o = o + P[..., T + j:T + j + 1] * Vk
     L = (o * torch.tensor(dO)).sum()
     L.backward()
+    l1 = sum(float((f * wq.grad).abs().sum()) for f, wq in offs)
     return (o.detach().numpy(), lse.detach().numpy(), Q.grad.numpy(), Kleaf.grad.numpy(),
-            Vleaf.grad.numpy(), float(a.grad))
+            Vleaf.grad.numpy(), float(a.grad), l1)
 
 
 # ---------------------------------------------------------------------------
@@ -164,13 +171,16 @@ def test_forward_backward_match_autograd(T, D, W, base, alpha):
     q, k, v, dO = (rand((2, 1, T, D), s) for s in (11, 12, 13, 14))
     o, lse = oracle.forward(q, k, v, W, base, alpha)
     dq, dk, dv, da, l1 = oracle.backward(q, k, v, dO, W, base, alpha)
-    oa, la, dqa, dka, dva, daa = dense_autograd(q, k, v, dO, W, base, alpha)
+    oa, la, dqa, dka, dva, daa, l1a = dense_autograd(q, k, v, dO, W, base, alpha)
     np.testing.assert_allclose(o, oa, atol=1e-12)
     np.testing.assert_allclose(lse, la, atol=1e-12)
     np.testing.assert_allclose(dq, dqa, atol=1e-11)
     np.testing.assert_allclose(dk, dka, atol=1e-11)
     np.testing.assert_allclose(dv, dva, atol=1e-11)
     assert abs(da - daa) <= 1e-10 * max(1.0, l1)
+    # the L1 mass that scales the float32 dalpha tolerance, from autograd's per-entry
+    # gradients (zero when no rung is included anywhere)
+    assert abs(l1 - l1a) <= 1e-10 * max(1.0, l1a)
 
 
 @pytest.mark.parametrize("Hkv,case", [(1, 1), (2, 3), (2, 5)])
@@ -182,7 +192,7 @@ def test_grouped_heads_match_autograd(Hkv, case):
     k, v = rand((2, Hkv, T, D), 22), rand((2, Hkv, T, D), 23)
     o, lse = oracle.forward(q, k, v, W, base, alpha)
     dq, dk, dv, da, l1 = oracle.backward(q, k, v, dO, W, base, alpha)
-    oa, la, dqa, dka, dva, daa = dense_autograd(q, k, v, dO, W, base, alpha)
+    oa, la, dqa, dka, dva, daa, l1a = dense_autograd(q, k, v, dO, W, base, alpha)
     assert dk.shape == k.shape and dv.shape == v.shape
     np.testing.assert_allclose(o, oa, atol=1e-12)
     np.testing.assert_allclose(lse, la, atol=1e-12)
@@ -190,6 +200,7 @@ def test_grouped_heads_match_autograd(Hkv, case):
     np.testing.assert_allclose(dk, dka, atol=1e-11)
     np.testing.assert_allclose(dv, dva, atol=1e-11)
     assert abs(da - daa) <= 1e-10 * max(1.0, l1)
+    assert abs(l1 - l1a) <= 1e-10 * max(1.0, l1a)
 
 
 def test_grouped_heads_equal_repeated_heads():
