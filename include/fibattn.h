@@ -56,7 +56,8 @@ typedef enum {
     FIBATTN_ERR_INVALID_ARG = 1,  /* null/misaligned pointer, bad size, bad base table, bad alpha */
     FIBATTN_ERR_UNSUPPORTED = 2,  /* valid but not implemented: d_head, W or K beyond the limits */
     FIBATTN_ERR_WORKSPACE = 3,    /* backward workspace missing or too small */
-    FIBATTN_ERR_HIP = 4           /* a kernel launch failed (hipGetLastError) */
+    FIBATTN_ERR_HIP = 4,          /* a kernel launch failed (hipGetLastError) */
+    FIBATTN_ERR_SCRATCH = 5       /* the problem needs more than FIBATTN_SCRATCH_BYTES of scratch */
 } fibattn_status_t;
 
 typedef enum {
@@ -248,6 +249,32 @@ fibattn_status_t fibattn_rope(const void *x, void *y, int B, int H, int T, int d
 fibattn_status_t fibattn_rope_qk(const void *q, const void *k, void *q_out, void *k_out,
                                  int B, int H, int T, int d_head, float rope_base,
                                  fibattn_dtype_t dtype, hipStream_t stream);
+
+/*
+ * Backward that allocates nothing and takes no workspace: for callers that cannot
+ * allocate device memory during the call (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Arguments, semantics and results are those
+ * of fibattn_backward_gqa (bitwise the same outputs, same kernels), without
+ * `workspace` / `workspace_bytes`: the scratch (Delta, the dalpha partials and the
+ * per-(query, rung) terms) lives in a static device array of FIBATTN_SCRATCH_BYTES
+ * that the library holds on every GPU it runs on until the process ends.  Its address
+ * on a device is looked up once (on the first call whose stream is on that device).
+ *   Returns FIBATTN_ERR_SCRATCH, enqueueing nothing, when
+ *   fibattn_backward_workspace_bytes(B, H, T, d_head, W, K) exceeds
+ *   FIBATTN_SCRATCH_BYTES (e.g. B*H*T above ~1e6 query-heads at K = 15, d_head 64).
+ *   Every call on one GPU shares that GPU's array and leaves its contents behind:
+ *   calls that overlap on one GPU (concurrent streams, or host threads whose calls'
+ *   kernels can run at the same time) race on it and must be serialised by the caller.
+ *   Nothing in the array needs to start at zero.
+ */
+#define FIBATTN_SCRATCH_BYTES ((size_t)64 << 20)
+
+fibattn_status_t fibattn_backward_noalloc(const void *q, const void *k, const void *v,
+                                          const void *o, const float *lse, const void *dO,
+                                          void *dq, void *dk, void *dv, float *dalpha,
+                                          int B, int H, int H_kv, int T, int d_head, int W,
+                                          const int32_t *base, int K, float alpha, float rope_base,
+                                          fibattn_dtype_t dtype, hipStream_t stream);
 
 /* Human-readable name of a status code (static storage). */
 const char *fibattn_status_string(fibattn_status_t status);

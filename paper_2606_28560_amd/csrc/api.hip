@@ -5,6 +5,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <vector>
 
 #include "../../include/fibattn.h"
@@ -80,6 +81,36 @@ struct Timing {
     std::vector<hipEvent_t> ev;  // start/stop pairs
     int used = 0;
 } g_timing;
+
+// ---- static scratch of the allocation-free backward -------------------------
+// One copy per GPU, created with the library's code object on that device.  Host code
+// never uses this name as an address (on the host it is only a stand-in): kernels and
+// copies get the device address resolved by scratch_on().
+static __device__ __align__(256) unsigned char scratch[FIBATTN_SCRATCH_BYTES];
+
+std::mutex g_scratch_mu;
+std::vector<void *> g_scratch;  // per device ordinal; nullptr until resolved
+
+// Device address of `dev`'s copy of the scratch array, looked up once per device with
+// that device current (the caller's current device is restored).  nullptr on failure.
+void *scratch_on(int dev) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (dev < 0) return nullptr;
+    if ((size_t)dev < g_scratch.size() && g_scratch[dev]) return g_scratch[dev];
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return nullptr;
+    if (cur != dev && hipSetDevice(dev) != hipSuccess) return nullptr;
+    void *ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !ptr) {
+        (void)hipGetLastError();  // leave no sticky error for the caller's next call
+        return nullptr;
+    }
+    if ((size_t)dev >= g_scratch.size()) g_scratch.resize((size_t)dev + 1, nullptr);
+    g_scratch[dev] = ptr;
+    return ptr;
+}
 
 }  // namespace
 
@@ -260,6 +291,30 @@ fibattn_status_t fibattn_backward(const void *q, const void *k, const void *v, c
                                 B, H, H, T, d_head, W, base, K, alpha, rope_base, dtype, stream);
 }
 
+fibattn_status_t fibattn_backward_noalloc(const void *q, const void *k, const void *v,
+                                          const void *o, const float *lse, const void *dO,
+                                          void *dq, void *dk, void *dv, float *dalpha, int B, int H,
+                                          int H_kv, int T, int d_head, int W, const int32_t *base,
+                                          int K, float alpha, float rope_base, fibattn_dtype_t dtype,
+                                          hipStream_t stream) {
+    // the size checks come first, so a problem too large for the scratch enqueues nothing
+    fibattn_status_t st = check_common(B, H, T, d_head, W, K, dtype);
+    if (st != FIBATTN_OK) return st;
+    if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
+    const size_t need = workspace_layout(B, H, T, d_head, W, K).total;
+    if (need > FIBATTN_SCRATCH_BYTES) return FIBATTN_ERR_SCRATCH;
+    int dev = -1;
+    if (stream ? hipStreamGetDevice(stream, &dev) != hipSuccess : hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return FIBATTN_ERR_HIP;
+    }
+    void *ws = scratch_on(dev);
+    if (!ws) return FIBATTN_ERR_HIP;
+    return backward_impl(q, k, v, o, lse, dO, dq, dk, dv, dalpha, ws, FIBATTN_SCRATCH_BYTES,
+                         packed_layouts(H, H_kv, T, d_head), B, H, H_kv, T, d_head, W, base, K, alpha,
+                         rope_base, dtype, stream);
+}
+
 // ---- device-resident alpha -------------------------------------------------------
 
 size_t fibattn_device_table_bytes(void) { return align256(sizeof(RungTable)); }
@@ -374,6 +429,9 @@ const char *fibattn_status_string(fibattn_status_t s) {
         case FIBATTN_ERR_UNSUPPORTED: return "unsupported size or configuration";
         case FIBATTN_ERR_WORKSPACE: return "workspace missing or too small";
         case FIBATTN_ERR_HIP: return "HIP launch error";
+        case FIBATTN_ERR_SCRATCH:
+            return "problem needs more scratch than the allocation-free backward's static buffer "
+                   "(FIBATTN_SCRATCH_BYTES = 64 MiB)";
     }
     return "unknown status";
 }

@@ -25,7 +25,9 @@ EXPORTED = ("fibattn_rung_table", "fibattn_forward", "fibattn_backward_workspace
             "fibattn_forward_strided", "fibattn_backward_strided",
             "fibattn_device_table_bytes", "fibattn_device_table", "fibattn_forward_dt",
             "fibattn_backward_dt", "fibattn_alpha_from_theta", "fibattn_dtheta", "fibattn_rope",
-            "fibattn_rope_qk", "fibattn_status_string", "fibattn_timing_begin", "fibattn_timing_end")
+            "fibattn_rope_qk", "fibattn_status_string", "fibattn_timing_begin", "fibattn_timing_end",
+            "fibattn_backward_noalloc")
+SCRATCH_BYTES = 64 << 20  # FIBATTN_SCRATCH_BYTES: the allocation-free backward's static scratch
 
 
 class FibattnError(RuntimeError):
@@ -85,6 +87,9 @@ def lib():
     L.fibattn_rope.restype = i
     L.fibattn_rope_qk.argtypes = [vp, vp, vp, vp, i, i, i, i, f, i, vp]
     L.fibattn_rope_qk.restype = i
+    L.fibattn_backward_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                           i, i, i, i, i, i, ip, i, f, f, i, vp]
+    L.fibattn_backward_noalloc.restype = i
     L.fibattn_status_string.argtypes = [i]
     L.fibattn_status_string.restype = ctypes.c_char_p
     L.fibattn_timing_begin.argtypes = [i, i]
@@ -250,6 +255,32 @@ def fibattn_backward(q, k, v, o, lse, dO, W: int, base, alpha: float, *, dq=None
     else:
         st = lib().fibattn_backward_gqa(*ptrs, B, H, Hkv, *tail)
         _check("fibattn_backward_gqa", st)
+    return dq, dk, dv, dalpha
+
+
+def fibattn_backward_noalloc(q, k, v, o, lse, dO, W: int, base, alpha: float, *, dq, dk, dv, dalpha,
+                             rope_base: float = 0.0, stream=None):
+    """As fibattn_backward on packed tensors, with the library's static device scratch
+    instead of a workspace: neither this function nor the library allocates.  The
+    caller passes every output (dq, dk, dv shaped like q, k, v; dalpha one float32)."""
+    import torch
+
+    B, H, T, D = q.shape
+    Hkv = _kv_heads(q, k)
+    kvs = (B, Hkv, T, D)
+    for n_, t, sh in (("q", q, q.shape), ("k", k, kvs), ("v", v, kvs), ("o", o, q.shape),
+                      ("dO", dO, q.shape), ("dq", dq, q.shape), ("dk", dk, kvs), ("dv", dv, kvs)):
+        _check_tensor(n_, t, sh, q.dtype)
+    _check_tensor("lse", lse, (B, H, T), torch.float32)
+    if dalpha.dtype != torch.float32 or dalpha.numel() < 1 or not dalpha.is_cuda:
+        raise ValueError("dalpha: a float32 device tensor")
+    b, bp = _base_array(base)
+    st = lib().fibattn_backward_noalloc(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                        lse.data_ptr(), dO.data_ptr(), dq.data_ptr(), dk.data_ptr(),
+                                        dv.data_ptr(), dalpha.data_ptr(), B, H, Hkv, T, D, int(W), bp,
+                                        b.size, ctypes.c_float(alpha), ctypes.c_float(rope_base),
+                                        _dtype_code(q), _stream(stream))
+    _check("fibattn_backward_noalloc", st)
     return dq, dk, dv, dalpha
 
 

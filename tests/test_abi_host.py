@@ -189,3 +189,17 @@ def test_strided_layouts_are_checked_before_any_launch():
     assert bwd(None) == 1
     assert bwd(lay(*([good] * 7 + [(0, 0, 12)]))) == 1                   # dv rows misaligned
     assert bwd(lay(*([good] * 5 + [(0, -8, 64)] + [good] * 2))) == 1     # dq head stride negative
+
+
+def test_noalloc_backward_refuses_problems_beyond_its_scratch_without_gpu():
+    # the size check comes before any pointer is read or any HIP call is made
+    L = F.lib()
+    b = (ctypes.c_int32 * 15)(*schedules.FIB15)
+    one, zero = ctypes.c_float(1.0), ctypes.c_float(0.0)
+    need = F.fibattn_backward_workspace_bytes(32, 8, 16384, 64, 8, 15)
+    assert need > F.SCRATCH_BYTES
+    st = L.fibattn_backward_noalloc(*([16] * 10), 32, 8, 8, 16384, 64, 8, b, 15, one, zero, 1, None)
+    assert st == 5 and "scratch" in F.status_string(st)
+    # bad sizes are refused as by the other entry points
+    assert L.fibattn_backward_noalloc(*([16] * 10), 0, 8, 8, 1024, 64, 8, b, 15, one, zero, 1, None) == 1
+    assert L.fibattn_backward_noalloc(*([16] * 10), 1, 8, 3, 1024, 64, 8, b, 15, one, zero, 1, None) == 1
