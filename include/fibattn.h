@@ -57,12 +57,20 @@ typedef enum {
     FIBATTN_ERR_UNSUPPORTED = 2,  /* valid but not implemented: d_head, W or K beyond the limits */
     FIBATTN_ERR_WORKSPACE = 3,    /* backward workspace missing or too small */
     FIBATTN_ERR_HIP = 4,          /* a kernel launch failed (hipGetLastError) */
-    FIBATTN_ERR_SCRATCH = 5       /* the problem needs more than FIBATTN_SCRATCH_BYTES of scratch */
+    FIBATTN_ERR_SCRATCH = 5,      /* the problem needs more than FIBATTN_SCRATCH_BYTES of scratch */
+    /* not statuses: they give the type the range of int, so that any int a caller
+     * passes (fibattn_status_string) is a valid value of it */
+    FIBATTN_STATUS_MIN_ = -0x7fffffff - 1,
+    FIBATTN_STATUS_MAX_ = 0x7fffffff
 } fibattn_status_t;
 
 typedef enum {
     FIBATTN_FP32 = 0,             /* float32 storage and arithmetic */
-    FIBATTN_BF16 = 1              /* bfloat16 storage, float32 arithmetic, one rounding per output */
+    FIBATTN_BF16 = 1,             /* bfloat16 storage, float32 arithmetic, one rounding per output */
+    /* not dtypes: any int passed as a dtype is a valid value of the type, and every
+     * value other than the two above is refused with FIBATTN_ERR_INVALID_ARG */
+    FIBATTN_DTYPE_MIN_ = -0x7fffffff - 1,
+    FIBATTN_DTYPE_MAX_ = 0x7fffffff
 } fibattn_dtype_t;
 
 #define FIBATTN_MAX_RUNGS 32      /* K <= 32 */
@@ -196,7 +204,8 @@ fibattn_status_t fibattn_backward_strided(const void *q, const void *k, const vo
  * fibattn_device_table_bytes() bytes, 16-byte aligned.  The table is read by
  * fibattn_forward_dt / fibattn_backward_dt, which take it in place of (base, K, alpha)
  * and otherwise behave as fibattn_forward_gqa / fibattn_backward_gqa; W must be the
- * one the table was built with, and the backward's workspace is
+ * one the table was built with (the table records it: called with another W, every
+ * output is NaN, as for a bad alpha), and the backward's workspace is
  * fibattn_backward_workspace_bytes(B, H, T, d_head, W, 0).  A table may hold any weights, so these calls always
  * run the interpolating kernels.  An alpha that is not finite and positive yields a
  * table that makes every output (o, lse, dq, dk, dv, dalpha) NaN.
@@ -280,9 +289,10 @@ fibattn_status_t fibattn_backward_noalloc(const void *q, const void *k, const vo
 const char *fibattn_status_string(fibattn_status_t status);
 
 /*
- * Kernel timing (instrumentation for benchmarks; not thread-safe).
+ * Kernel timing (instrumentation for benchmarks).  The state is per host thread:
  * fibattn_timing_begin(id, capacity) makes the library launch each of the next
- * `capacity` launches of kernel `id` with a HIP event pair that takes the dispatch's
+ * `capacity` launches of kernel `id` made by the calling thread with a HIP event
+ * pair that takes the dispatch's
  * own start and end timestamps on the launch stream (0 rope, 1 forward, 2 backward
  * dq+dalpha, 3 backward dk/dv, 4 dalpha reduce, 5 device-alpha kernels).
  * fibattn_timing_end(&avg_ms, &count) synchronises on the last event, returns

@@ -75,12 +75,15 @@ fibattn_status_t check_layout(const fibattn_layout_t &l, int T, int d_head, fiba
 }
 
 // ---- kernel timing -------------------------------------------------------
+// Per host thread: only launches made by the thread that began timing are timed, so
+// calls from other threads never touch this state.
 struct Timing {
     int id = -1;
     int capacity = 0;
     std::vector<hipEvent_t> ev;  // start/stop pairs
     int used = 0;
-} g_timing;
+};
+thread_local Timing g_timing;
 
 // ---- static scratch of the allocation-free backward -------------------------
 // One copy per GPU, created with the library's code object on that device.  Host code
@@ -432,6 +435,7 @@ const char *fibattn_status_string(fibattn_status_t s) {
         case FIBATTN_ERR_SCRATCH:
             return "problem needs more scratch than the allocation-free backward's static buffer "
                    "(FIBATTN_SCRATCH_BYTES = 64 MiB)";
+        default: break;
     }
     return "unknown status";
 }

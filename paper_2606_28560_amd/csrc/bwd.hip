@@ -39,7 +39,7 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(
     S *__restrict__ dq, float *__restrict__ delta_out, double *__restrict__ partials, int T,
     int W, RungTable rt_arg, const RungTable *__restrict__ rtp, float tau, Heads hd, Layouts lay) {
     const RungTable &rt = DEV ? *rtp : rt_arg;
-    const bool bad = DEV && rt.n < 0;  // a device alpha that is not finite and positive
+    const bool bad = DEV && table_unusable(rt, W);  // bad device alpha, or another W
     constexpr int VN = Vec<S>::N;
     constexpr int LPQ = D / VN;
     constexpr int QPB = 256 / LPQ;
@@ -239,7 +239,7 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(
             }
         }
     }
-    if (DEV && rt.n < 0) {  // a device alpha that is not finite and positive
+    if (DEV && table_unusable(rt, W)) {  // bad device alpha, or another W
 #pragma unroll
         for (int x = 0; x < VN; ++x) { adk[x] = NAN; adv[x] = NAN; }
     }

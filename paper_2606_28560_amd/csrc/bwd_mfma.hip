@@ -48,7 +48,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     RungTerms terms, int T, int W, RungTable rt_arg, const RungTable *__restrict__ rtp, RopeFreq rf,
     float tau, int tiles, Heads hd, Layouts lay) {
     const RungTable &rt = DEV ? *rtp : rt_arg;
-    const bool bad = DEV && rt.n < 0;  // a device alpha that is not finite and positive
+    const bool bad = DEV && table_unusable(rt, W);  // bad device alpha, or another W
     // staged K, V rows [T0 - kLeadQ, T0 + 64): the band and, interpolating, the short rungs
     constexpr int kLeadQ = INTERP ? 32 : 16;
     constexpr int kStage = kBwdB + kLeadQ;
@@ -566,7 +566,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     if (hs == 0) {
         if (rf.on) acc_rope_t(adk, j_key, sfreq + 8 * gq);  // gradient w.r.t. the unrotated k
         if (j_key < T) {
-            const float sc = DEV && rt.n < 0 ? NAN : 1.f;  // a device alpha not finite and positive
+            const float sc = DEV && table_unusable(rt, W) ? NAN : 1.f;  // bad device alpha, or another W
             store_acc(dk + head_at<STRIDED, kD>(lay.dk, bk, hd.kv_heads(), T) + (size_t)j_key * stdk, gq, adk, sc);
             store_acc(dv + head_at<STRIDED, kD>(lay.dv, bk, hd.kv_heads(), T) + (size_t)j_key * stdv, gq, adv, sc);
         }

@@ -11,15 +11,23 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
 // Rung table: the offsets every query of a launch shares (floor of the distance,
-// blend weight, base value), increasing d.  Passed by value in the kernel arguments,
-// or built on the device from a device-resident alpha (rung_table_fill).  n < 0 marks
-// a table built from an alpha that is not finite and positive: kernels then write NaN.
+// blend weight, base value), increasing d, for the window W it was built with.  Passed
+// by value in the kernel arguments, or built on the device from a device-resident alpha
+// (rung_table_fill).  n < 0 marks a table built from an alpha that is not finite and
+// positive; kernels reading a device table write NaN for such a table and for one
+// built with another W (table_unusable).
 struct RungTable {
     int n;
+    int W;
     int d0[kMaxRungs];
     float w[kMaxRungs];
     int f[kMaxRungs];
 };
+
+// A device-built table that must not be used for a launch with window W: its alpha
+// was not finite and positive, or it was built for another window (its in-window rule
+// then dropped or kept the wrong rungs).
+__host__ __device__ inline bool table_unusable(const RungTable &rt, int W) { return rt.n < 0 || rt.W != W; }
 
 // A validated base table (strictly increasing, >= 1, K <= kMaxRungs) by value.
 struct BaseTable {
@@ -35,6 +43,7 @@ struct BaseTable {
 __host__ __device__ inline bool rung_table_fill(float alpha, const BaseTable &b, int W, RungTable *rt) {
     for (int a = 0; a < kMaxRungs; ++a) { rt->d0[a] = 0; rt->w[a] = 0.f; rt->f[a] = 0; }
     rt->n = -1;
+    rt->W = W;
     if (!(alpha > 0.f) || !(alpha < INFINITY)) return false;
     int n = 0;
     float last = -1.f;

@@ -102,7 +102,7 @@ __global__ __launch_bounds__(256) void fwd_kernel(const S *__restrict__ q, const
                 for (int c = 0; c < VN; ++c) acc[c] = fmaf(p1, vv[c], acc[c]);
             }
         }
-        const bool bad = DEV && rt.n < 0;  // a device alpha that is not finite and positive
+        const bool bad = DEV && table_unusable(rt, W);  // bad device alpha, or another W
         const float inv = bad ? NAN : 1.f / l;
 #pragma unroll
         for (int c = 0; c < VN; ++c) acc[c] *= inv;

@@ -218,7 +218,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     }
 
     if (i < T) {
-        const bool bad = DEV && rt.n < 0;  // a device alpha that is not finite and positive
+        const bool bad = DEV && table_unusable(rt, W);  // bad device alpha, or another W
         store_acc(o + head_at<STRIDED, kD>(lay.o, bh, hd.H, T) + (size_t)i * sto, gq, acc, bad ? NAN : 1.f / l);
         if (gq == 0) lse[(size_t)bh * T + i] = bad ? NAN : (m + log2f(l)) * kLn2;
     }

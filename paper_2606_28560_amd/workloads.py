@@ -1,7 +1,7 @@
 """The five synthetic workloads, shaped like the paper's 60M model.
 
 Section 3 "Model and training": d_model 512 = 8 heads x d_head 64, 16 layers,
-training length 1024, bf16 autocast, seed 42; Section 4.4 evaluates at 4x length
+training length 1024, bf16 autocast, seed 42; Section 4.5 ("Length extrapolation") evaluates at 4x length
 (T = 4096) with RoPE and the offsets unchanged.  The run matrix sweeps
 W in {6, 8, 10, 12} (Section 3 "Run matrix").  Inputs are i.i.d. N(0,1)
 (paper_2606_28560_amd.inputs); layers are independent calls with their own seeded

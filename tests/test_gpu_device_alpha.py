@@ -16,14 +16,14 @@ POW2 = schedules.POW2_11
 
 
 def _table_fields(buf):
-    """(n, d0, w, f) of a device table read back (the library's layout: int n, then
-    int d0[32], float w[32], int f[32])."""
+    """(n, d0, w, f, W) of a device table read back (the library's layout: int n, int W,
+    then int d0[32], float w[32], int f[32])."""
     raw = buf.cpu().numpy()
-    n = int(raw[:4].view(np.int32)[0])
-    d0 = raw[4:132].view(np.int32)
-    w = raw[132:260].view(np.float32)
-    f = raw[260:388].view(np.int32)
-    return n, d0, w, f
+    n, W = (int(x) for x in raw[:8].view(np.int32))
+    d0 = raw[8:136].view(np.int32)
+    w = raw[136:264].view(np.float32)
+    f = raw[264:392].view(np.int32)
+    return n, d0, w, f, W
 
 
 def _device_alphas():
@@ -40,17 +40,18 @@ def test_device_table_equals_host_table(base, W):
     for idx, a in enumerate(alphas):
         buf = F.fibattn_device_table(a_dev[idx:idx + 1], base, W)
         torch.cuda.synchronize()
-        n, d0, w, f = _table_fields(buf)
+        n, d0, w, f, tw = _table_fields(buf)
         host = F.fibattn_rung_table(float(a), base, W)
         assert n == len(host), (float(a), n, len(host))
+        assert tw == W
         for r, (hd0, hw, hf) in enumerate(host):
             assert (int(d0[r]), float(w[r]), int(f[r])) == (hd0, hw, hf), (float(a), r)
 
 
-def _dev_run(x, W, base, alpha, rope=0.0, poison=True):
+def _dev_run(x, W, base, alpha, rope=0.0, poison=True, table_W=None):
     Q, K, V, G = (x[n].cuda().contiguous() for n in ("q", "k", "v", "dO"))
     a_dev = torch.tensor([alpha], dtype=torch.float32, device="cuda")
-    table = F.fibattn_device_table(a_dev, base, W)
+    table = F.fibattn_device_table(a_dev, base, W if table_W is None else table_W)
     o = torch.empty_like(Q)
     lse = torch.empty(Q.shape[:3], device="cuda", dtype=torch.float32)
     dq, dk, dv = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
@@ -93,6 +94,18 @@ def test_device_alpha_parity(B, H, Hkv, T, D, dtype, W, base, alpha):
 def test_invalid_device_alpha_gives_nan(alpha):
     x = inputs.attention_inputs(1, 2, 100, 64, "bf16", 450, 0)
     got = _dev_run(x, 8, FIB, alpha, poison=False)
+    for name in ("o", "lse", "dq", "dk", "dv"):
+        assert np.all(np.isnan(got[name])), name
+    assert np.isnan(got["dalpha"])
+
+
+@pytest.mark.parametrize("dtype,D,table_W,W", [("bf16", 64, 8, 12), ("bf16", 64, 20, 17),
+                                               ("fp32", 32, 8, 6)])
+def test_table_used_with_another_window_gives_nan(dtype, D, table_W, W):
+    # a table records its W: with another W its in-window rule would have dropped or
+    # kept the wrong rungs, so every output is NaN (matrix-core and generic kernels)
+    x = inputs.attention_inputs(1, 2, 150, D, dtype, 451, 0)
+    got = _dev_run(x, W, FIB, 0.9, poison=False, table_W=table_W)
     for name in ("o", "lse", "dq", "dk", "dv"):
         assert np.all(np.isnan(got[name])), name
     assert np.isnan(got["dalpha"])
