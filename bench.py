@@ -38,7 +38,7 @@ def parse_args():
     p.add_argument("--steps", type=int, default=40)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="layer_60m_fixed_T1024")
-    p.add_argument("--sets", type=int, default=0, help="buffer sets to rotate (0: enough for > 320 MB)")
+    p.add_argument("--sets", type=int, default=0, help="buffer sets to rotate (0: more than twice the 256 MB last-level cache between reuses)")
     p.add_argument("--eager", action="store_true", help="launch eagerly instead of replaying graphs")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the oracle sample")
@@ -47,6 +47,8 @@ def parse_args():
     p.add_argument("--no-learned-alpha", action="store_true", help="skip the device-alpha figure")
     p.add_argument("--no-integer-offsets", action="store_true",
                    help="skip the continuous vs rounded-offset stagger figure")
+    p.add_argument("--no-configs", action="store_true",
+                   help="skip the per-workload 16-layer sequence figures")
     p.add_argument("--copy-probe-mb", type=int, default=0,
                    help="also run one plain device copy of this many MiB (counter calibration)")
     return p.parse_args()
@@ -129,9 +131,8 @@ class Step:
 
     def forward(self):
         F, c = self.F, self.call
-        if self.grouped:  # q and k have different head counts: one RoPE launch each
-            F.fibattn_rope(self.q, ROPE_BASE, out=self.qr)
-            F.fibattn_rope(self.k, ROPE_BASE, out=self.kr)
+        if self.grouped:  # q and k have different head counts (one launch for both)
+            F.fibattn_rope_qk_table(self.q, self.k, ROPE_BASE, q_out=self.qr, k_out=self.kr)
         else:
             F.fibattn_rope_qk(self.q, self.k, ROPE_BASE, q_out=self.qr, k_out=self.kr)
         F.fibattn_forward(self.qr, self.kr, self.v, c.W, c.base, c.alpha, o=self.o, lse=self.lse)
@@ -146,6 +147,26 @@ class Step:
     def __call__(self):
         self.forward()
         self.backward()
+
+
+MALL_BYTES = 256 * 2**20  # MI355X last-level (Infinity) cache
+
+
+def buffer_sets(per_set_bytes: int) -> int:
+    """Buffer sets to rotate so that more than twice the last-level cache lies between
+    two uses of one set (and at least 6 sets of the small ones)."""
+    n = -(-2 * MALL_BYTES // per_set_bytes) + 1
+    return max(n, 6 if per_set_bytes < 128 * 2**20 else 2)
+
+
+def step_bytes(wl, call, kv_heads=None) -> int:
+    """Device bytes of one Step's buffers (inputs, RoPE outputs, outputs, workspace)."""
+    s = 2 if wl.dtype == "bf16" else 4
+    hkv = kv_heads or wl.H
+    qrow, kvrow = wl.B * wl.H * wl.T * wl.D * s, wl.B * hkv * wl.T * wl.D * s
+    from paper_2606_28560_amd import fibattn as F
+    ws = F.fibattn_backward_workspace_bytes(wl.B, wl.H, wl.T, wl.D, call.W, len(call.base))
+    return 5 * qrow + 5 * kvrow + 4 * wl.B * wl.H * wl.T + ws
 
 
 def capture(fn):
@@ -221,6 +242,12 @@ def cpu_baseline(wl, call, target_s: float):
         if el >= target_s or reps >= 1000:
             break
     qh = reps * b * wl.H * wl.T
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
+    except OSError:
+        pass
     return {
         "value": qh / el,
         "unit": "queries·heads/s",
@@ -228,6 +255,9 @@ def cpu_baseline(wl, call, target_s: float):
         "kind": "oracle",
         "sample": f"{reps} x the full step (RoPE, forward, backward, R^T) of one layer "
                   f"({b}x{wl.H}x{wl.T} query-heads), {el:.1f} s",
+        "openmp_threads": oracle.num_threads(),
+        "nproc": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count(),
+        "cpu_model": model,
     }
 
 
@@ -237,7 +267,7 @@ def t4096_figure(steps: int, warmup: int, eager: bool):
 
     wl = workloads.workload("extrap_coprime16_T4096")
     call = wl.calls[1]
-    sets = [Step(wl, call, i) for i in range(3)]
+    sets = [Step(wl, call, i) for i in range(buffer_sets(step_bytes(wl, call)))]
     if eager:
         run = lambda i: sets[i % len(sets)]()  # noqa: E731
         fwd = lambda i: sets[i % len(sets)].forward()  # noqa: E731
@@ -273,7 +303,7 @@ def integer_offsets_figure(steps: int, warmup: int, eager: bool, layer: int = 3)
     out = {"workload": wl.name, "layer": layer, "alpha": float(call.alpha)}
     for tag, c in (("continuous", call), ("integer", rounded)):
         from paper_2606_28560_amd import fibattn as F
-        sets = [Step(wl, c, i) for i in range(3)]
+        sets = [Step(wl, c, i) for i in range(buffer_sets(step_bytes(wl, c)))]
         if eager:
             run = lambda i: attn_one(F, sets[i % len(sets)])  # noqa: E731
         else:
@@ -296,7 +326,8 @@ def gqa_figure(steps: int, warmup: int, eager: bool, kv_heads: int = 2):
 
     wl = workloads.workload("layer_60m_fixed_T1024")
     call = wl.calls[0]
-    sets = [Step(wl, call, i, kv_heads=kv_heads) for i in range(4)]
+    sets = [Step(wl, call, i, kv_heads=kv_heads)
+            for i in range(buffer_sets(step_bytes(wl, call, kv_heads)))]
     if eager:
         run = lambda i: sets[i % len(sets)]()  # noqa: E731
     else:
@@ -305,8 +336,8 @@ def gqa_figure(steps: int, warmup: int, eager: bool, kv_heads: int = 2):
     ms, _ = timed(run, steps, warmup)
     kt = {}
     for k in ("forward", "bwd_dq", "bwd_dkdv", "rope"):
-        kms, n = kernel_time(F, sets, k, steps, 2 if k == "rope" else 1)
-        kt[k] = round(kms * n / steps, 6)  # per step (RoPE: the q and the k launch)
+        kms, n = kernel_time(F, sets, k, steps, 1)
+        kt[k] = round(kms * n / steps, 6)  # per step
     qh = wl.queries_heads
     return {"workload": wl.name, "H": wl.H, "H_kv": kv_heads, "ms_per_step": ms,
             "value": qh / (ms * 1e-3), "kernels_ms_per_step": kt}
@@ -315,8 +346,8 @@ def gqa_figure(steps: int, warmup: int, eager: bool, kv_heads: int = 2):
 def learned_alpha_figure(steps: int, warmup: int, eager: bool, layer: int = 0):
     """Learned-alpha layer of the pow2/fib workload (B=32, H=8, T=1024, W=10, Fibonacci
     base, alpha = 0.5 + sigmoid(theta)) with theta resident on the device: theta ->
-    alpha -> rung table -> RoPE -> forward -> backward -> dtheta, against the same
-    layer with alpha passed from the host."""
+    alpha and rung table, in the RoPE launch -> forward -> backward with dtheta, against
+    the same layer with alpha passed from the host."""
     import torch
 
     from paper_2606_28560_amd import fibattn as F
@@ -325,7 +356,7 @@ def learned_alpha_figure(steps: int, warmup: int, eager: bool, layer: int = 0):
     wl = workloads.workload("pow2_fib_learned16_T1024")
     call = next(c for c in wl.calls if c.base_name == "fib15" and c.layer == layer)
     theta = torch.tensor(inputs.thetas(16, case=5)[layer:layer + 1], dtype=torch.float32, device="cuda")
-    sets = [Step(wl, call, i) for i in range(2)]
+    sets = [Step(wl, call, i) for i in range(buffer_sets(step_bytes(wl, call)))]
     dev = []
     for st in sets:
         st.theta, st.alpha = theta, torch.empty_like(theta)
@@ -337,13 +368,12 @@ def learned_alpha_figure(steps: int, warmup: int, eager: bool, layer: int = 0):
 
         def run_dev(st=st):
             c = st.call
-            F.fibattn_alpha_from_theta(st.theta, alpha=st.alpha)
-            F.fibattn_device_table(st.alpha, c.base, c.W, table=st.table)
-            F.fibattn_rope_qk(st.q, st.k, ROPE_BASE, q_out=st.qr, k_out=st.kr)
+            F.fibattn_rope_qk_table(st.q, st.k, ROPE_BASE, theta=st.theta, base=c.base, W=c.W, table=st.table,
+                                    alpha=st.alpha, q_out=st.qr, k_out=st.kr)
             F.fibattn_forward_dt(st.qr, st.kr, st.v, c.W, st.table, o=st.o, lse=st.lse)
             F.fibattn_backward_dt(st.qr, st.kr, st.v, st.o, st.lse, st.dO, c.W, st.table, dq=st.dq,
-                                  dk=st.dk, dv=st.dv, dalpha=st.da, workspace=st.ws, rope_base=ROPE_BASE)
-            F.fibattn_dtheta(st.theta, st.da, dtheta=st.dtheta)
+                                  dk=st.dk, dv=st.dv, dalpha=st.da, dtheta=st.dtheta, workspace=st.ws,
+                                  rope_base=ROPE_BASE)
         dev.append(run_dev)
     out = {"workload": wl.name, "layer": layer, "alpha": float(call.alpha)}
     for tag, fns in (("device_alpha", dev), ("host_alpha", sets)):
@@ -355,6 +385,92 @@ def learned_alpha_figure(steps: int, warmup: int, eager: bool, layer: int = 0):
         ms, _ = timed(run, steps, warmup)
         out[tag + "_ms"] = ms
         out[tag + "_value"] = wl.queries_heads / (ms * 1e-3)
+        kt = {}
+        for k in ("forward", "bwd_dq", "bwd_dkdv", "alpha"):
+            kms, n = kernel_time(F, fns, k, steps, 1)
+            if n:
+                kt[k] = round(kms, 6)
+        out[tag + "_kernels_ms"] = kt
+    return out
+
+
+class LayerSet:
+    """Buffers of one rotation set for attention-only layer calls (q, k post-RoPE)."""
+
+    def __init__(self, wl, call, set_index):
+        import torch
+
+        from paper_2606_28560_amd import inputs
+
+        x = inputs.attention_inputs(wl.B, wl.H, wl.T, wl.D, wl.dtype, wl.case, 2000 + set_index)
+        self.q, self.k, self.v, self.dO = (x[n].to("cuda") for n in ("q", "k", "v", "dO"))
+        del x
+        self.o, self.dq = torch.empty_like(self.q), torch.empty_like(self.q)
+        self.dk, self.dv = torch.empty_like(self.k), torch.empty_like(self.v)
+        self.lse = torch.empty((wl.B, wl.H, wl.T), device="cuda", dtype=torch.float32)
+        self.da = torch.empty(1, device="cuda", dtype=torch.float32)
+        from paper_2606_28560_amd import fibattn as F
+        need = max(F.fibattn_backward_workspace_bytes(wl.B, wl.H, wl.T, wl.D, c.W, len(c.base))
+                   for c in wl.calls)
+        self.ws = torch.empty(need, device="cuda", dtype=torch.uint8)
+
+
+def sequence_figure(F, wl, calls, sets, backward: bool, steps: int, warmup: int, eager: bool):
+    """One pass over `calls` (a 16-layer sequence), layer l on buffer set l % len(sets),
+    each layer an attention forward (and backward) on its own alpha and W."""
+    def run_seq():
+        for l, c in enumerate(calls):
+            st = sets[l % len(sets)]
+            F.fibattn_forward(st.q, st.k, st.v, c.W, c.base, c.alpha, o=st.o, lse=st.lse)
+            if backward:
+                F.fibattn_backward(st.q, st.k, st.v, st.o, st.lse, st.dO, c.W, c.base, c.alpha,
+                                   dq=st.dq, dk=st.dk, dv=st.dv, dalpha=st.da, workspace=st.ws)
+    if eager:
+        run = lambda i: run_seq()  # noqa: E731
+    else:
+        g = capture(run_seq)
+        run = lambda i: g.replay()  # noqa: E731
+    ms, _ = timed(run, steps, warmup)
+    s = 2 if wl.dtype == "bf16" else 4
+    qh = wl.queries_heads * len(calls)
+    byt = alg_bytes("fwd+bwd" if backward else "forward", wl.D, s) * qh
+    return {"layers": len(calls), "ms": ms, "ms_per_layer": ms / len(calls), "value": qh / (ms * 1e-3),
+            "alg_GBs": byt / (ms * 1e-3) / 1e9, "frac": byt / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
+
+
+def config_figures(steps: int, warmup: int, eager: bool):
+    """Attention forward + backward (no RoPE) of each workload's 16-layer sequence at its
+    own shape: the stagger sweep once per W, the 4x-length coprime stagger forward-only
+    and forward + backward, the pow2/fib learned-alpha layers once per base.  queries·heads/s
+    and the fraction of 8 TB/s for the algorithmic bytes (fwd+bwd 12·d·s+8, fwd 4·d·s+4 per
+    query-head)."""
+    import torch
+
+    from paper_2606_28560_amd import fibattn as F
+    from paper_2606_28560_amd import workloads
+
+    out = {}
+    for name in ("stagger16_T1024", "extrap_coprime16_T4096", "pow2_fib_learned16_T1024"):
+        wl = workloads.workload(name)
+        per = step_bytes(wl, wl.calls[0])
+        n = max(2, -(-2 * MALL_BYTES // per) + 1)
+        sets = [LayerSet(wl, wl.calls[0], i) for i in range(n)]
+        fig = {"B": wl.B, "H": wl.H, "T": wl.T, "d_head": wl.D, "buffer_sets": n}
+        if name == "stagger16_T1024":
+            for W in sorted(set(c.W for c in wl.calls)):
+                calls = [c for c in wl.calls if c.W == W]
+                fig[f"W{W}"] = sequence_figure(F, wl, calls, sets, True, steps, warmup, eager)
+        elif name == "extrap_coprime16_T4096":
+            fig["forward"] = sequence_figure(F, wl, wl.calls, sets, False, steps, warmup, eager)
+            fig["fwd+bwd"] = sequence_figure(F, wl, wl.calls, sets, True, steps, warmup, eager)
+        else:
+            for b in ("pow2_11", "fib15"):
+                calls = [c for c in wl.calls if c.base_name == b]
+                fig[b] = sequence_figure(F, wl, calls, sets, True, steps, warmup, eager)
+        out[name] = fig
+        del sets
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
     return out
 
 
@@ -376,8 +492,7 @@ def main():
     wl = workloads.workload(args.workload)
     call = wl.calls[0]
     s = 2 if wl.dtype == "bf16" else 4
-    per_set = wl.queries_heads * wl.D * s * 10
-    nsets = args.sets or max(3, -(-320 * 2**20 // per_set))
+    nsets = args.sets or buffer_sets(step_bytes(wl, call))
     print(f"# workload {wl.name}: B{wl.B} H{wl.H} T{wl.T} D{wl.D} {wl.dtype} W{call.W} "
           f"{call.base_name} alpha={float(call.alpha)}; {nsets} buffer sets", file=sys.stderr, flush=True)
     sets = [Step(wl, call, i) for i in range(nsets)]
@@ -433,7 +548,9 @@ def main():
                    "launch": "eager" if args.eager else "hip_graph", "buffer_sets": nsets},
         "roofline": roofline,
         "attention_only": {"ms_per_step": ms_attn, "value": qh / (ms_attn * 1e-3),
-                           "alg_GBs": alg_bytes("fwd+bwd", wl.D, s) * qh / (ms_attn * 1e-3) / 1e9},
+                           "alg_GBs": alg_bytes("fwd+bwd", wl.D, s) * qh / (ms_attn * 1e-3) / 1e9,
+                           "frac": alg_bytes("fwd+bwd", wl.D, s) * qh / (ms_attn * 1e-3) / 1e9
+                           / PEAK_HBM_GBS},
         "kernels": kt,
     }
     if not args.no_t4096:
@@ -444,6 +561,8 @@ def main():
         result["learned_alpha"] = learned_alpha_figure(max(5, args.steps // 4), 2, args.eager)
     if not args.no_integer_offsets:
         result["integer_offsets"] = integer_offsets_figure(max(5, args.steps // 4), 2, args.eager)
+    if not args.no_configs:
+        result["configs"] = config_figures(max(3, args.steps // 8), 1, args.eager)
     if args.copy_probe_mb:
         a = torch.empty(args.copy_probe_mb * 2**20, dtype=torch.uint8, device="cuda")
         b = torch.empty_like(a)

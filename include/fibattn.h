@@ -213,6 +213,15 @@ fibattn_status_t fibattn_backward_strided(const void *q, const void *k, const vo
  * fibattn_alpha_from_theta: alpha[l] = 0.5 + sigmoid(theta[l]), l < n (sigmoid in
  * float64, rounded once to float32).  fibattn_dtheta: dtheta[l] = dalpha[l] *
  * sigmoid(theta[l]) (1 - sigmoid(theta[l])).  All pointers are device float32 arrays.
+ *
+ * fibattn_device_table_theta: the layer's step in one launch instead of two: from one
+ * device float theta it writes alpha = 0.5 + sigmoid(theta) to *alpha (skipped when
+ * alpha is NULL; the same value as fibattn_alpha_from_theta) and builds that alpha's
+ * table (as fibattn_device_table), which also records d alpha / d theta.  Given such a
+ * table, fibattn_backward_dt writes dL/dtheta = dalpha * sigmoid (1 - sigmoid) to its
+ * `dtheta` argument (the value fibattn_dtheta computes from the stored dalpha), so the
+ * learned-alpha step needs no launch of its own besides the table.  dtheta may be NULL;
+ * with a table built from alpha (fibattn_device_table) it receives NaN.
  */
 size_t fibattn_device_table_bytes(void);
 
@@ -226,11 +235,15 @@ fibattn_status_t fibattn_forward_dt(const void *q, const void *k, const void *v,
 
 fibattn_status_t fibattn_backward_dt(const void *q, const void *k, const void *v,
                                      const void *o, const float *lse, const void *dO,
-                                     void *dq, void *dk, void *dv, float *dalpha,
+                                     void *dq, void *dk, void *dv, float *dalpha, float *dtheta,
                                      void *workspace, size_t workspace_bytes,
                                      int B, int H, int H_kv, int T, int d_head, int W,
                                      const void *table, float rope_base,
                                      fibattn_dtype_t dtype, hipStream_t stream);
+
+fibattn_status_t fibattn_device_table_theta(const float *theta, float *alpha,
+                                            const int32_t *base, int K, int W,
+                                            void *table, hipStream_t stream);
 
 fibattn_status_t fibattn_alpha_from_theta(const float *theta, float *alpha, int n,
                                           hipStream_t stream);
@@ -284,6 +297,22 @@ fibattn_status_t fibattn_backward_noalloc(const void *q, const void *k, const vo
                                           int B, int H, int H_kv, int T, int d_head, int W,
                                           const int32_t *base, int K, float alpha, float rope_base,
                                           fibattn_dtype_t dtype, hipStream_t stream);
+
+/*
+ * A layer's prologue in one launch: RoPE of q [B,H,T,d_head] and k [B,H_kv,T,d_head]
+ * (H_kv dividing H: grouped heads) as fibattn_rope_qk, and, when theta is not NULL, the
+ * layer's rung table from theta (as fibattn_device_table_theta: alpha = 0.5 +
+ * sigmoid(theta) written to *alpha unless alpha is NULL, the table of that alpha for
+ * (base, K, W) written to `table`, which also records d alpha / d theta).  So the step
+ * of a layer with a learned alpha launches as many kernels as one with a host alpha:
+ * this, fibattn_forward_dt and fibattn_backward_dt (which then also returns dtheta).
+ * With theta NULL, base, K, W and table are ignored.  Same limits and errors as
+ * fibattn_rope_qk and fibattn_device_table_theta.
+ */
+fibattn_status_t fibattn_rope_qk_table(const void *q, const void *k, void *q_out, void *k_out,
+                                       int B, int H, int H_kv, int T, int d_head, float rope_base,
+                                       const float *theta, float *alpha, const int32_t *base, int K,
+                                       int W, void *table, fibattn_dtype_t dtype, hipStream_t stream);
 
 /* Human-readable name of a status code (static storage). */
 const char *fibattn_status_string(fibattn_status_t status);

@@ -15,6 +15,12 @@ __global__ void rung_table_kernel(const float *__restrict__ alpha, BaseTable b, 
     *out = t;
 }
 
+__global__ void rung_table_theta_kernel(const float *__restrict__ theta, float *__restrict__ alpha_out,
+                                        BaseTable b, int W, RungTable *__restrict__ out) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    table_from_theta(theta, alpha_out, b, W, out);  // alpha as alpha_from_theta_kernel
+}
+
 // sigmoid in float64, rounded once to float32 (the host schedules round the same way)
 __global__ __launch_bounds__(256) void alpha_from_theta_kernel(const float *__restrict__ theta,
                                                                float *__restrict__ alpha, int n) {
@@ -36,6 +42,11 @@ __global__ __launch_bounds__(256) void dtheta_kernel(const float *__restrict__ t
 hipError_t launch_rung_table(const float *alpha, const BaseTable &b, int W, RungTable *out,
                              hipStream_t s) {
     return launch(kAlpha, rung_table_kernel, dim3(1), dim3(64), 0, s, alpha, b, W, out);
+}
+
+hipError_t launch_rung_table_theta(const float *theta, float *alpha_out, const BaseTable &b, int W,
+                                   RungTable *out, hipStream_t s) {
+    return launch(kAlpha, rung_table_theta_kernel, dim3(1), dim3(64), 0, s, theta, alpha_out, b, W, out);
 }
 
 hipError_t launch_alpha_from_theta(const float *theta, float *alpha, int n, hipStream_t s) {

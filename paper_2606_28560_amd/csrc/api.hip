@@ -248,7 +248,7 @@ static fibattn_status_t backward_impl(const void *q, const void *k, const void *
     const RungTerms terms{(uint32_t *)((char *)workspace + wl.terms), wl.planes};
     const RopeFreq rf = make_rope_freq((double)rope_base, d_head);
     const Heads hd{H, H / H_kv};
-    hipError_t e = launch_backward((int)dtype, d_head, q, k, v, o, lse, dO, dq, dk, dv, dalpha,
+    hipError_t e = launch_backward((int)dtype, d_head, q, k, v, o, lse, dO, dq, dk, dv, dalpha, nullptr,
                                    delta_ws, partials, terms, B * H, hd, T, W, rt, nullptr, rf,
                                    rope_base, lay, stream);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
@@ -333,6 +333,17 @@ fibattn_status_t fibattn_device_table(const float *alpha, const int32_t *base, i
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
 }
 
+fibattn_status_t fibattn_device_table_theta(const float *theta, float *alpha, const int32_t *base, int K,
+                                            int W, void *table, hipStream_t stream) {
+    if (!theta || !table || !aligned16(table) || W < 0 || W > FIBATTN_MAX_WINDOW)
+        return FIBATTN_ERR_INVALID_ARG;
+    BaseTable b;
+    fibattn_status_t st = check_base(base, K, &b);
+    if (st != FIBATTN_OK) return st;
+    hipError_t e = launch_rung_table_theta(theta, alpha, b, W, (RungTable *)table, stream);
+    return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
 fibattn_status_t fibattn_forward_dt(const void *q, const void *k, const void *v, void *o, float *lse,
                                     int B, int H, int H_kv, int T, int d_head, int W,
                                     const void *table, fibattn_dtype_t dtype, hipStream_t stream) {
@@ -353,7 +364,7 @@ fibattn_status_t fibattn_forward_dt(const void *q, const void *k, const void *v,
 
 fibattn_status_t fibattn_backward_dt(const void *q, const void *k, const void *v, const void *o,
                                      const float *lse, const void *dO, void *dq, void *dk, void *dv,
-                                     float *dalpha, void *workspace, size_t workspace_bytes, int B,
+                                     float *dalpha, float *dtheta, void *workspace, size_t workspace_bytes, int B,
                                      int H, int H_kv, int T, int d_head, int W, const void *table,
                                      float rope_base, fibattn_dtype_t dtype, hipStream_t stream) {
     fibattn_status_t st = check_common(B, H, T, d_head, W, 0, dtype);
@@ -374,7 +385,7 @@ fibattn_status_t fibattn_backward_dt(const void *q, const void *k, const void *v
     const RungTerms terms{(uint32_t *)((char *)workspace + wl.terms), wl.planes};
     const RopeFreq rf = make_rope_freq((double)rope_base, d_head);
     const Heads hd{H, H / H_kv};
-    hipError_t e = launch_backward((int)dtype, d_head, q, k, v, o, lse, dO, dq, dk, dv, dalpha,
+    hipError_t e = launch_backward((int)dtype, d_head, q, k, v, o, lse, dO, dq, dk, dv, dalpha, dtheta,
                                    delta_ws, partials, terms, B * H, hd, T, W, unused,
                                    (const RungTable *)table, rf, rope_base,
                                    packed_layouts(H, H_kv, T, d_head), stream);
@@ -422,6 +433,34 @@ fibattn_status_t fibattn_rope_qk(const void *q, const void *k, void *q_out, void
     const Layout l = Layout::packed(H, T, d_head);
     hipError_t e = launch_rope((int)dtype, d_head, q, q_out, l, l, k, k_out, l, l, B * H, H, T, rope_base,
                                0, stream);
+    return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
+fibattn_status_t fibattn_rope_qk_table(const void *q, const void *k, void *q_out, void *k_out, int B, int H,
+                                       int H_kv, int T, int d_head, float rope_base, const float *theta,
+                                       float *alpha, const int32_t *base, int K, int W, void *table,
+                                       fibattn_dtype_t dtype, hipStream_t stream) {
+    if (B < 1 || H < 1 || T < 1 || !q || !k || !q_out || !k_out) return FIBATTN_ERR_INVALID_ARG;
+    if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(q_out) || !aligned16(k_out))
+        return FIBATTN_ERR_INVALID_ARG;
+    if (dtype != FIBATTN_FP32 && dtype != FIBATTN_BF16) return FIBATTN_ERR_INVALID_ARG;
+    if (!(rope_base > 1.f) || !isfinite(rope_base)) return FIBATTN_ERR_INVALID_ARG;
+    if (d_head != 32 && d_head != 64 && d_head != 128) return FIBATTN_ERR_UNSUPPORTED;
+    if ((long long)B * H > 65535ll * 16) return FIBATTN_ERR_UNSUPPORTED;
+    TableJob job{};
+    if (theta) {
+        if (!table || !aligned16(table) || W < 0 || W > FIBATTN_MAX_WINDOW) return FIBATTN_ERR_INVALID_ARG;
+        const fibattn_status_t st = check_base(base, K, &job.b);
+        if (st != FIBATTN_OK) return st;
+        job.theta = theta;
+        job.alpha = alpha;
+        job.out = (RungTable *)table;
+        job.W = W;
+    }
+    const Layout lq = Layout::packed(H, T, d_head), lk = Layout::packed(H_kv, T, d_head);
+    hipError_t e = launch_rope((int)dtype, d_head, q, q_out, lq, lq, k, k_out, lk, lk, B * H, H, T, rope_base,
+                               0, stream, B * H_kv, H_kv, theta ? &job : nullptr);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
 }
 

@@ -250,8 +250,11 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(
 // ---------------------------------------------------------------------------
 // dalpha: one workgroup sums the partials in a fixed order, in float64.
 // ---------------------------------------------------------------------------
+// dtheta (device tables built from theta): dalpha (as stored) times d alpha / d theta.
 __global__ __launch_bounds__(256) void dalpha_reduce_kernel(const double *__restrict__ partials,
-                                                            size_t n, float *__restrict__ dalpha) {
+                                                            size_t n, float *__restrict__ dalpha,
+                                                            float *__restrict__ dtheta,
+                                                            const RungTable *__restrict__ rtp) {
     __shared__ double red[256];
     double s = 0.0;
     for (size_t t = threadIdx.x; t < n; t += 256) s += partials[t];
@@ -262,7 +265,11 @@ __global__ __launch_bounds__(256) void dalpha_reduce_kernel(const double *__rest
         if ((int)threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
         __syncthreads();
     }
-    if (threadIdx.x == 0) *dalpha = (float)red[0];
+    if (threadIdx.x == 0) {
+        const float da = (float)red[0];
+        *dalpha = da;
+        if (dtheta) *dtheta = (float)((double)da * rtp->dadtheta);
+    }
 }
 
 template <typename S, int D>
@@ -284,7 +291,7 @@ size_t bwd_num_partials(int dtype, int D, int BH, int T) {
 template <typename S, int D>
 static hipError_t launch_bwd_t(const void *q, const void *k, const void *v, const void *o,
                                const float *lse, const void *dO, void *dq, void *dk, void *dv,
-                               float *dalpha, float *delta_ws, double *partials, int BH,
+                               float *dalpha, float *dtheta, float *delta_ws, double *partials, int BH,
                                const Heads &hd, int T, int W, const RungTable &rt,
                                const RungTable *rtp, const Layouts &lay, hipStream_t s) {
     constexpr int QPB = 256 / (D / Vec<S>::N);
@@ -299,17 +306,17 @@ static hipError_t launch_bwd_t(const void *q, const void *k, const void *v, cons
                lse, (const S *)dO, delta_ws, (S *)dk, (S *)dv, T, W, rt, rtp, tau, hd, lay);
     if (e != hipSuccess) return e;
     return launch(kDalphaReduce, dalpha_reduce_kernel, dim3(1), dim3(256), 0, s, partials,
-                  (size_t)grid.x * grid.y, dalpha);
+                  (size_t)grid.x * grid.y, dalpha, dtheta, rtp);
 }
 
 static hipError_t launch_backward_generic(int dtype, int D, const void *q, const void *k, const void *v,
                                           const void *o, const float *lse, const void *dO, void *dq,
-                                          void *dk, void *dv, float *dalpha, float *delta_ws,
+                                          void *dk, void *dv, float *dalpha, float *dtheta, float *delta_ws,
                                           double *partials, int BH, const Heads &hd, int T, int W,
                                           const RungTable &rt, const RungTable *rtp, const Layouts &lay,
                                           hipStream_t s) {
 #define FIBATTN_BWD(S_, D_)                                                                  \
-    return launch_bwd_t<S_, D_>(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials, \
+    return launch_bwd_t<S_, D_>(q, k, v, o, lse, dO, dq, dk, dv, dalpha, dtheta, delta_ws, partials, \
                                 BH, hd, T, W, rt, rtp, lay, s)
     if (dtype == 0 && D == 32) FIBATTN_BWD(float, 32);
     if (dtype == 0 && D == 64) FIBATTN_BWD(float, 64);
@@ -324,28 +331,20 @@ static hipError_t launch_backward_generic(int dtype, int D, const void *q, const
 
 hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const void *v,
                            const void *o, const float *lse, const void *dO, void *dq, void *dk,
-                           void *dv, float *dalpha, float *delta_ws, double *partials,
+                           void *dv, float *dalpha, float *dtheta, float *delta_ws, double *partials,
                            const RungTerms &terms, int BH, const Heads &hd, int T, int W,
                            const RungTable &rt, const RungTable *rtp, const RopeFreq &rf,
                            float rope_base, const Layouts &lay, hipStream_t s) {
     if (backward_mfma_supported(dtype, D, W))
-        return launch_backward_mfma(q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws, partials,
+        return launch_backward_mfma(q, k, v, o, lse, dO, dq, dk, dv, dalpha, dtheta, delta_ws, partials,
                                     terms, BH, hd, T, W, rt, rtp, rf, lay, s);
-    hipError_t e = launch_backward_generic(dtype, D, q, k, v, o, lse, dO, dq, dk, dv, dalpha, delta_ws,
+    hipError_t e = launch_backward_generic(dtype, D, q, k, v, o, lse, dO, dq, dk, dv, dalpha, dtheta, delta_ws,
                                            partials, BH, hd, T, W, rt, rtp, lay, s);
     // R^T on dq and dk in place: gradients w.r.t. the unrotated q, k (R^T is linear, so
     // it also carries the group sum in dk)
     if (e == hipSuccess && rf.on) {
-        if (hd.G == 1) {
-            e = launch_rope(dtype, D, dq, dq, lay.dq, lay.dq, dk, dk, lay.dk, lay.dk, BH, hd.H, T,
-                            rope_base, 1, s);
-        } else {
-            e = launch_rope(dtype, D, dq, dq, lay.dq, lay.dq, nullptr, nullptr, lay.dq, lay.dq, BH, hd.H,
-                            T, rope_base, 1, s);
-            if (e == hipSuccess)
-                e = launch_rope(dtype, D, dk, dk, lay.dk, lay.dk, nullptr, nullptr, lay.dk, lay.dk,
-                                BH / hd.G, hd.kv_heads(), T, rope_base, 1, s);
-        }
+        e = launch_rope(dtype, D, dq, dq, lay.dq, lay.dq, dk, dk, lay.dk, lay.dk, BH, hd.H, T, rope_base, 1,
+                        s, BH / hd.G, hd.kv_heads());
     }
     return e;
 }

@@ -97,12 +97,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     const int last = t0 + 15;
     int nact = 0;
 #pragma unroll
-    for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && rt.d0[r] <= last) ? 1 : 0;
+    // (a device table is tested unconditionally: wide scalar loads, no chain of dependent ones)
+    for (int r = 0; r < kMaxRungs; ++r)
+        nact += (DEV ? ((r < rt.n) & (rt.d0[r] <= last)) : (r < rt.n && rt.d0[r] <= last)) ? 1 : 0;
     nact = __builtin_amdgcn_readfirstlane(nact);  // wave-uniform: scalar branches
     // rungs whose rows r0 and r1 for every query of the wave lie in the staged rows
     int nlds = 0;
 #pragma unroll
-    for (int r = 0; r < kMaxRungs; ++r) nlds += (INTERP && r < rt.n && rt.d0[r] + 1 <= kLeadQ + 16 * wv) ? 1 : 0;
+    for (int r = 0; r < kMaxRungs; ++r)
+        nlds += (INTERP && (DEV ? ((r < rt.n) & (rt.d0[r] + 1 <= kLeadQ + 16 * wv))
+                                : (r < rt.n && rt.d0[r] + 1 <= kLeadQ + 16 * wv))) ? 1 : 0;
     nlds = __builtin_amdgcn_readfirstlane(nlds);
     // x = {k0, v0, k1, v1}: rows r0 and r1 = r0 - 1 of K and V (r1 is needed for
     // dalpha even when w == 0; then it is row r0 of the previous query, but loading it
@@ -262,7 +266,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const float *__restrict__ lse, const uint16_t *__restrict__ dO, const float *__restrict__ delta_in,
     RungTerms terms, uint16_t *__restrict__ dk, uint16_t *__restrict__ dv,
-    const double *__restrict__ partials, int n_partials, float *__restrict__ dalpha, int T, int W,
+    const double *__restrict__ partials, int n_partials, float *__restrict__ dalpha,
+    float *__restrict__ dtheta, int T, int W,
     RungTable rt_arg,
     const RungTable *__restrict__ rtp, RopeFreq rf, float tau, int tiles, Heads hd, Layouts lay) {
     const RungTable &rt = DEV ? *rtp : rt_arg;
@@ -308,7 +313,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
             if ((int)threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
             __syncthreads();
         }
-        if (threadIdx.x == 0) *dalpha = (float)red[0];
+        if (threadIdx.x == 0) {
+            const float da = (float)red[0];
+            *dalpha = da;
+            // a table built from theta: d L / d theta = dalpha * d alpha / d theta
+            if (DEV && dtheta) *dtheta = (float)((double)da * rt.dadtheta);
+        }
         __syncthreads();
     }
 
@@ -319,7 +329,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     // rungs: some key of this wave has j + floor(d) < T for a prefix of the table
     int nact = 0;
 #pragma unroll
-    for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && t0 + rt.d0[r] < T) ? 1 : 0;
+    for (int r = 0; r < kMaxRungs; ++r)  // a device table: unconditional tests (wide scalar loads)
+        nact += (DEV ? ((r < rt.n) & (t0 + rt.d0[r] < T)) : (r < rt.n && t0 + rt.d0[r] < T)) ? 1 : 0;
     nact = __builtin_amdgcn_readfirstlane(nact);  // wave-uniform: scalar branches
 
     // With several passes the table is staged before the pass loop: inside it the
@@ -581,7 +592,7 @@ template <int NH>
 static hipError_t launch_dkdv(bool interp, const void *q, const void *k, const void *v,
                               const float *lse, const void *dO, const float *delta_ws,
                               const RungTerms &terms, void *dk, void *dv, const double *partials,
-                              int n_partials, float *dalpha,
+                              int n_partials, float *dalpha, float *dtheta,
                               int BH, const Heads &hd, int T, int W, const RungTable &rt,
                               const RungTable *rtp, const RopeFreq &rf, float tau,
                               const Layouts &lay, hipStream_t s) {
@@ -599,13 +610,13 @@ static hipError_t launch_dkdv(bool interp, const void *q, const void *k, const v
                         : (interp ? FIBATTN_DKDV(true, false) : FIBATTN_DKDV(false, false));
 #undef FIBATTN_DKDV
     return launch(kBwdDkDv, kern, dim3(tiles * (BH / hd.G)), dim3(256), 0, s, q, k, v, lse, dO,
-                  delta_ws, terms, dk, dv, partials, n_partials, dalpha, T, W, rt, rtp, rf, tau,
+                  delta_ws, terms, dk, dv, partials, n_partials, dalpha, dtheta, T, W, rt, rtp, rf, tau,
                   tiles, hd, lay);
 }
 
 hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, const void *o,
                                 const float *lse, const void *dO, void *dq, void *dk, void *dv,
-                                float *dalpha, float *delta_ws, double *partials,
+                                float *dalpha, float *dtheta, float *delta_ws, double *partials,
                                 const RungTerms &terms, int BH, const Heads &hd, int T, int W,
                                 const RungTable &rt, const RungTable *rtp, const RopeFreq &rf,
                                 const Layouts &lay, hipStream_t s) {
@@ -625,12 +636,12 @@ hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, con
     if (e != hipSuccess) return e;
     // query heads per key/value head processed side by side in a workgroup
     if (hd.G % 4 == 0)
-        return launch_dkdv<4>(interp, q, k, v, lse, dO, delta_ws, terms, dk, dv, partials, nb, dalpha, BH,
+        return launch_dkdv<4>(interp, q, k, v, lse, dO, delta_ws, terms, dk, dv, partials, nb, dalpha, dtheta, BH,
                               hd, T, W, rt, rtp, rf, tau, lay, s);
     if (hd.G % 2 == 0)
-        return launch_dkdv<2>(interp, q, k, v, lse, dO, delta_ws, terms, dk, dv, partials, nb, dalpha, BH,
+        return launch_dkdv<2>(interp, q, k, v, lse, dO, delta_ws, terms, dk, dv, partials, nb, dalpha, dtheta, BH,
                               hd, T, W, rt, rtp, rf, tau, lay, s);
-    return launch_dkdv<1>(interp, q, k, v, lse, dO, delta_ws, terms, dk, dv, partials, nb, dalpha, BH, hd,
+    return launch_dkdv<1>(interp, q, k, v, lse, dO, delta_ws, terms, dk, dv, partials, nb, dalpha, dtheta, BH, hd,
                           T, W, rt, rtp, rf, tau, lay, s);
 }
 

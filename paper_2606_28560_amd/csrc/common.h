@@ -22,6 +22,9 @@ struct RungTable {
     int d0[kMaxRungs];
     float w[kMaxRungs];
     int f[kMaxRungs];
+    // d alpha / d theta = sigmoid(theta) (1 - sigmoid(theta)) for a table built from theta
+    // (alpha = 0.5 + sigmoid(theta)); NaN for a table built from alpha itself
+    double dadtheta;
 };
 
 // A device-built table that must not be used for a launch with window W: its alpha
@@ -44,6 +47,7 @@ __host__ __device__ inline bool rung_table_fill(float alpha, const BaseTable &b,
     for (int a = 0; a < kMaxRungs; ++a) { rt->d0[a] = 0; rt->w[a] = 0.f; rt->f[a] = 0; }
     rt->n = -1;
     rt->W = W;
+    rt->dadtheta = __builtin_nan("");
     if (!(alpha > 0.f) || !(alpha < INFINITY)) return false;
     int n = 0;
     float last = -1.f;
@@ -62,6 +66,30 @@ __host__ __device__ inline bool rung_table_fill(float alpha, const BaseTable &b,
     rt->n = n;
     return true;
 }
+
+// The table of a layer whose alpha is learned (Section 2, "The per-layer scalar"):
+// alpha = 0.5 + sigmoid(theta) with the sigmoid in float64 and one rounding to float32
+// (as the host schedules), the table of that alpha, and d alpha / d theta.  One thread.
+__device__ inline void table_from_theta(const float *theta, float *alpha_out, const BaseTable &b, int W,
+                                        RungTable *out) {
+    const double sg = 1.0 / (1.0 + exp(-(double)*theta));
+    const float alpha = (float)(0.5 + sg);
+    RungTable t;
+    rung_table_fill(alpha, b, W, &t);
+    t.dadtheta = sg * (1.0 - sg);
+    *out = t;
+    if (alpha_out) *alpha_out = alpha;
+}
+
+// A table build carried by another launch (the RoPE of a learned-alpha layer): done by
+// thread 0 of block 0 when `out` is set.
+struct TableJob {
+    const float *theta;
+    float *alpha;
+    RungTable *out;
+    BaseTable b;
+    int W;
+};
 
 // Per-(query, rung) terms of the backward that the dq kernel of the matrix-core path
 // hands to its dk/dv kernel: for query i of flat head bh and rung r of the table, the

@@ -64,16 +64,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
 
     const int t0 = T0 + 16 * wv;
     const int last = t0 + 15;  // the wave's last query
-    // rungs some query of this wave includes: a prefix of the table (sorted by d)
+    // rungs some query of this wave includes: a prefix of the table (sorted by d).  A
+    // table in device memory is tested entry by entry unconditionally (entries past n are
+    // zero), so it is fetched with a few wide scalar loads rather than a chain of
+    // dependent ones; a table in the kernel arguments keeps the short-circuit form.
     int nact = 0;
 #pragma unroll
-    for (int r = 0; r < kMaxRungs; ++r) nact += (r < rt.n && rt.d0[r] <= last) ? 1 : 0;
+    for (int r = 0; r < kMaxRungs; ++r)
+        nact += (DEV ? ((r < rt.n) & (rt.d0[r] <= last)) : (r < rt.n && rt.d0[r] <= last)) ? 1 : 0;
     nact = __builtin_amdgcn_readfirstlane(nact);  // wave-uniform: scalar branches
     // rungs whose rows (r0 and, interpolating, r1) for every query of the wave lie in
     // the staged rows: a prefix of the table
     int nlds = 0;
 #pragma unroll
-    for (int r = 0; r < kMaxRungs; ++r) nlds += (INTERP && r < rt.n && rt.d0[r] + NS - 1 <= kLeadF + 16 * wv) ? 1 : 0;
+    for (int r = 0; r < kMaxRungs; ++r)
+        nlds += (INTERP && (DEV ? ((r < rt.n) & (rt.d0[r] + NS - 1 <= kLeadF + 16 * wv))
+                                : (r < rt.n && rt.d0[r] + NS - 1 <= kLeadF + 16 * wv))) ? 1 : 0;
     nlds = __builtin_amdgcn_readfirstlane(nlds);
 
     const int im = t0 + nm;  // query of this lane in the MFMA layout

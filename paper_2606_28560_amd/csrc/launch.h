@@ -40,9 +40,10 @@ hipError_t launch_forward(int dtype, int D, const void *q, const void *k, const 
 // Number of dalpha partials the dq kernel writes (one per workgroup).
 size_t bwd_num_partials(int dtype, int D, int BH, int T);
 
+// dtheta (nullable, device tables only): also writes dalpha * rtp->dadtheta there.
 hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const void *v,
                            const void *o, const float *lse, const void *dO, void *dq, void *dk,
-                           void *dv, float *dalpha, float *delta_ws, double *partials,
+                           void *dv, float *dalpha, float *dtheta, float *delta_ws, double *partials,
                            const RungTerms &terms, int BH, const Heads &hd, int T, int W,
                            const RungTable &rt, const RungTable *rtp, const RopeFreq &rf,
                            float rope_base, const Layouts &lay, hipStream_t s);
@@ -56,7 +57,7 @@ bool backward_mfma_supported(int dtype, int D, int W);
 size_t bwd_mfma_num_partials(int BH, int T);
 hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, const void *o,
                                 const float *lse, const void *dO, void *dq, void *dk, void *dv,
-                                float *dalpha, float *delta_ws, double *partials,
+                                float *dalpha, float *dtheta, float *delta_ws, double *partials,
                                 const RungTerms &terms, int BH, const Heads &hd, int T, int W,
                                 const RungTable &rt, const RungTable *rtp, const RopeFreq &rf,
                                 const Layouts &lay, hipStream_t s);
@@ -66,14 +67,21 @@ RopeFreq make_rope_freq(double rope_base, int D);  // on = 0 when rope_base <= 0
 // Device-resident alpha: builds the rung table from *alpha (one thread) into *out.
 hipError_t launch_rung_table(const float *alpha, const BaseTable &b, int W, RungTable *out,
                              hipStream_t s);
+// The same from *theta: alpha = 0.5 + sigmoid(theta) (written to *alpha_out when not null)
+// and the table, which also records d alpha / d theta, in one launch.
+hipError_t launch_rung_table_theta(const float *theta, float *alpha_out, const BaseTable &b, int W,
+                                   RungTable *out, hipStream_t s);
 // alpha_l = 0.5 + sigmoid(theta_l); dtheta_l = dalpha_l sigmoid(theta_l) (1 - sigmoid(theta_l)).
 hipError_t launch_alpha_from_theta(const float *theta, float *alpha, int n, hipStream_t s);
 hipError_t launch_dtheta(const float *theta, const float *dalpha, float *dtheta, int n, hipStream_t s);
 
-// RoPE of one tensor (x1 == nullptr) or of two same-shaped tensors in one launch:
-// BH = batch * heads rows; inputs and outputs placed by their layouts.
+// RoPE of one tensor (x1 == nullptr) or of two tensors in one launch: BH = batch * heads
+// rows of the first, BH1 rows of heads1 heads of the second (BH1 <= 0: same as the first);
+// inputs and outputs placed by their layouts.  A table job (may be null) is carried by
+// the first launch.
 hipError_t launch_rope(int dtype, int D, const void *x0, void *y0, const Layout &lx0, const Layout &ly0,
                        const void *x1, void *y1, const Layout &lx1, const Layout &ly1, int BH, int heads,
-                       int T, float rope_base, int transpose, hipStream_t s);
+                       int T, float rope_base, int transpose, hipStream_t s, int BH1 = 0, int heads1 = 0,
+                       const TableJob *job = nullptr);
 
 }  // namespace fibattn

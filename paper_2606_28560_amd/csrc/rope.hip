@@ -27,9 +27,12 @@ template <> __device__ __forceinline__ void st1<uint16_t>(uint16_t *p, float x) 
 // BH = batch * heads rows of positions [0, T); x and y placed by lx and ly.
 template <typename S, int D>
 __global__ __launch_bounds__(256) void rope_kernel(const S *x, S *y, int BH, int T, double rope_base,
-                                                   int transpose, int heads, Layout lx, Layout ly) {
+                                                   int transpose, int heads, Layout lx, Layout ly,
+                                                   TableJob job) {
     constexpr int HALF = D / 2;
     __shared__ float cs[kRopeTP * HALF], sn[kRopeTP * HALF];
+    if (job.out && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
+        table_from_theta(job.theta, job.alpha, job.b, job.W, job.out);
     const int t0 = blockIdx.x * kRopeTP;
     for (int a = threadIdx.x; a < kRopeTP * HALF; a += 256) {
         const int t = t0 + a / HALF;
@@ -70,20 +73,26 @@ __global__ __launch_bounds__(256) void rope_kernel(const S *x, S *y, int BH, int
 constexpr int kRope64TP = 8;
 constexpr int kRope64RB = 16;
 
-// blockIdx.z selects the tensor: (x0 -> y0) or (x1 -> y1), each placed by its io
+// blockIdx.z selects the tensor: (x0 -> y0) or (x1 -> y1), each with its own row count
+// (batch * heads) and head count (k may have fewer heads than q) and placed by its io
 // (STRIDED; else every tensor is packed [BH, T, 64]).
 struct RopeIO {
     Layout x, y;
+    int BH, heads;
 };
 template <bool STRIDED>
 __global__ __launch_bounds__(256) void rope_bf16_d64_kernel(const uint16_t *x0, uint16_t *y0,
-                                                            const uint16_t *x1, uint16_t *y1, int BH,
+                                                            const uint16_t *x1, uint16_t *y1,
                                                             int T, RopeFreq rf, int transpose,
-                                                            int heads, RopeIO io0, RopeIO io1) {
+                                                            RopeIO io0, RopeIO io1, TableJob job) {
     __shared__ float cs[kRope64TP * 32], sn[kRope64TP * 32];
     const uint16_t *x = blockIdx.z ? x1 : x0;
     uint16_t *y = blockIdx.z ? y1 : y0;
     const RopeIO &io = blockIdx.z ? io1 : io0;
+    const int BH = io.BH, heads = io.heads;
+    if (job.out && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && threadIdx.x == 0)
+        table_from_theta(job.theta, job.alpha, job.b, job.W, job.out);
+    if (blockIdx.y * kRope64RB >= BH) return;  // the tensor with fewer heads
     const int t0 = blockIdx.x * kRope64TP;
     const int g = threadIdx.x & 3;
     const int rr = threadIdx.x >> 2;  // 0..63
@@ -139,12 +148,12 @@ RopeFreq make_rope_freq(double rope_base, int D) {
 
 static hipError_t launch_rope_generic(int dtype, int D, const void *x, void *y, int BH, int T,
                                       double lb, int transpose, int heads, const Layout &lx,
-                                      const Layout &ly, hipStream_t s) {
+                                      const Layout &ly, const TableJob &job, hipStream_t s) {
     dim3 grid((T + kRopeTP - 1) / kRopeTP, (BH + kRopeRB - 1) / kRopeRB);
 #define FIBATTN_ROPE(S, DD)                                                                          \
     if ((dtype == 0) == (sizeof(S) == 4) && D == DD)                                                  \
         return launch(kRope, rope_kernel<S, DD>, grid, dim3(256), 0, s, x, y, BH, T, lb, transpose, \
-                      heads, lx, ly);
+                      heads, lx, ly, job);
     FIBATTN_ROPE(float, 32)
     FIBATTN_ROPE(float, 64)
     FIBATTN_ROPE(float, 128)
@@ -155,25 +164,35 @@ static hipError_t launch_rope_generic(int dtype, int D, const void *x, void *y, 
     return hipErrorInvalidValue;
 }
 
-// One launch for one tensor (x1 == nullptr) or two tensors of the same shape; BH =
-// batch * heads rows; each input and output placed by its layout.
+// One launch for one tensor (x1 == nullptr) or two tensors (BH1 rows of heads1 heads for
+// the second); BH = batch * heads rows; each input and output placed by its layout.  The
+// table job (job.out set) rides on the first launch.
 hipError_t launch_rope(int dtype, int D, const void *x0, void *y0, const Layout &lx0, const Layout &ly0,
                        const void *x1, void *y1, const Layout &lx1, const Layout &ly1, int BH, int heads,
-                       int T, float rope_base, int transpose, hipStream_t s) {
+                       int T, float rope_base, int transpose, hipStream_t s, int BH1, int heads1,
+                       const TableJob *job) {
     const double lb = (double)rope_base;
+    TableJob nojob{};
+    const TableJob &tj = job ? *job : nojob;
+    if (BH1 <= 0) { BH1 = BH; heads1 = heads; }
     if (dtype == 1 && D == 64) {
         const RopeFreq rf = make_rope_freq(lb, 64);
-        const Layout p = Layout::packed(heads, T, 64);
-        auto same = [&](const Layout &l) { return l.sb == p.sb && l.sh == p.sh && l.st == p.st; };
-        const bool strided = !same(lx0) || !same(ly0) || (x1 && (!same(lx1) || !same(ly1)));
+        auto same = [&](const Layout &l, int hs) {
+            const Layout p = Layout::packed(hs, T, 64);
+            return l.sb == p.sb && l.sh == p.sh && l.st == p.st;
+        };
+        const bool strided = !same(lx0, heads) || !same(ly0, heads) ||
+                             (x1 && (!same(lx1, heads1) || !same(ly1, heads1)));
+        const int rows = x1 ? max(BH, BH1) : BH;
         return launch(kRope, strided ? rope_bf16_d64_kernel<true> : rope_bf16_d64_kernel<false>,
-                      dim3((T + kRope64TP - 1) / kRope64TP, (BH + kRope64RB - 1) / kRope64RB,
+                      dim3((T + kRope64TP - 1) / kRope64TP, (rows + kRope64RB - 1) / kRope64RB,
                            x1 ? 2 : 1),
-                      dim3(256), 0, s, x0, y0, x1, y1, BH, T, rf, transpose, heads, RopeIO{lx0, ly0},
-                      RopeIO{lx1, ly1});
+                      dim3(256), 0, s, x0, y0, x1, y1, T, rf, transpose, RopeIO{lx0, ly0, BH, heads},
+                      RopeIO{lx1, ly1, BH1, heads1}, tj);
     }
-    hipError_t e = launch_rope_generic(dtype, D, x0, y0, BH, T, lb, transpose, heads, lx0, ly0, s);
-    if (e == hipSuccess && x1) e = launch_rope_generic(dtype, D, x1, y1, BH, T, lb, transpose, heads, lx1, ly1, s);
+    hipError_t e = launch_rope_generic(dtype, D, x0, y0, BH, T, lb, transpose, heads, lx0, ly0, tj, s);
+    if (e == hipSuccess && x1)
+        e = launch_rope_generic(dtype, D, x1, y1, BH1, T, lb, transpose, heads1, lx1, ly1, nojob, s);
     return e;
 }
 

@@ -26,7 +26,7 @@ EXPORTED = ("fibattn_rung_table", "fibattn_forward", "fibattn_backward_workspace
             "fibattn_device_table_bytes", "fibattn_device_table", "fibattn_forward_dt",
             "fibattn_backward_dt", "fibattn_alpha_from_theta", "fibattn_dtheta", "fibattn_rope",
             "fibattn_rope_qk", "fibattn_status_string", "fibattn_timing_begin", "fibattn_timing_end",
-            "fibattn_backward_noalloc")
+            "fibattn_backward_noalloc", "fibattn_device_table_theta", "fibattn_rope_qk_table")
 SCRATCH_BYTES = 64 << 20  # FIBATTN_SCRATCH_BYTES: the allocation-free backward's static scratch
 
 
@@ -76,8 +76,12 @@ def lib():
     L.fibattn_device_table.restype = i
     L.fibattn_forward_dt.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, vp, i, vp]
     L.fibattn_forward_dt.restype = i
-    L.fibattn_backward_dt.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+    L.fibattn_backward_dt.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                       i, i, i, i, i, i, vp, f, i, vp]
+    L.fibattn_device_table_theta.argtypes = [vp, vp, ip, i, i, vp, vp]
+    L.fibattn_device_table_theta.restype = i
+    L.fibattn_rope_qk_table.argtypes = [vp, vp, vp, vp, i, i, i, i, i, f, vp, vp, ip, i, i, vp, i, vp]
+    L.fibattn_rope_qk_table.restype = i
     L.fibattn_backward_dt.restype = i
     L.fibattn_alpha_from_theta.argtypes = [vp, vp, i, vp]
     L.fibattn_alpha_from_theta.restype = i
@@ -304,6 +308,28 @@ def fibattn_device_table(alpha, base, W: int, *, table=None, stream=None):
     return table
 
 
+def fibattn_device_table_theta(theta, base, W: int, *, table=None, alpha=None, stream=None):
+    """Rung table of alpha = 0.5 + sigmoid(theta) for a device theta (a 1-element float32
+    tensor, or one element of a per-layer array), built on the device in one launch;
+    writes alpha too when given.  Returns the table buffer (uint8 tensor)."""
+    import torch
+
+    if theta.device.type != "cuda" or theta.dtype != torch.float32 or theta.numel() < 1:
+        raise ValueError("theta: a float32 device tensor")
+    nb = int(lib().fibattn_device_table_bytes())
+    if table is None:
+        table = torch.empty(nb, device=theta.device, dtype=torch.uint8)
+    if table.numel() < nb or not table.is_contiguous():
+        raise ValueError(f"table: {nb} contiguous bytes")
+    if alpha is not None and (alpha.dtype != torch.float32 or alpha.numel() < 1 or not alpha.is_cuda):
+        raise ValueError("alpha: a float32 device tensor")
+    b, bp = _base_array(base)
+    st = lib().fibattn_device_table_theta(theta.data_ptr(), None if alpha is None else alpha.data_ptr(), bp,
+                                          b.size, int(W), table.data_ptr(), _stream(stream))
+    _check("fibattn_device_table_theta", st)
+    return table
+
+
 def fibattn_forward_dt(q, k, v, W: int, table, *, o=None, lse=None, stream=None):
     """As fibattn_forward, with the rung table built on the device."""
     import torch
@@ -324,8 +350,9 @@ def fibattn_forward_dt(q, k, v, W: int, table, *, o=None, lse=None, stream=None)
 
 
 def fibattn_backward_dt(q, k, v, o, lse, dO, W: int, table, *, dq=None, dk=None, dv=None,
-                        dalpha=None, workspace=None, rope_base: float = 0.0, stream=None):
-    """As fibattn_backward, with the rung table built on the device."""
+                        dalpha=None, dtheta=None, workspace=None, rope_base: float = 0.0, stream=None):
+    """As fibattn_backward, with the rung table built on the device; with `dtheta` (a
+    float32 device tensor) and a table built from theta, also dL/dtheta."""
     import torch
 
     B, H, T, D = q.shape
@@ -347,7 +374,8 @@ def fibattn_backward_dt(q, k, v, o, lse, dO, W: int, table, *, dq=None, dk=None,
         workspace = torch.empty(max(need, 1), device=q.device, dtype=torch.uint8)
     st = lib().fibattn_backward_dt(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
                                    dO.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
-                                   dalpha.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                                   dalpha.data_ptr(), None if dtheta is None else dtheta.data_ptr(),
+                                   workspace.data_ptr(), workspace.numel(),
                                    B, H, Hkv, T, D, int(W), table.data_ptr(), ctypes.c_float(rope_base),
                                    _dtype_code(q), _stream(stream))
     _check("fibattn_backward_dt", st)
@@ -408,6 +436,40 @@ def fibattn_rope_qk(q, k, rope_base: float = 10000.0, *, q_out=None, k_out=None,
                                D, ctypes.c_float(rope_base), _dtype_code(q), _stream(stream))
     _check("fibattn_rope_qk", st)
     return q_out, k_out
+
+
+def fibattn_rope_qk_table(q, k, rope_base: float = 10000.0, *, theta=None, base=(), W: int = 0, table=None,
+                          alpha=None, q_out=None, k_out=None, stream=None):
+    """R q and R k in one launch (k may have fewer heads than q); with `theta` (a float32
+    device tensor) the same launch builds the rung table of alpha = 0.5 + sigmoid(theta)
+    for (base, W) into `table` (allocated when None) and writes alpha when given.
+    Returns (q_out, k_out, table)."""
+    import torch
+
+    B, H, T, D = q.shape
+    Hkv = _kv_heads(q, k)
+    _check_tensor("q", q, q.shape, q.dtype)
+    _check_tensor("k", k, (B, Hkv, T, D), q.dtype)
+    q_out = torch.empty_like(q) if q_out is None else q_out
+    k_out = torch.empty_like(k) if k_out is None else k_out
+    _check_tensor("q_out", q_out, q.shape, q.dtype)
+    _check_tensor("k_out", k_out, k.shape, q.dtype)
+    b, bp = _base_array(base)
+    if theta is not None:
+        if theta.device.type != "cuda" or theta.dtype != torch.float32 or theta.numel() < 1:
+            raise ValueError("theta: a float32 device tensor")
+        nb = int(lib().fibattn_device_table_bytes())
+        table = torch.empty(nb, device=q.device, dtype=torch.uint8) if table is None else table
+        if table.numel() < nb or not table.is_contiguous():
+            raise ValueError(f"table: {nb} contiguous bytes")
+    st = lib().fibattn_rope_qk_table(q.data_ptr(), k.data_ptr(), q_out.data_ptr(), k_out.data_ptr(), B, H, Hkv,
+                                     T, D, ctypes.c_float(rope_base),
+                                     None if theta is None else theta.data_ptr(),
+                                     None if alpha is None else alpha.data_ptr(), bp, b.size, int(W),
+                                     None if table is None else table.data_ptr(), _dtype_code(q),
+                                     _stream(stream))
+    _check("fibattn_rope_qk_table", st)
+    return q_out, k_out, table
 
 
 def fibattn_timing_begin(kernel: str, capacity: int):

@@ -14,6 +14,10 @@
 #include "fibattn.h"
 
 static int bad = 0;
+static const int32_t *unsorted_base() {
+    static const int32_t b[3] = {5, 3, 8};
+    return b;
+}
 #define EXPECT(cond)                                                   \
     do {                                                               \
         if (!(cond)) { fprintf(stderr, "line %d: %s\n", __LINE__, #cond); bad = 1; } \
@@ -87,7 +91,13 @@ int main() {
     EXPECT(fibattn_device_table(fp, fib, 15, 8, nullptr, 0) == FIBATTN_ERR_INVALID_ARG);
     EXPECT(fibattn_device_table(fp, fib, 15, -1, p, 0) == FIBATTN_ERR_INVALID_ARG);
     EXPECT(fibattn_forward_dt(p, p, p, p, fp, 1, 2, 2, 64, 64, 8, nullptr, FIBATTN_BF16, 0) == FIBATTN_ERR_INVALID_ARG);
-    EXPECT(fibattn_backward_dt(p, p, p, p, fp, p, p, p, p, fp, p, 16, 1, 2, 2, 64, 64, 8, p, 0.f, FIBATTN_BF16,
+    EXPECT(fibattn_device_table_theta(nullptr, fp, fib, 15, 8, p, 0) == FIBATTN_ERR_INVALID_ARG);
+    EXPECT(fibattn_rope_qk_table(p, p, p, p, 1, 8, 3, 64, 64, 1e4f, nullptr, nullptr, fib, 15, 8, nullptr,
+                                 FIBATTN_BF16, 0) == FIBATTN_ERR_INVALID_ARG);
+    EXPECT(fibattn_rope_qk_table(p, p, p, p, 1, 8, 2, 64, 64, 1e4f, fp, nullptr, unsorted_base(), 3, 8, p,
+                                 FIBATTN_BF16, 0) == FIBATTN_ERR_INVALID_ARG);
+    EXPECT(fibattn_device_table_theta(fp, nullptr, fib, 15, 8, mis, 0) == FIBATTN_ERR_INVALID_ARG);
+    EXPECT(fibattn_backward_dt(p, p, p, p, fp, p, p, p, p, fp, nullptr, p, 16, 1, 2, 2, 64, 64, 8, p, 0.f, FIBATTN_BF16,
                                0) == FIBATTN_ERR_WORKSPACE);
     EXPECT(fibattn_alpha_from_theta(fp, fp, 0, 0) == FIBATTN_ERR_INVALID_ARG);
     EXPECT(fibattn_dtheta(fp, nullptr, fp, 4, 0) == FIBATTN_ERR_INVALID_ARG);

@@ -147,11 +147,20 @@ def test_invalid_arguments_return_codes_without_gpu():
     assert L.fibattn_device_table(16, bad, 3, 8, 16, None) == 1
     assert L.fibattn_device_table(None, b, 15, 8, 16, None) == 1
     assert L.fibattn_device_table(16, b, 15, 8, 18, None) == 1  # misaligned table
-    assert L.fibattn_device_table_bytes() >= 4 + 3 * 4 * 32
+    assert L.fibattn_device_table_bytes() >= 8 + 3 * 4 * 32 + 8
     assert L.fibattn_forward_dt(16, 16, 16, 16, 16, 1, 2, 2, 8, 64, 8, None, 1, None) == 1
     assert L.fibattn_forward_dt(16, 16, 16, 16, 16, 1, 8, 3, 8, 64, 8, 16, 1, None) == 1
-    assert L.fibattn_backward_dt(16, 16, 16, 16, 16, 16, 16, 16, 16, 16, None, 0,
+    assert L.fibattn_backward_dt(16, 16, 16, 16, 16, 16, 16, 16, 16, 16, None, None, 0,
                                  1, 1, 1, 8, 64, 8, 16, zero, 1, None) == 3
+    assert L.fibattn_device_table_theta(None, None, b, 15, 8, 16, None) == 1
+    # RoPE + table: H_kv must divide H; a theta needs an aligned table and a valid base
+    assert L.fibattn_rope_qk_table(16, 16, 16, 16, 1, 8, 3, 8, 64, ctypes.c_float(1e4), None, None, b, 15, 8,
+                                   None, 1, None) == 1
+    assert L.fibattn_rope_qk_table(16, 16, 16, 16, 1, 8, 2, 8, 64, ctypes.c_float(1e4), 16, None, b, 15, 8,
+                                   None, 1, None) == 1
+    assert L.fibattn_rope_qk_table(16, 16, 16, 16, 1, 8, 2, 8, 64, ctypes.c_float(0.5), None, None, b, 15, 8,
+                                   None, 1, None) == 1
+    assert L.fibattn_device_table_theta(16, None, b, 15, -1, 16, None) == 1
     assert L.fibattn_alpha_from_theta(16, 16, 0, None) == 1
     assert L.fibattn_dtheta(16, None, 16, 4, None) == 1
     for s in range(5):

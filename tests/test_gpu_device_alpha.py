@@ -123,6 +123,67 @@ def test_alpha_from_theta_and_dtheta():
     np.testing.assert_allclose(dt, da.cpu().numpy() * sg * (1 - sg), rtol=1e-6, atol=1e-7)
 
 
+@pytest.mark.parametrize("base,W", [(FIB, 8), (POW2, 10), (FIB, 20)])
+def test_table_from_theta_equals_table_from_alpha(base, W):
+    theta = torch.tensor(inputs.thetas(16, case=5).astype(np.float32), device="cuda")
+    for l in range(16):
+        a_ref = F.fibattn_alpha_from_theta(theta[l:l + 1])
+        t_ref = F.fibattn_device_table(a_ref, base, W)
+        a = torch.full((1,), float("nan"), device="cuda")
+        t = F.fibattn_device_table_theta(theta[l:l + 1], base, W, alpha=a)
+        torch.cuda.synchronize()
+        assert torch.equal(a, a_ref)
+        # the same table (n, W, d0, w, f); only the theta table records d alpha / d theta
+        assert torch.equal(t[:392], t_ref[:392])
+        sg = 1.0 / (1.0 + np.exp(-float(theta[l].item())))
+        assert t[392:400].cpu().numpy().view(np.float64)[0] == sg * (1.0 - sg)
+        assert np.isnan(t_ref[392:400].cpu().numpy().view(np.float64)[0])
+
+
+@pytest.mark.parametrize("dtype,D,W", [("bf16", 64, 8), ("fp32", 32, 8), ("bf16", 64, 20)])
+def test_backward_dtheta_equals_separate_dtheta(dtype, D, W):
+    # dtheta written by the backward (matrix-core and generic kernels) is bitwise the
+    # value fibattn_dtheta computes from the stored dalpha; a table built from alpha
+    # gives NaN
+    x = inputs.attention_inputs(1, 4, 200, D, dtype, 452, 0)
+    Q, K, V, G = (x[n].cuda() for n in ("q", "k", "v", "dO"))
+    theta = torch.tensor([0.37], device="cuda")
+    table = F.fibattn_device_table_theta(theta, FIB, W)
+    o, lse = F.fibattn_forward_dt(Q, K, V, W, table)
+    da, dth = torch.empty(1, device="cuda"), torch.full((1,), float("nan"), device="cuda")
+    F.fibattn_backward_dt(Q, K, V, o, lse, G, W, table, dalpha=da, dtheta=dth)
+    ref = F.fibattn_dtheta(theta, da)
+    torch.cuda.synchronize()
+    assert np.isfinite(float(dth.item())) and torch.equal(dth, ref)
+    table_a = F.fibattn_device_table(F.fibattn_alpha_from_theta(theta), FIB, W)
+    F.fibattn_backward_dt(Q, K, V, o, lse, G, W, table_a, dalpha=da, dtheta=dth)
+    torch.cuda.synchronize()
+    assert np.isnan(float(dth.item()))
+
+
+@pytest.mark.parametrize("dtype,D,H,Hkv", [("bf16", 64, 8, 2), ("bf16", 64, 4, 4), ("fp32", 32, 6, 3)])
+def test_rope_qk_table_equals_separate_launches(dtype, D, H, Hkv):
+    # RoPE of q and of k with fewer heads, and the table from theta, in one launch: the
+    # same bits as fibattn_rope on each tensor and fibattn_device_table_theta
+    x = inputs.attention_inputs(2, H, 300, D, dtype, 453, 0, names=("q",))
+    x.update(inputs.attention_inputs(2, Hkv, 300, D, dtype, 453, 0, names=("k",)))
+    q, k = x["q"].cuda(), x["k"].cuda()
+    theta = torch.tensor([-0.42], device="cuda")
+    alpha = torch.full((1,), float("nan"), device="cuda")
+    qo, ko, table = F.fibattn_rope_qk_table(q, k, 10000.0, theta=theta, base=FIB, W=8, alpha=alpha)
+    rq, rk = F.fibattn_rope(q, 10000.0), F.fibattn_rope(k, 10000.0)
+    ta = torch.full((1,), float("nan"), device="cuda")
+    tref = F.fibattn_device_table_theta(theta, FIB, 8, alpha=ta)
+    torch.cuda.synchronize()
+    assert torch.equal(qo, rq) and torch.equal(ko, rk)
+    assert torch.equal(table[:400], tref[:400]) and torch.equal(alpha, ta)
+    # without theta: RoPE only, the table untouched
+    t2 = torch.full_like(table, 7)
+    qo2, ko2, _ = F.fibattn_rope_qk_table(q, k, 10000.0, table=t2)
+    torch.cuda.synchronize()
+    assert torch.equal(qo2, rq) and torch.equal(ko2, rk) and bool((t2 == 7).all())
+
+
 def test_learned_alpha_step_in_a_graph():
     # theta (device) -> alpha -> rung table -> RoPE -> forward -> backward -> dtheta,
     # captured once and replayed with theta changed in place between replays: every
@@ -141,14 +202,12 @@ def test_learned_alpha_step_in_a_graph():
     ws = torch.empty(F.fibattn_backward_workspace_bytes(B, H, T, D, W, 0), device="cuda", dtype=torch.uint8)
     base = wl.calls[0].base
 
-    def step():
-        F.fibattn_alpha_from_theta(theta, alpha=alpha)
-        F.fibattn_device_table(alpha, base, W, table=table)
-        F.fibattn_rope_qk(q, k, 10000.0, q_out=qr, k_out=kr)
+    def step():  # RoPE, theta -> alpha and table in one launch; dtheta from the backward
+        F.fibattn_rope_qk_table(q, k, 10000.0, theta=theta, base=base, W=W, table=table, alpha=alpha,
+                                q_out=qr, k_out=kr)
         F.fibattn_forward_dt(qr, kr, v, W, table, o=o, lse=lse)
         F.fibattn_backward_dt(qr, kr, v, o, lse, dO, W, table, dq=dq, dk=dk, dv=dv, dalpha=da,
-                              workspace=ws, rope_base=10000.0)
-        F.fibattn_dtheta(theta, da, dtheta=dth)
+                              dtheta=dth, workspace=ws, rope_base=10000.0)
 
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
@@ -178,3 +237,5 @@ def test_learned_alpha_step_in_a_graph():
                 "bf16", f"graph replay {rep}")
         sg = 1.0 / (1.0 + np.exp(-float(np.float32(th))))
         assert abs(float(dth.item()) - got["dalpha"] * sg * (1 - sg)) <= 1e-5 * max(1.0, abs(got["dalpha"]))
+        # against the oracle: the chain rule through alpha = 0.5 + sigmoid(theta)
+        assert abs(float(dth.item()) - rda * sg * (1 - sg)) <= 2e-2 * max(1.0, abs(rda * sg * (1 - sg)))
