@@ -339,8 +339,15 @@ def gqa_figure(steps: int, warmup: int, eager: bool, kv_heads: int = 2):
         kms, n = kernel_time(F, sets, k, steps, 1)
         kt[k] = round(kms * n / steps, 6)  # per step
     qh = wl.queries_heads
+    # algorithmic bytes per query-head with G query heads per key/value head: the k, v
+    # (and dk, dv) terms shrink by G
+    G, D, s = wl.H // kv_heads, wl.D, 2 if wl.dtype == "bf16" else 4
+    grouped = {"forward": 2 * D * s + 2 * D * s // G + 4, "bwd_dq": 4 * D * s + 2 * D * s // G + 8,
+               "bwd_dkdv": 2 * D * s + 4 * D * s // G + 8, "rope": 2 * D * s + 2 * D * s // G}
+    frac = {k: round(grouped[k] * qh / (kt[k] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4) for k in grouped if kt.get(k)}
     return {"workload": wl.name, "H": wl.H, "H_kv": kv_heads, "ms_per_step": ms,
-            "value": qh / (ms * 1e-3), "kernels_ms_per_step": kt}
+            "value": qh / (ms * 1e-3), "kernels_ms_per_step": kt, "buffer_sets": len(sets),
+            "alg_bytes_per_qh": grouped, "kernels_frac": frac}
 
 
 def learned_alpha_figure(steps: int, warmup: int, eager: bool, layer: int = 0):

@@ -40,7 +40,10 @@ constexpr int kBwdB = 64;                // rows per workgroup
 // INTERP: some rung has w != 0 (rows r0 and r1 both loaded per rung).  DEV: the rung
 // table is the one at rtp, built on the device (rt_arg unused).  STRIDED: rows placed
 // by the layouts' position strides (else every row stride is 64, a constant).
-template <bool INTERP, bool DEV, bool STRIDED>
+// HS: query heads per workgroup, all reading one key/value head: the four waves are HS
+// heads times 4/HS runs of 16 queries at the same positions (as in the forward), so the
+// staged K, V rows serve every head of the group.
+template <bool INTERP, bool DEV, bool STRIDED, int HS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void bwd_dq_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     const uint16_t *__restrict__ o, const float *__restrict__ lse, const uint16_t *__restrict__ dO,
@@ -50,8 +53,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     const RungTable &rt = DEV ? *rtp : rt_arg;
     const bool bad = DEV && table_unusable(rt, W);  // bad device alpha, or another W
     // staged K, V rows [T0 - kLeadQ, T0 + 64): the band and, interpolating, the short rungs
+    constexpr int kQ = kBwdB / HS;  // queries per workgroup and head
     constexpr int kLeadQ = INTERP ? 32 : 16;
-    constexpr int kStage = kBwdB + kLeadQ;
+    constexpr int kStage = kQ + kLeadQ;
     __shared__ __align__(16) uint16_t kr[kStage * kD];
     __shared__ __align__(16) uint16_t vr[kStage * kD];
     __shared__ double sfreq[32];
@@ -61,15 +65,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     __shared__ uint32_t sterm[kMaxRungs * kBwdB];
 
     const int lane = threadIdx.x & 63;
-    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar work
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar work
+    const int wv = wave / HS;  // run of 16 queries
     const int nm = lane & 15, gm = lane >> 4;  // MFMA layout
     const int nq = lane >> 2, gq = lane & 3;   // quad layout
     // Raised issue priority while the prologue's loads and row copies are issued (as
     // in the forward); dk/dv keeps the default (measured slower at T = 4096).
     __builtin_amdgcn_s_setprio(2);
     const int blk = xcd_remap(blockIdx.x, gridDim.x);
-    const int bh = blk / tiles;
-    const int T0 = (blk % tiles) * kBwdB;
+    const int bh = (blk / tiles) * HS + wave % HS;  // this wave's query head
+    const int T0 = (blk % tiles) * kQ;
     const int bk = hd.kv_of(bh);
     const uint16_t *Q = q + head_at<STRIDED, kD>(lay.q, bh, hd.H, T);
     const uint16_t *K = k + head_at<STRIDED, kD>(lay.k, bk, hd.kv_heads(), T);
@@ -206,7 +211,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
         const float p = incl ? fast_exp2(sc * sl2 - lse2) : 0.f;
         const float cc = tau * p * (dP - delta);
         // (tau dS, p) of this entry for the dk/dv kernel (zeros for an excluded entry)
-        if (gq == 0) sterm[r * kBwdB + 16 * wv + nq] = pack_bf16(cc, p);
+        if (gq == 0) sterm[r * kBwdB + 16 * wave + nq] = pack_bf16(cc, p);
         if (INTERP)
             acc_axpy2(acc, cc * (1.f - w), x[0], cc * w, x[2]);
         else
@@ -237,7 +242,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     __builtin_amdgcn_wave_barrier();
     for (int r0 = 0; r0 < nact; r0 += 4) {
         const int r = r0 + (lane >> 4), qi = 16 * wv + (lane & 15);
-        if (r < nact && T0 + qi < T) terms.p[((size_t)bh * terms.planes + r) * T + T0 + qi] = sterm[r * kBwdB + qi];
+        if (r < nact && T0 + qi < T)
+            terms.p[((size_t)bh * terms.planes + r) * T + T0 + qi] = sterm[r * kBwdB + 16 * wave + (lane & 15)];
     }
 
     if (rf.on) acc_rope_t(acc, i, sfreq + 8 * gq);  // gradient w.r.t. the unrotated q
@@ -251,7 +257,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     double dal = (double)dal_q;
 #pragma unroll
     for (int st = 32; st >= 1; st >>= 1) dal += __shfl_xor(dal, st, 64);
-    if (lane == 0) red[wv] = dal;
+    if (lane == 0) red[wave] = dal;
     __syncthreads();
     if (threadIdx.x == 0) partials[blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
 }
@@ -586,6 +592,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 
 bool backward_mfma_supported(int dtype, int D, int W) { return dtype == 1 && D == 64 && W <= 16; }
 
+// (with HS heads per workgroup the dq grid has ceil(T / (64 / HS)) * BH / HS <= this many)
 size_t bwd_mfma_num_partials(int BH, int T) { return (size_t)((T + kBwdB - 1) / kBwdB) * (size_t)BH; }
 
 template <int NH>
@@ -620,17 +627,22 @@ hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, con
                                 const RungTerms &terms, int BH, const Heads &hd, int T, int W,
                                 const RungTable &rt, const RungTable *rtp, const RopeFreq &rf,
                                 const Layouts &lay, hipStream_t s) {
-    const int tiles = (T + kBwdB - 1) / kBwdB;
     const float tau = 1.f / sqrtf(64.f);
-    const int nb = tiles * BH;
     bool interp = rtp != nullptr;  // a device table may hold any weights
     for (int r = 0; r < rt.n && !interp; ++r) interp = rt.w[r] != 0.f;
     const bool strided = lay.q.st != kD || lay.k.st != kD || lay.v.st != kD || lay.o.st != kD ||
                          lay.g.st != kD || lay.dq.st != kD;
     if (rtp && strided) return hipErrorInvalidValue;  // device tables come with packed tensors
-    auto dqk = rtp ? bwd_dq_bf16_d64_kernel<true, true, false>
-             : strided ? (interp ? bwd_dq_bf16_d64_kernel<true, false, true> : bwd_dq_bf16_d64_kernel<false, false, true>)
-                       : (interp ? bwd_dq_bf16_d64_kernel<true, false, false> : bwd_dq_bf16_d64_kernel<false, false, false>);
+    // query heads per dq workgroup: the group's heads side by side for packed tensors with
+    // a host table (as the forward)
+    const int hs = (rtp || strided) ? 1 : hd.G % 4 == 0 ? 4 : hd.G % 2 == 0 ? 2 : 1;
+    const int tiles = (T + kBwdB / hs - 1) / (kBwdB / hs);  // runs of 64 / hs queries
+    const int nb = tiles * (BH / hs);                          // dq workgroups = dalpha partials
+    auto dqk = rtp ? bwd_dq_bf16_d64_kernel<true, true, false, 1>
+             : strided ? (interp ? bwd_dq_bf16_d64_kernel<true, false, true, 1> : bwd_dq_bf16_d64_kernel<false, false, true, 1>)
+             : hs == 4 ? (interp ? bwd_dq_bf16_d64_kernel<true, false, false, 4> : bwd_dq_bf16_d64_kernel<false, false, false, 4>)
+             : hs == 2 ? (interp ? bwd_dq_bf16_d64_kernel<true, false, false, 2> : bwd_dq_bf16_d64_kernel<false, false, false, 2>)
+                       : (interp ? bwd_dq_bf16_d64_kernel<true, false, false, 1> : bwd_dq_bf16_d64_kernel<false, false, false, 1>);
     hipError_t e = launch(kBwdDq, dqk, dim3(nb), dim3(256), 0, s, q, k, v, o, lse, dO, dq, delta_ws,
                           partials, terms, T, W, rt, rtp, rf, tau, tiles, hd, lay);
     if (e != hipSuccess) return e;

@@ -30,7 +30,11 @@ constexpr float kSlack = 8.f;              // log2 units a logit may exceed the 
 // INTERP: some rung has w != 0, so the second row r1 is read.  DEV: the rung table
 // is the one at rtp, built on the device (rt_arg unused).  STRIDED: rows are placed
 // by the layouts' position strides (else every row stride is 64, a constant).
-template <bool INTERP, bool DEV, bool STRIDED>
+// HS: query heads per workgroup, all reading one key/value head (grouped heads): the
+// four waves are HS heads times 4/HS runs of 16 queries at the same positions, so the
+// staged band rows serve every head of the group and the rung rows the heads gather
+// are the same addresses (HS = 1: one head, 64 queries).
+template <bool INTERP, bool DEV, bool STRIDED, int HS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void fwd_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     uint16_t *__restrict__ o, float *__restrict__ lse, int T, int W, RungTable rt_arg,
@@ -38,22 +42,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     const RungTable &rt = DEV ? *rtp : rt_arg;
     constexpr int RB = INTERP ? 1 : 2;  // rungs per load batch; two batches in flight
     constexpr int NS = INTERP ? 2 : 1;  // rows per rung (r0, and r1 when interpolating)
-    // staged rows [T0 - kLeadF, T0 + 64): the band and, interpolating, the short rungs
+    constexpr int kQ = kFwdBQ / HS;     // queries per workgroup and head
+    // staged rows [T0 - kLeadF, T0 + kQ): the band and, interpolating, the short rungs
     constexpr int kLeadF = INTERP ? 32 : 16;
-    constexpr int kBandRows = kFwdBQ + kLeadF;
+    constexpr int kBandRows = kQ + kLeadF;
     __shared__ __align__(16) uint16_t kr[kBandRows * kD];
     __shared__ __align__(16) uint16_t vr[kBandRows * kD];
 
     const int lane = threadIdx.x & 63;
-    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar work
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar work
+    const int wv = wave / HS;                  // run of 16 queries
     const int nm = lane & 15, gm = lane >> 4;  // MFMA layout
     const int nq = lane >> 2, gq = lane & 3;   // quad layout
     // Raised issue priority while this wave sets up and issues its row copies, so a
     // starting workgroup's loads are not queued behind resident waves' rung arithmetic.
     __builtin_amdgcn_s_setprio(2);
     const int blk = xcd_remap(blockIdx.x, gridDim.x);
-    const int bh = blk / tiles;
-    const int T0 = (blk % tiles) * kFwdBQ;
+    const int bh = (blk / tiles) * HS + wave % HS;  // this wave's query head
+    const int T0 = (blk % tiles) * kQ;
     const int bk = hd.kv_of(bh);
     const uint16_t *Q = q + head_at<STRIDED, kD>(lay.q, bh, hd.H, T);
     const uint16_t *K = k + head_at<STRIDED, kD>(lay.k, bk, hd.kv_heads(), T);
@@ -238,19 +244,26 @@ static bool any_interp(const RungTable &rt) {
 
 bool forward_mfma_supported(int dtype, int D, int W) { return dtype == 1 && D == 64 && W <= 16; }
 
+// Query heads per workgroup for G query heads per key/value head (packed tensors with a
+// host table; other launches take one head per workgroup).
+static int heads_per_wg(int G) { return G % 4 == 0 ? 4 : G % 2 == 0 ? 2 : 1; }
+
 hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void *o, float *lse,
                                int BH, const Heads &hd, int T, int W, const RungTable &rt,
                                const RungTable *rtp, const Layouts &lay, hipStream_t s) {
-    const int tiles = (T + kFwdBQ - 1) / kFwdBQ;
     const float sl2 = kLog2e / sqrtf(64.f);
     // device tables come with packed tensors only
     const bool strided = lay.q.st != kD || lay.k.st != kD || lay.v.st != kD || lay.o.st != kD;
     if (rtp && strided) return hipErrorInvalidValue;
     const bool interp = any_interp(rt);
-    auto kern = rtp ? fwd_bf16_d64_kernel<true, true, false>
-              : strided ? (interp ? fwd_bf16_d64_kernel<true, false, true> : fwd_bf16_d64_kernel<false, false, true>)
-                        : (interp ? fwd_bf16_d64_kernel<true, false, false> : fwd_bf16_d64_kernel<false, false, false>);
-    return launch(kForward, kern, dim3(tiles * BH), dim3(256), 0, s, q, k, v, o, lse, T, W, rt, rtp,
+    const int hs = (rtp || strided) ? 1 : heads_per_wg(hd.G);
+    const int tiles = (T + kFwdBQ / hs - 1) / (kFwdBQ / hs);  // runs of 64 / hs queries
+    auto kern = rtp ? fwd_bf16_d64_kernel<true, true, false, 1>
+              : strided ? (interp ? fwd_bf16_d64_kernel<true, false, true, 1> : fwd_bf16_d64_kernel<false, false, true, 1>)
+              : hs == 4 ? (interp ? fwd_bf16_d64_kernel<true, false, false, 4> : fwd_bf16_d64_kernel<false, false, false, 4>)
+              : hs == 2 ? (interp ? fwd_bf16_d64_kernel<true, false, false, 2> : fwd_bf16_d64_kernel<false, false, false, 2>)
+                        : (interp ? fwd_bf16_d64_kernel<true, false, false, 1> : fwd_bf16_d64_kernel<false, false, false, 1>);
+    return launch(kForward, kern, dim3(tiles * (BH / hs)), dim3(256), 0, s, q, k, v, o, lse, T, W, rt, rtp,
                   sl2, tiles, hd, lay);
 }
 
