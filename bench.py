@@ -20,6 +20,7 @@ import argparse
 import hashlib
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -57,16 +58,16 @@ def parse_args():
 # HBM traffic per launch of the layer_60m_fixed_T1024 kernels, from two rocprofv3 --pmc
 # passes (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) over
 #   bench.py --eager --steps 10 --warmup 2 --no-cpu-baseline --no-t4096 --no-gqa
-#            --no-learned-alpha --no-integer-offsets --copy-probe-mb 256
+#            --no-learned-alpha --no-integer-offsets --no-configs --copy-probe-mb 256
 # each scaled by what the same counter reads for the plain 256 MiB device copy of that run.
 # They hold only for the kernel sources they were taken on (COUNTER_SOURCES_SHA).
-COUNTER_SOURCES_SHA = "8b8e424c556dbf5b0502cf05bbe01adc1c42b6bf2bcce09b4ab3d7a2d3d38ef7"
+COUNTER_SOURCES_SHA = "2707019921cfd26ba1fec791ac864361142f6a30475efada9ec52685385d699e"
 COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
 COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
-    "forward": (12387.6, 8448.0),
-    "bwd_dq": (20787.9, 10417.0),
-    "bwd_dkdv": (18885.5, 16384.0),
-    "rope": (8228.8, 16384.0),
+    "forward": (12390.6, 8550.2),
+    "bwd_dq": (20793.6, 10424.2),
+    "bwd_dkdv": (18547.8, 16614.0),
+    "rope": (8236.5, 16384.0),
 }
 COPY_PROBE_KIB = (262144.0, 131092.6, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
 
@@ -383,21 +384,30 @@ def learned_alpha_figure(steps: int, warmup: int, eager: bool, layer: int = 0):
                                   rope_base=ROPE_BASE)
         dev.append(run_dev)
     out = {"workload": wl.name, "layer": layer, "alpha": float(call.alpha)}
+    runs = {}
     for tag, fns in (("device_alpha", dev), ("host_alpha", sets)):
         if eager:
             run = lambda i, fns=fns: fns[i % len(fns)]()  # noqa: E731
         else:
             gs = [capture(fn) for fn in fns]
             run = lambda i, gs=gs: gs[i % len(gs)].replay()  # noqa: E731
-        ms, _ = timed(run, steps, warmup)
+        runs[tag] = (fns, run)
+    # The two steps alternate over three rounds and the medians are reported: whichever
+    # is measured first otherwise carries the GPU's ramp-up (7% on one run).
+    ms_r = {tag: [] for tag in runs}
+    kt_r = {tag: {} for tag in runs}
+    for _ in range(3):
+        for tag, (fns, run) in runs.items():
+            ms_r[tag].append(timed(run, steps, warmup)[0])
+            for k in ("forward", "bwd_dq", "bwd_dkdv", "rope"):
+                kms, n = kernel_time(F, fns, k, steps, 1)
+                if n:
+                    kt_r[tag].setdefault(k, []).append(kms)
+    for tag in runs:
+        ms = statistics.median(ms_r[tag])
         out[tag + "_ms"] = ms
         out[tag + "_value"] = wl.queries_heads / (ms * 1e-3)
-        kt = {}
-        for k in ("forward", "bwd_dq", "bwd_dkdv", "alpha"):
-            kms, n = kernel_time(F, fns, k, steps, 1)
-            if n:
-                kt[k] = round(kms, 6)
-        out[tag + "_kernels_ms"] = kt
+        out[tag + "_kernels_ms"] = {k: round(statistics.median(v), 6) for k, v in kt_r[tag].items()}
     return out
 
 

@@ -154,6 +154,13 @@ __device__ __forceinline__ void rope_cs(int t, double inv_freq, float &c, float 
     sincosf((float)r, &s, &c);
 }
 
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+// 16-byte store that does not allocate in the caches (the outputs are not read again
+// by this kernel)
+__device__ __forceinline__ void nt_store16(void *p, uint4 x) {
+    __builtin_nontemporal_store(u32x4{x.x, x.y, x.z, x.w}, reinterpret_cast<u32x4 *>(p));
+}
+
 // ---- storage types -------------------------------------------------------
 // A lane moves 16 bytes of a row at a time: 4 float32 or 8 bfloat16 values.
 __device__ __forceinline__ float bf16_lo(uint32_t x) { return __uint_as_float(x << 16); }

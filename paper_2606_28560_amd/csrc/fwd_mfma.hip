@@ -70,6 +70,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
 
     const int t0 = T0 + 16 * wv;
     const int last = t0 + 15;  // the wave's last query
+    // rows [T0-kLeadF, T0+64) of K and V, straight to LDS (rows outside [0, T) are
+    // clamped copies: their keys are masked below).  They need no table entry, so they
+    // are issued before the wave waits for the rung table's scalar loads (strided rows:
+    // after the first rung batch, which keeps the strided instance free of spills).
+    auto stage_band = [&]() {
+        dma_rows<kBandRows>(kr, K, T0 - kLeadF, T, stk);
+        dma_rows<kBandRows>(vr, V, T0 - kLeadF, T, stv);
+    };
+    if constexpr (!STRIDED) stage_band();
     // rungs some query of this wave includes: a prefix of the table (sorted by d).  A
     // table in device memory is tested entry by entry unconditionally (entries past n are
     // zero), so it is fetched with a few wide scalar loads rather than a chain of
@@ -121,10 +130,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     };
     Slice kA[RB * NS], vA[RB * NS], kB[RB * NS], vB[RB * NS];
     if (0 < nact) load_batch(0, kA, vA, 1);  // in flight during the band phase
-    // rows [T0-kLeadF, T0+64) of K and V, straight to LDS (rows outside [0, T) are
-    // clamped copies: their keys are masked below)
-    dma_rows<kBandRows>(kr, K, T0 - kLeadF, T, stk);
-    dma_rows<kBandRows>(vr, V, T0 - kLeadF, T, stv);
+    if constexpr (STRIDED) stage_band();
     __builtin_amdgcn_s_setprio(0);
     wait_vmem();
     __syncthreads();
@@ -232,7 +238,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     if (i < T) {
         const bool bad = DEV && table_unusable(rt, W);  // bad device alpha, or another W
         store_acc(o + head_at<STRIDED, kD>(lay.o, bh, hd.H, T) + (size_t)i * sto, gq, acc, bad ? NAN : 1.f / l);
-        if (gq == 0) lse[(size_t)bh * T + i] = bad ? NAN : (m + log2f(l)) * kLn2;
+        if (gq == 0) __builtin_nontemporal_store(bad ? NAN : (m + log2f(l)) * kLn2, lse + (size_t)bh * T + i);
     }
 }
 

@@ -150,8 +150,8 @@ __device__ __forceinline__ void store_acc(uint16_t *row, int g, const Acc16 &acc
     b.y = pack_bf16(acc.c[2][2] * scale, acc.c[2][3] * scale);
     b.z = pack_bf16(acc.c[3][0] * scale, acc.c[3][1] * scale);
     b.w = pack_bf16(acc.c[3][2] * scale, acc.c[3][3] * scale);
-    *reinterpret_cast<uint4 *>(row + 8 * g) = a;
-    *reinterpret_cast<uint4 *>(row + 32 + 8 * g) = b;
+    nt_store16(row + 8 * g, a);
+    nt_store16(row + 32 + 8 * g, b);
 }
 
 // cos and sin of the angle 2 pi t fr (fr: revolutions per position): t fr is reduced to
