@@ -15,7 +15,7 @@ import torch
 import oracle
 from paper_2606_28560_amd import inputs, schedules, workloads
 from paper_2606_28560_amd import fibattn as F
-from tests.parity import compare, gpu_run, oracle_run
+from tests.parity import compare, gpu_run, oracle_run, rope_flip_size, rope_rounding_slack
 
 pytestmark = pytest.mark.gpu
 
@@ -167,10 +167,13 @@ def test_pipeline_with_rope(dtype, D, W, alpha):
     o, lse = F.fibattn_forward(Q, K, V, W, FIB, alpha)
     dq, dk, dv, da = F.fibattn_backward(Q, K, V, o, lse, G, W, FIB, alpha, rope_base=10000.0)
     torch.cuda.synchronize()
-    rq, rk = oracle.rope(x["q"]), oracle.rope(x["k"])
-    rq, rk = (inputs.round_to(r.astype(np.float32), dtype).double().numpy() for r in (rq, rk))
-    np.testing.assert_allclose(Q.double().cpu().numpy(), rq, atol=1e-5 if dtype == "fp32" else 0,
-                               rtol=0 if dtype == "fp32" else 2 ** -7)
+    eq, ek = oracle.rope(x["q"]), oracle.rope(x["k"])  # exact rotations
+    rq, rk = (inputs.round_to(r.astype(np.float32), dtype).double().numpy() for r in (eq, ek))
+    slack = rope_rounding_slack(x["q"].double().numpy(), x["k"].double().numpy(), eq, ek, dtype, W, FIB, alpha)
+    if dtype == "fp32":
+        np.testing.assert_allclose(Q.double().cpu().numpy(), rq, atol=1e-5, rtol=0)
+    else:  # the oracle's rounding, or the other neighbour where a float32 rotation may flip it
+        assert np.all(np.abs(Q.double().cpu().numpy() - rq) <= rope_flip_size(x["q"].double().numpy(), eq))
     ro, rl = oracle.forward(rq, rk, x["v"], W, FIB, alpha)
     rdq, rdk, rdv, rda, l1 = oracle.backward(rq, rk, x["v"], x["dO"], W, FIB, alpha)
     rdq, rdk = oracle.rope(rdq, transpose=True), oracle.rope(rdk, transpose=True)
@@ -178,7 +181,7 @@ def test_pipeline_with_rope(dtype, D, W, alpha):
     got = {kk: vv.double().cpu().numpy() for kk, vv in got.items()}
     got["dalpha"] = float(da.item())
     compare(got, {"o": ro, "lse": rl, "dq": rdq, "dk": rdk, "dv": rdv, "dalpha": rda, "l1": l1},
-            dtype, f"pipeline {dtype} D{D} W{W}")
+            dtype, f"pipeline {dtype} D{D} W{W}", lse_slack=slack)
 
 
 HEAD128 = [
@@ -206,8 +209,9 @@ def test_head_dim_128_rope_pipeline():
     o, lse = F.fibattn_forward(Q, K, V, 8, FIB, 0.9)
     dq, dk, dv, da = F.fibattn_backward(Q, K, V, o, lse, G, 8, FIB, 0.9, rope_base=10000.0)
     torch.cuda.synchronize()
-    rq, rk = oracle.rope(x["q"]), oracle.rope(x["k"])
-    rq, rk = (inputs.round_to(r.astype(np.float32), "bf16").double().numpy() for r in (rq, rk))
+    eq, ek = oracle.rope(x["q"]), oracle.rope(x["k"])  # exact rotations
+    rq, rk = (inputs.round_to(r.astype(np.float32), "bf16").double().numpy() for r in (eq, ek))
+    slack = rope_rounding_slack(x["q"].double().numpy(), x["k"].double().numpy(), eq, ek, "bf16", 8, FIB, 0.9)
     ro, rl = oracle.forward(rq, rk, x["v"], 8, FIB, 0.9)
     rdq, rdk, rdv, rda, l1 = oracle.backward(rq, rk, x["v"], x["dO"], 8, FIB, 0.9)
     rdq, rdk = oracle.rope(rdq, transpose=True), oracle.rope(rdk, transpose=True)
@@ -215,7 +219,7 @@ def test_head_dim_128_rope_pipeline():
            {"o": o, "lse": lse, "dq": dq, "dk": dk, "dv": dv}.items()}
     got["dalpha"] = float(da.item())
     compare(got, {"o": ro, "lse": rl, "dq": rdq, "dk": rdk, "dv": rdv, "dalpha": rda, "l1": l1},
-            "bf16", "d_head 128 pipeline")
+            "bf16", "d_head 128 pipeline", lse_slack=slack)
 
 
 GQA = [
@@ -317,8 +321,9 @@ def test_grouped_heads_pipeline_with_rope(dtype, D, W, alpha):
     o, lse = F.fibattn_forward(Q, K, V, W, FIB, alpha)
     dq, dk, dv, da = F.fibattn_backward(Q, K, V, o, lse, G, W, FIB, alpha, rope_base=10000.0)
     torch.cuda.synchronize()
-    rq, rk = oracle.rope(x["q"]), oracle.rope(x["k"])
-    rq, rk = (inputs.round_to(r.astype(np.float32), dtype).double().numpy() for r in (rq, rk))
+    eq, ek = oracle.rope(x["q"]), oracle.rope(x["k"])  # exact rotations
+    rq, rk = (inputs.round_to(r.astype(np.float32), dtype).double().numpy() for r in (eq, ek))
+    slack = rope_rounding_slack(x["q"].double().numpy(), x["k"].double().numpy(), eq, ek, dtype, W, FIB, alpha)
     ro, rl = oracle.forward(rq, rk, x["v"], W, FIB, alpha)
     rdq, rdk, rdv, rda, l1 = oracle.backward(rq, rk, x["v"], x["dO"], W, FIB, alpha)
     rdq, rdk = oracle.rope(rdq, transpose=True), oracle.rope(rdk, transpose=True)
@@ -326,7 +331,7 @@ def test_grouped_heads_pipeline_with_rope(dtype, D, W, alpha):
     got = {kk: vv.double().cpu().numpy() for kk, vv in got.items()}
     got["dalpha"] = float(da.item())
     compare(got, {"o": ro, "lse": rl, "dq": rdq, "dk": rdk, "dv": rdv, "dalpha": rda, "l1": l1},
-            dtype, f"gqa pipeline {dtype} D{D}")
+            dtype, f"gqa pipeline {dtype} D{D}", lse_slack=slack)
 
 
 def test_rope_qk_matches_two_single_launches():

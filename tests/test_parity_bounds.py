@@ -70,3 +70,46 @@ def test_tensor_bounds_reject_a_missing_row(full_ref):
         flat[r] = 0.0
         with pytest.raises(AssertionError):
             compare(g, ref, "bf16", f"{name} {t}")
+
+
+def _float32_rope(raw, base=10000.0):
+    """The rotation a float32 kernel computes (float64-reduced angle, cos/sin rounded to
+    float32, one fused multiply-add per output), before bfloat16 rounding: an emulation
+    independent of rope_flip_size, to check that it flags every flip such a kernel can
+    make."""
+    a = np.asarray(raw, dtype=np.float64)
+    B, H, T, D = a.shape
+    half = D // 2
+    ang = np.arange(T)[:, None] * base ** (-2.0 * np.arange(half) / D)[None, :]
+    r = (ang - 2 * np.pi * np.rint(ang / (2 * np.pi))).astype(np.float32).astype(np.float64)
+    c = np.cos(r).astype(np.float32).astype(np.float64)
+    s = np.sin(r).astype(np.float32).astype(np.float64)
+    u, v = a[..., :half], a[..., half:]
+    x0 = (u * c - (v * s).astype(np.float32)).astype(np.float32)
+    x1 = (v * c + (u * s).astype(np.float32)).astype(np.float32)
+    return np.concatenate([x0, x1], axis=-1).astype(np.float64)
+
+
+def test_rope_rounding_slack_covers_float32_rotation():
+    # every element where a float32 rotation rounds to a different bfloat16 value than the
+    # exact one is flagged, the lse of the flipped inputs stays within 1e-3 + slack, and
+    # most queries keep the plain 1e-3 bound (slack only where a flagged element is read)
+    import oracle
+    from tests.parity import TOL_BF16_LSE, rope_flip_size, rope_rounding_slack
+
+    x = inputs.attention_inputs(1, 4, 400, 64, "bf16", 412, 0)
+    raw_q, raw_k = x["q"].double().numpy(), x["k"].double().numpy()
+    eq, ek = oracle.rope(x["q"]), oracle.rope(x["k"])
+    rq, rk = (inputs.round_to(r.astype(np.float32), "bf16").double().numpy() for r in (eq, ek))
+    gq, gk = (inputs.round_to(_float32_rope(r).astype(np.float32), "bf16").double().numpy()
+              for r in (raw_q, raw_k))
+    assert (gq != rq).sum() + (gk != rk).sum() > 0  # the case exercises flips
+    for g, r, raw, e in ((gq, rq, raw_q, eq), (gk, rk, raw_k, ek)):
+        f = rope_flip_size(raw, e)
+        assert np.all(f[g != r] > 0)
+        assert np.all(np.abs(g - r) <= f + 1e-30)
+    slack = rope_rounding_slack(raw_q, raw_k, eq, ek, "bf16", 8, schedules.FIB15, 1.0)
+    _, l_ref = oracle.forward(rq, rk, x["v"], 8, schedules.FIB15, 1.0)
+    _, l_flip = oracle.forward(gq, gk, x["v"], 8, schedules.FIB15, 1.0)
+    assert np.all(np.abs(l_flip - l_ref) <= TOL_BF16_LSE + slack)
+    assert np.median(slack) < 1e-4 and (slack > TOL_BF16_LSE).mean() < 0.1
