@@ -282,9 +282,15 @@ def t4096_figure(steps: int, warmup: int, eager: bool):
     qh = wl.queries_heads
     from paper_2606_28560_amd import fibattn as F
     kt = {k: round(kernel_time(F, sets, k, steps, 1)[0], 6) for k in ("forward", "bwd_dq", "bwd_dkdv", "rope")}
+    # fwd+bwd compulsory bytes over the three attention kernels' summed launch durations
+    s = 2 if wl.dtype == "bf16" else 4
+    attn_ms = kt["forward"] + kt["bwd_dq"] + kt["bwd_dkdv"]
+    frac = alg_bytes("fwd+bwd", wl.D, s) * qh / (attn_ms * 1e-3) / 1e9 / PEAK_HBM_GBS
+    kfrac = {k: round(alg_bytes(k, wl.D, s) * qh / (kt[k] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4) for k in kt}
     return {"workload": wl.name, "alpha": float(call.alpha), "ms_per_step": ms,
             "value": qh / (ms * 1e-3), "fwd_only_ms": msf, "fwd_only_value": qh / (msf * 1e-3),
-            "kernels_mean_ms": kt}
+            "kernels_mean_ms": kt, "kernels_frac": kfrac, "attention_kernels_ms": attn_ms,
+            "attention_frac": round(frac, 4)}
 
 
 def integer_offsets_figure(steps: int, warmup: int, eager: bool, layer: int = 3):
