@@ -550,32 +550,31 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
 
     if constexpr (NH > 1) {
         // sum the head slots: slots 1.. hand their accumulators (quad layout, 32 floats
-        // per lane) to slot 0 of the same key group through the staging LDS
+        // per lane) to slot 0 of the same key group through the staging LDS, as eight
+        // 16-byte vectors per lane stored lane-minor (vector v of lane l at v * 64 + l),
+        // so a wave's 16-byte accesses cover consecutive banks (lane-major 128-byte
+        // blocks put every lane of an access on one bank: 6x the conflict cycles)
         static_assert(sizeof(stage) >= (size_t)(4 - kKG) * 64 * 32 * sizeof(float), "LDS for the sum");
-        float *xfer = reinterpret_cast<float *>(stage);
+        f32x4 *xfer = reinterpret_cast<f32x4 *>(stage);
         __syncthreads();  // every wave is done with the staged rows
         if (hs > 0) {
-            float *dst = xfer + ((size_t)(kg * (NH - 1) + hs - 1) * 64 + lane) * 32;
+            f32x4 *dst = xfer + (size_t)(kg * (NH - 1) + hs - 1) * 8 * 64 + lane;
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    dst[4 * c + e] = adk.c[c][e];
-                    dst[16 + 4 * c + e] = adv.c[c][e];
-                }
+            for (int c = 0; c < 4; ++c) {
+                dst[c * 64] = adk.c[c];
+                dst[(4 + c) * 64] = adv.c[c];
+            }
         }
         __syncthreads();
         if (hs == 0) {
 #pragma unroll 1
             for (int u = 1; u < NH; ++u) {
-                const float *src = xfer + ((size_t)(kg * (NH - 1) + u - 1) * 64 + lane) * 32;
+                const f32x4 *src = xfer + (size_t)(kg * (NH - 1) + u - 1) * 8 * 64 + lane;
 #pragma unroll
-                for (int c = 0; c < 4; ++c)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        adk.c[c][e] += src[4 * c + e];
-                        adv.c[c][e] += src[16 + 4 * c + e];
-                    }
+                for (int c = 0; c < 4; ++c) {
+                    adk.c[c] += src[c * 64];
+                    adv.c[c] += src[(4 + c) * 64];
+                }
             }
         }
     }
