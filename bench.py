@@ -61,15 +61,15 @@ def parse_args():
 #            --no-learned-alpha --no-integer-offsets --no-configs --copy-probe-mb 256
 # each scaled by what the same counter reads for the plain 256 MiB device copy of that run.
 # They hold only for the kernel sources they were taken on (COUNTER_SOURCES_SHA).
-COUNTER_SOURCES_SHA = "5f12290b9be79def35bac4b1f997da7899f4f8e7a3cccc28c41dedfa80979917"
+COUNTER_SOURCES_SHA = "0aa68feb44c86095affb2bf7b699f82e423d507dba8f382f342746122da60f5a"
 COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
 COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
-    "forward": (12390.6, 8551.2),
-    "bwd_dq": (20793.6, 10424.1),
-    "bwd_dkdv": (18794.5, 16610.6),
+    "forward": (12390.6, 8550.0),
+    "bwd_dq": (20800.6, 10427.5),
+    "bwd_dkdv": (18533.3, 16620.5),
     "rope": (8236.5, 16384.0),
 }
-COPY_PROBE_KIB = (262144.0, 131092.8, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
+COPY_PROBE_KIB = (262144.0, 131092.5, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
 
 
 def kernel_sources_sha() -> str:
