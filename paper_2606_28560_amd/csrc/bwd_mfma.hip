@@ -72,11 +72,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void b
     // Raised issue priority while the prologue's loads and row copies are issued (as
     // in the forward); dk/dv keeps the default (measured slower at T = 4096).
     __builtin_amdgcn_s_setprio(2);
-    // Each XCD serves its work items last-first: the forward (and dk/dv after this
-    // kernel) serve theirs first-first, and an XCD keeps the same heads in all three, so
-    // the tiles this kernel starts with are the ones the forward touched last and the
-    // tiles it ends with are the ones dk/dv starts with: their rows are still in the
-    // XCD's L2 (T = 1024 step -1 us, dk/dv -0.4 us; T = 4096 step -1.8 us).
+    // Each XCD serves its work items last-first, while dk/dv (the next kernel) serves its
+    // own first-first and an XCD keeps the same heads in both: the tiles dk/dv starts
+    // with are then the ones this kernel touched last, whose rows and rung terms are
+    // still in the XCD's L2 (dk/dv -0.4 us, T = 1024 step -1 us, T = 4096 step -1.8 us).
     int blk = xcd_remap(blockIdx.x, gridDim.x);
     if ((gridDim.x & 7) == 0) {
         const int per = gridDim.x >> 3, x = blk / per;
