@@ -61,15 +61,15 @@ def parse_args():
 #            --no-learned-alpha --no-integer-offsets --no-configs --copy-probe-mb 256
 # each scaled by what the same counter reads for the plain 256 MiB device copy of that run.
 # They hold only for the kernel sources they were taken on (COUNTER_SOURCES_SHA).
-COUNTER_SOURCES_SHA = "0aa68feb44c86095affb2bf7b699f82e423d507dba8f382f342746122da60f5a"
+COUNTER_SOURCES_SHA = "28757283bda056403acd89de5829807f70146373e34224ef8d2e89985bb8c59a"
 COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
 COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
-    "forward": (12390.6, 8550.0),
-    "bwd_dq": (20800.6, 10427.5),
-    "bwd_dkdv": (18533.3, 16620.5),
-    "rope": (8236.5, 16384.0),
+    "forward": (12390.6, 8550.5),
+    "bwd_dq": (20800.6, 10426.7),
+    "bwd_dkdv": (18507.5, 16610.2),
+    "rope": (8236.6, 16384.0),
 }
-COPY_PROBE_KIB = (262144.0, 131092.5, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
+COPY_PROBE_KIB = (262144.0, 131093.2, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
 
 
 def kernel_sources_sha() -> str:
