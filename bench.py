@@ -46,6 +46,8 @@ def parse_args():
     p.add_argument("--no-t4096", action="store_true", help="skip the T=4096 figure")
     p.add_argument("--no-gqa", action="store_true", help="skip the grouped-heads figure")
     p.add_argument("--no-learned-alpha", action="store_true", help="skip the device-alpha figure")
+    p.add_argument("--no-rope-on-load", action="store_true",
+                   help="skip the figure of RoPE applied to q inside the forward")
     p.add_argument("--no-integer-offsets", action="store_true",
                    help="skip the continuous vs rounded-offset stagger figure")
     p.add_argument("--no-configs", action="store_true",
@@ -96,15 +98,22 @@ def hbm_traffic(kernel: str, workload: str):
 def alg_bytes(kernel: str, D: int, s: int) -> int:
     return {
         "forward": 4 * D * s + 4,        # read q, k, v; write o, lse
+        "forward_rope_q": 5 * D * s + 4, # read raw q, k, v; write o, lse, R q
         "bwd_dq": 6 * D * s + 8,         # read q, k, v, o, dO, lse; write dq, Delta
         "bwd_dkdv": 6 * D * s + 8,       # read q, k, v, dO, lse, Delta; write dk, dv
         "rope": 4 * D * s,               # read q, k; write R q, R k (one launch)
+        "rope_k": 2 * D * s,             # read k; write R k
         "fwd+bwd": 12 * D * s + 8,       # forward + backward compulsory traffic
     }[kernel]
 
 
+# the library kernel timed under each timing id in a Step -> its algorithmic-bytes key
+STEP_ALG = {"forward": "forward_rope_q", "bwd_dq": "bwd_dq", "bwd_dkdv": "bwd_dkdv", "rope": "rope_k"}
+
+
 class Step:
-    """Buffers of one rotation set and the launches of one step."""
+    """Buffers of one rotation set and the launches of one step: RoPE of k, the forward
+    that rotates q where it loads it (writing R q for the backward), the backward."""
 
     def __init__(self, wl, call, set_index, kv_heads=None):
         import torch
@@ -131,12 +140,24 @@ class Step:
         self.ws = torch.empty(need, device=dev, dtype=torch.uint8)
 
     def forward(self):
+        self.forward_q_on_load(True)
+
+    def forward_two_launch(self):
+        # one RoPE launch for q and k, then the forward on the rotated rows
         F, c = self.F, self.call
         if self.grouped:  # q and k have different head counts (one launch for both)
             F.fibattn_rope_qk_table(self.q, self.k, ROPE_BASE, q_out=self.qr, k_out=self.kr)
         else:
             F.fibattn_rope_qk(self.q, self.k, ROPE_BASE, q_out=self.qr, k_out=self.kr)
         F.fibattn_forward(self.qr, self.kr, self.v, c.W, c.base, c.alpha, o=self.o, lse=self.lse)
+
+    def forward_q_on_load(self, keep_q: bool):
+        # RoPE of k alone, then the forward that rotates each query row where it loads it
+        # (keep_q: it also writes R q for a backward)
+        F, c = self.F, self.call
+        F.fibattn_rope(self.k, ROPE_BASE, out=self.kr)
+        F.fibattn_forward_rope_q(self.q, self.kr, self.v, c.W, c.base, c.alpha, ROPE_BASE, o=self.o,
+                                 lse=self.lse, q_out=self.qr if keep_q else None, keep_q=keep_q)
 
     def backward(self):
         # gradients w.r.t. the raw (unrotated) q, k: R^T is applied inside the backward
@@ -286,11 +307,56 @@ def t4096_figure(steps: int, warmup: int, eager: bool):
     s = 2 if wl.dtype == "bf16" else 4
     attn_ms = kt["forward"] + kt["bwd_dq"] + kt["bwd_dkdv"]
     frac = alg_bytes("fwd+bwd", wl.D, s) * qh / (attn_ms * 1e-3) / 1e9 / PEAK_HBM_GBS
-    kfrac = {k: round(alg_bytes(k, wl.D, s) * qh / (kt[k] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4) for k in kt}
+    kfrac = {k: round(alg_bytes(STEP_ALG[k], wl.D, s) * qh / (kt[k] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4) for k in kt}
     return {"workload": wl.name, "alpha": float(call.alpha), "ms_per_step": ms,
             "value": qh / (ms * 1e-3), "fwd_only_ms": msf, "fwd_only_value": qh / (msf * 1e-3),
             "kernels_mean_ms": kt, "kernels_frac": kfrac, "attention_kernels_ms": attn_ms,
             "attention_frac": round(frac, 4)}
+
+
+def rope_on_load_figure(steps: int, warmup: int, eager: bool, rounds: int = 3):
+    """RoPE applied to q where the forward loads it, against one RoPE launch for q and k
+    ahead of the forward: forward only (no R q written) at the T=1024 layer and at the
+    4x-length layer, and the T=1024 training step (R q written for the backward).  The
+    variants alternate over `rounds` rounds; medians."""
+    import statistics
+
+    import torch
+
+    from paper_2606_28560_amd import fibattn as F
+    from paper_2606_28560_amd import workloads
+
+    out = {}
+    cases = [("layer_60m_fixed_T1024", 0, True), ("extrap_coprime16_T4096", 1, False)]
+    for name, ci, train in cases:
+        wl = workloads.workload(name)
+        call = wl.calls[ci]
+        sets = [Step(wl, call, i) for i in range(buffer_sets(step_bytes(wl, call)))]
+        variants = {"two_launch_fwd": lambda st: st.forward_two_launch(),
+                    "on_load_fwd": lambda st: st.forward_q_on_load(False)}
+        if train:
+            variants["two_launch_step"] = lambda st: (st.forward_two_launch(), st.backward())
+            variants["on_load_step"] = lambda st: st()
+        runs = {}
+        for vname, fn in variants.items():
+            if eager:
+                runs[vname] = lambda i, fn=fn: fn(sets[i % len(sets)])
+            else:
+                gs = [capture(lambda st=st, fn=fn: fn(st)) for st in sets]
+                runs[vname] = lambda i, gs=gs: gs[i % len(gs)].replay()
+        res = {v: [] for v in variants}
+        for _ in range(rounds):
+            for vname in variants:
+                res[vname].append(timed(runs[vname], steps, warmup)[0])
+        fig = {v + "_ms": statistics.median(t) for v, t in res.items()}
+        # launch durations of the rotating forward and of the RoPE launch on k alone
+        fsets = [lambda st=st: st.forward_q_on_load(False) for st in sets]
+        fig["on_load_kernels_ms"] = {k: round(kernel_time(F, fsets, k, steps, 1)[0], 6) for k in ("forward", "rope")}
+        fig["alpha"] = float(call.alpha)
+        out[name] = fig
+        del sets, runs
+        torch.cuda.synchronize()
+    return out
 
 
 def integer_offsets_figure(steps: int, warmup: int, eager: bool, layer: int = 3):
@@ -326,8 +392,8 @@ def integer_offsets_figure(steps: int, warmup: int, eager: bool, layer: int = 3)
 
 def gqa_figure(steps: int, warmup: int, eager: bool, kv_heads: int = 2):
     """The 60M model's layer with its grouped key/value heads (8 query heads, 2 key/value
-    heads; B=8, T=1024, W=8, Fibonacci, alpha=1): the full step (RoPE of q and of k,
-    forward, backward) and per-kernel launch durations."""
+    heads; B=8, T=1024, W=8, Fibonacci, alpha=1): the full step (RoPE of k, the forward
+    rotating q on load, backward) and per-kernel launch durations."""
     from paper_2606_28560_amd import fibattn as F
     from paper_2606_28560_amd import workloads
 
@@ -349,8 +415,8 @@ def gqa_figure(steps: int, warmup: int, eager: bool, kv_heads: int = 2):
     # algorithmic bytes per query-head with G query heads per key/value head: the k, v
     # (and dk, dv) terms shrink by G
     G, D, s = wl.H // kv_heads, wl.D, 2 if wl.dtype == "bf16" else 4
-    grouped = {"forward": 2 * D * s + 2 * D * s // G + 4, "bwd_dq": 4 * D * s + 2 * D * s // G + 8,
-               "bwd_dkdv": 2 * D * s + 4 * D * s // G + 8, "rope": 2 * D * s + 2 * D * s // G}
+    grouped = {"forward": 3 * D * s + 2 * D * s // G + 4, "bwd_dq": 4 * D * s + 2 * D * s // G + 8,
+               "bwd_dkdv": 2 * D * s + 4 * D * s // G + 8, "rope": 2 * D * s // G}
     frac = {k: round(grouped[k] * qh / (kt[k] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4) for k in grouped if kt.get(k)}
     return {"workload": wl.name, "H": wl.H, "H_kv": kv_heads, "ms_per_step": ms,
             "value": qh / (ms * 1e-3), "kernels_ms_per_step": kt, "buffer_sets": len(sets),
@@ -542,14 +608,15 @@ def main():
     kt = {}
     for kname in ("forward", "bwd_dq", "bwd_dkdv", "rope"):
         kms, n = kernel_time(F, sets, kname, args.steps, 1)
-        kt[kname] = {"mean_ms": kms, "launches": n}
+        kt[kname] = {"mean_ms": kms, "launches": n,
+                     "frac": alg_bytes(STEP_ALG[kname], wl.D, s) * qh / (kms * 1e-3) / 1e9 / PEAK_HBM_GBS}
     per_step = {k: v["mean_ms"] for k, v in kt.items()}
     dom = max(per_step, key=per_step.get)
     units = qh  # query-heads per launch
-    achieved = alg_bytes(dom, wl.D, s) * units / (kt[dom]["mean_ms"] * 1e-3) / 1e9
+    achieved = alg_bytes(STEP_ALG[dom], wl.D, s) * units / (kt[dom]["mean_ms"] * 1e-3) / 1e9
     roofline = {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": hbm_traffic(dom, wl.name),
-                "bytes_per_launch": alg_bytes(dom, wl.D, s) * units,
+                "bytes_per_launch": alg_bytes(STEP_ALG[dom], wl.D, s) * units,
                 "mean_launch_ms": kt[dom]["mean_ms"]}
 
     result = {
@@ -567,7 +634,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "T": wl.T, "d_head": wl.D,
                    "W": call.W, "base": call.base_name, "alpha": float(call.alpha),
-                   "step": "rope(q,k) + forward + backward (dq, dk w.r.t. unrotated q, k)",
+                   "step": "rope(k) + forward rotating q on load + backward (dq, dk w.r.t. unrotated q, k)",
                    "launch": "eager" if args.eager else "hip_graph", "buffer_sets": nsets},
         "roofline": roofline,
         "attention_only": {"ms_per_step": ms_attn, "value": qh / (ms_attn * 1e-3),
@@ -582,6 +649,8 @@ def main():
         result["gqa"] = gqa_figure(max(5, args.steps // 4), 2, args.eager)
     if not args.no_learned_alpha:
         result["learned_alpha"] = learned_alpha_figure(max(5, args.steps // 4), 2, args.eager)
+    if not args.no_rope_on_load:
+        result["rope_on_load"] = rope_on_load_figure(max(5, args.steps // 4), 2, args.eager)
     if not args.no_integer_offsets:
         result["integer_offsets"] = integer_offsets_figure(max(5, args.steps // 4), 2, args.eager)
     if not args.no_configs:

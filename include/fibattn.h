@@ -160,6 +160,33 @@ fibattn_status_t fibattn_backward_gqa(const void *q, const void *k, const void *
                                       fibattn_dtype_t dtype, hipStream_t stream);
 
 /*
+ * The forward with RoPE applied to the queries where they are loaded (Section 2
+ * "Attended set": rotary embeddings at the true positions, before the gather).  As
+ * fibattn_forward_gqa, except that
+ *   q     : the UNROTATED queries, dtype, [B,H,T,d_head] (read)
+ *   k     : the keys already rotated (fibattn_rope, same rope_base), [B,H_kv,T,d_head]
+ *   q_out : nullable; R q, dtype, [B,H,T,d_head] (written; may be q itself), the rotated
+ *           queries a later fibattn_backward_gqa(..., rope_base) takes as q.  NULL
+ *           (forward-only callers) writes nothing beyond o and lse.
+ *   rope_base : > 1 and finite (else FIBATTN_ERR_INVALID_ARG); pairing and angles as
+ *           fibattn_rope
+ * A query row is read by its own query only, so it is rotated inside the forward at no
+ * extra row traffic; a key row is read by up to 1 + W + K queries and is rotated once,
+ * by the RoPE launch.  o and lse are those of fibattn_forward_gqa on (R q, k, v).
+ * bfloat16 with d_head 64 and W <= 16 is one launch; its cos and sin come from the
+ * hardware units (absolute error <= 2.3e-7 with the angle's float32 rounding, against
+ * ~1e-7 for fibattn_rope), so an element of q_out can differ from fibattn_rope's by one
+ * bfloat16 rounding step where the exact value lies that close to a rounding midpoint.
+ * Other shapes run the RoPE launch on q into q_out, then the forward (q_out NULL:
+ * FIBATTN_ERR_UNSUPPORTED).
+ */
+fibattn_status_t fibattn_forward_rope_q(const void *q, const void *k, const void *v,
+                                        void *o, float *lse, void *q_out,
+                                        int B, int H, int H_kv, int T, int d_head, int W,
+                                        const int32_t *base, int K, float alpha, float rope_base,
+                                        fibattn_dtype_t dtype, hipStream_t stream);
+
+/*
  * Tensors in any placement whose rows are contiguous, e.g. q, k, v taken straight out
  * of a [B, T, H, d_head] or a packed [B, T, 3, H, d_head] projection output, without a
  * copy.  A layout gives element strides: element (b, h, t, c) of a [B, heads, T,

@@ -191,6 +191,42 @@ fibattn_status_t fibattn_forward(const void *q, const void *k, const void *v, vo
     return fibattn_forward_gqa(q, k, v, o, lse, B, H, H, T, d_head, W, base, K, alpha, dtype, stream);
 }
 
+fibattn_status_t fibattn_forward_rope_q(const void *q, const void *k, const void *v, void *o,
+                                        float *lse, void *q_out, int B, int H, int H_kv, int T,
+                                        int d_head, int W, const int32_t *base, int K, float alpha,
+                                        float rope_base, fibattn_dtype_t dtype, hipStream_t stream) {
+    fibattn_status_t st = check_common(B, H, T, d_head, W, K, dtype);
+    if (st != FIBATTN_OK) return st;
+    if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
+    if (!q || !k || !v || !o || !lse) return FIBATTN_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse) ||
+        !aligned16(q_out))
+        return FIBATTN_ERR_INVALID_ARG;
+    if (!(rope_base > 1.f) || !isfinite(rope_base)) return FIBATTN_ERR_INVALID_ARG;
+    const bool on_load = forward_mfma_supported((int)dtype, d_head, W);
+    if (!on_load && !q_out) return FIBATTN_ERR_UNSUPPORTED;  // the rotated rows need a home
+    RungTable rt;
+    st = build_table(alpha, base, K, W, &rt);
+    if (st != FIBATTN_OK) return st;
+    const Heads hd{H, H / H_kv};
+    const Layouts lay = packed_layouts(H, H_kv, T, d_head);
+    hipError_t e;
+    if (on_load) {
+        // one launch: each query row is rotated where the forward loads it
+        const RopeFreq rf = make_rope_freq((double)rope_base, d_head);
+        e = launch_forward_mfma(q, k, v, o, lse, B * H, hd, T, W, rt, nullptr, lay, stream, &rf, q_out);
+    } else {
+        // the RoPE launch on q into q_out, then the forward on it
+        const Layout l = Layout::packed(H, T, d_head);
+        e = launch_rope((int)dtype, d_head, q, q_out, l, l, nullptr, nullptr, l, l, B * H, H, T, rope_base,
+                        0, stream);
+        if (e == hipSuccess)
+            e = launch_forward((int)dtype, d_head, q_out, k, v, o, lse, B * H, hd, T, W, rt, nullptr, lay,
+                               stream);
+    }
+    return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
 // Backward workspace: Delta (float32 [B,H,T]), then the per-workgroup dalpha partials
 // (float64; sized for the larger of the two dtypes' partial counts), then, for shapes
 // the matrix-core path may take (d_head 64, W <= 16), its per-(query, rung) terms:

@@ -34,11 +34,19 @@ constexpr float kSlack = 8.f;              // log2 units a logit may exceed the 
 // four waves are HS heads times 4/HS runs of 16 queries at the same positions, so the
 // staged band rows serve every head of the group and the rung rows the heads gather
 // are the same addresses (HS = 1: one head, 64 queries).
-template <bool INTERP, bool DEV, bool STRIDED, int HS>
+// RQ: q holds the raw (unrotated) queries and k the rotated keys.  Each lane rotates its
+// own slice of its query row at the query's position (RoPE, Section 2 "Attended set"),
+// attends with the rotated row and, when qrot is not null, writes it there for the
+// backward.  A query row is used by one query only, so rotating it where it is loaded
+// costs no extra row traffic; a key row is read by up to 1 + W + K queries and stays
+// with the RoPE launch.  rf: the RoPE frequencies (unused without RQ).
+template <bool INTERP, bool DEV, bool STRIDED, int HS, bool RQ>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void fwd_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
     uint16_t *__restrict__ o, float *__restrict__ lse, int T, int W, RungTable rt_arg,
-    const RungTable *__restrict__ rtp, float sl2, int tiles, Heads hd, Layouts lay) {
+    const RungTable *__restrict__ rtp, float sl2, int tiles, Heads hd, Layouts lay,
+    uint16_t *qrot, RopeFreq rf) {
+    static_assert(!RQ || (!DEV && !STRIDED), "rotation on load: packed tensors, host table");
     const RungTable &rt = DEV ? *rtp : rt_arg;
     constexpr int RB = INTERP ? 1 : 2;  // rungs per load batch; two batches in flight
     constexpr int NS = INTERP ? 2 : 1;  // rows per rung (r0, and r1 when interpolating)
@@ -48,6 +56,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     constexpr int kBandRows = kQ + kLeadF;
     __shared__ __align__(16) uint16_t kr[kBandRows * kD];
     __shared__ __align__(16) uint16_t vr[kBandRows * kD];
+    __shared__ double sfreq[RQ ? 32 : 1];  // RoPE frequencies, revolutions per position
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar work
@@ -100,7 +109,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     const int im = t0 + nm;  // query of this lane in the MFMA layout
     const int i = t0 + nq;   // ... in the quad layout
     const int ic = min(i, T - 1);
-    const Slice qq = load_row(Q, ic, gq, stq);
+    Slice qq = load_row(Q, ic, gq, stq);  // raw with RQ, rotated after the wait below
+    // RQ: cos and sin of the lane's eight angles (its query's position, frequencies
+    // 8 gq .. 8 gq + 7), evaluated while the row copies are in flight
+    float rc[RQ ? 8 : 1], rs[RQ ? 8 : 1];
+    if constexpr (RQ) {
+        stage_freq(sfreq, rf);
+        __syncthreads();
+#pragma unroll
+        for (int d = 0; d < 8; ++d) rope_cs_rev(i, sfreq[8 * gq + d], rc[d], rs[d]);
+    }
 
     // rung rows of a batch: kx[x*NS + s], vx[x*NS + s] = row r_s of rung rb + x
     // (from LDS for the first nlds rungs, else from global memory; `which` selects
@@ -135,6 +153,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     wait_vmem();
     __syncthreads();
     if (0 < nact) load_batch(0, kA, vA, 2);
+    if constexpr (RQ) {
+        // rotate-half pairs (8g + d, 32 + 8g + d) are slice positions d and d + 8: word w
+        // of a holds d = 2w, 2w + 1, word w of b their partners
+        uint32_t aw[4] = {qq.a.x, qq.a.y, qq.a.z, qq.a.w}, bw[4] = {qq.b.x, qq.b.y, qq.b.z, qq.b.w};
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            float x0, y0, x1, y1;
+            rope_rotate(bf16_lo(aw[w]), bf16_lo(bw[w]), rc[2 * w], rs[2 * w], x0, y0);
+            rope_rotate(bf16_hi(aw[w]), bf16_hi(bw[w]), rc[2 * w + 1], rs[2 * w + 1], x1, y1);
+            aw[w] = f32_to_bf16(x0) | (f32_to_bf16(x1) << 16);
+            bw[w] = f32_to_bf16(y0) | (f32_to_bf16(y1) << 16);
+        }
+        qq.a = make_uint4(aw[0], aw[1], aw[2], aw[3]);
+        qq.b = make_uint4(bw[0], bw[1], bw[2], bw[3]);
+        if (qrot && i < T) {  // read by the backward: ordinary stores
+            uint16_t *qr = qrot + ((size_t)bh * T + i) * kD;
+            *reinterpret_cast<uint4 *>(qr + 8 * gq) = qq.a;
+            *reinterpret_cast<uint4 *>(qr + 32 + 8 * gq) = qq.b;
+        }
+    }
 
     // ---- window band (MFMA layout): logits (log2 units), maximum, probabilities ----
     const Slice qm = slice_from_quad(qq, lane);  // the wave's q rows in the MFMA layout
@@ -256,21 +294,29 @@ static int heads_per_wg(int G) { return G % 4 == 0 ? 4 : G % 2 == 0 ? 2 : 1; }
 
 hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void *o, float *lse,
                                int BH, const Heads &hd, int T, int W, const RungTable &rt,
-                               const RungTable *rtp, const Layouts &lay, hipStream_t s) {
+                               const RungTable *rtp, const Layouts &lay, hipStream_t s,
+                               const RopeFreq *rq, void *q_rot) {
     const float sl2 = kLog2e / sqrtf(64.f);
-    // device tables come with packed tensors only
+    // device tables and rotation on load come with packed tensors only
     const bool strided = lay.q.st != kD || lay.k.st != kD || lay.v.st != kD || lay.o.st != kD;
-    if (rtp && strided) return hipErrorInvalidValue;
+    if ((rtp || rq) && strided) return hipErrorInvalidValue;
+    if (rq && rtp) return hipErrorInvalidValue;
     const bool interp = any_interp(rt);
     const int hs = (rtp || strided) ? 1 : heads_per_wg(hd.G);
     const int tiles = (T + kFwdBQ / hs - 1) / (kFwdBQ / hs);  // runs of 64 / hs queries
-    auto kern = rtp ? fwd_bf16_d64_kernel<true, true, false, 1>
-              : strided ? (interp ? fwd_bf16_d64_kernel<true, false, true, 1> : fwd_bf16_d64_kernel<false, false, true, 1>)
-              : hs == 4 ? (interp ? fwd_bf16_d64_kernel<true, false, false, 4> : fwd_bf16_d64_kernel<false, false, false, 4>)
-              : hs == 2 ? (interp ? fwd_bf16_d64_kernel<true, false, false, 2> : fwd_bf16_d64_kernel<false, false, false, 2>)
-                        : (interp ? fwd_bf16_d64_kernel<true, false, false, 1> : fwd_bf16_d64_kernel<false, false, false, 1>);
+#define FIBATTN_FWD(I, H, R) fwd_bf16_d64_kernel<I, false, false, H, R>
+#define FIBATTN_FWD_HS(R)                                                                        \
+    (hs == 4   ? (interp ? FIBATTN_FWD(true, 4, R) : FIBATTN_FWD(false, 4, R))                \
+     : hs == 2 ? (interp ? FIBATTN_FWD(true, 2, R) : FIBATTN_FWD(false, 2, R))                \
+               : (interp ? FIBATTN_FWD(true, 1, R) : FIBATTN_FWD(false, 1, R)))
+    auto kern = rtp ? fwd_bf16_d64_kernel<true, true, false, 1, false>
+              : strided ? (interp ? fwd_bf16_d64_kernel<true, false, true, 1, false>
+                                  : fwd_bf16_d64_kernel<false, false, true, 1, false>)
+              : rq ? FIBATTN_FWD_HS(true) : FIBATTN_FWD_HS(false);
+#undef FIBATTN_FWD_HS
+#undef FIBATTN_FWD
     return launch(kForward, kern, dim3(tiles * (BH / hs)), dim3(256), 0, s, q, k, v, o, lse, T, W, rt, rtp,
-                  sl2, tiles, hd, lay);
+                  sl2, tiles, hd, lay, (uint16_t *)q_rot, rq ? *rq : RopeFreq{});
 }
 
 }  // namespace fibattn

@@ -154,17 +154,6 @@ __device__ __forceinline__ void store_acc(uint16_t *row, int g, const Acc16 &acc
     nt_store16(row + 32 + 8 * g, b);
 }
 
-// cos and sin of the angle 2 pi t fr (fr: revolutions per position): t fr is reduced to
-// [-1/2, 1/2] in float64 and evaluated on the hardware sine and cosine units, whose
-// inputs are in revolutions (max absolute error 1.3e-7, measured over 2^24 points of
-// [-1/2, 1/2]; the float32 rounding of the reduced angle adds at most 2 pi 2^-26).
-__device__ __forceinline__ void rope_cs_rev(int t, double fr, float &c, float &s) {
-    const double a = (double)t * fr;
-    const float r = (float)(a - rint(a));
-    s = __builtin_amdgcn_sinf(r);
-    c = __builtin_amdgcn_cosf(r);
-}
-
 // R^T (the inverse RoPE rotation) at position t on the lane's slice: slice positions
 // d and d + 8 hold the rotate-half pair (8g + d, 32 + 8g + d); rev8 points at the
 // eight frequencies (in revolutions per position) of lane group g.

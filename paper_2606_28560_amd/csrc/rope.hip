@@ -63,14 +63,14 @@ __global__ __launch_bounds__(256) void rope_kernel(const S *x, S *y, int BH, int
     }
 }
 
-// bfloat16, d_head 64: a workgroup owns 8 positions of 16 (b, h) rows (128 rows; each
-// lane group of four handles two positions, t and t + 4, of one head, so two rows'
-// loads are in flight per lane: 10.7 -> 10.2 us for q and k of the 60M layer).
+// bfloat16, d_head 64: a workgroup owns 4 NP positions of 16 (b, h) rows; each lane group
+// of four handles NP positions (t, t + 4) of one head.  NP = 2 for two tensors (two rows'
+// loads in flight per lane: 10.7 -> 10.2 us for q and k of the 60M layer); NP = 1 for one
+// tensor, which doubles the workgroup count of that smaller launch.
 // Lane group g of a row's four lanes holds dims [8g, 8g+8) and [32+8g, 32+8g+8),
 // i.e. the eight rotate-half pairs (j, j+32), j in [8g, 8g+8): two 16-byte loads
 // and stores per lane and row, reading 64 contiguous bytes per row per instruction.
 // The loads are issued before the angles are evaluated.
-constexpr int kRope64TP = 8;
 constexpr int kRope64RB = 16;
 
 // blockIdx.z selects the tensor: (x0 -> y0) or (x1 -> y1), each with its own row count
@@ -80,11 +80,12 @@ struct RopeIO {
     Layout x, y;
     int BH, heads;
 };
-template <bool STRIDED>
+template <bool STRIDED, int NP>
 __global__ __launch_bounds__(256) void rope_bf16_d64_kernel(const uint16_t *x0, uint16_t *y0,
                                                             const uint16_t *x1, uint16_t *y1,
                                                             int T, RopeFreq rf, int transpose,
                                                             RopeIO io0, RopeIO io1, TableJob job) {
+    constexpr int kRope64TP = 4 * NP;  // positions per workgroup
     __shared__ float cs[kRope64TP * 32], sn[kRope64TP * 32];
     const uint16_t *x = blockIdx.z ? x1 : x0;
     uint16_t *y = blockIdx.z ? y1 : y0;
@@ -98,11 +99,11 @@ __global__ __launch_bounds__(256) void rope_bf16_d64_kernel(const uint16_t *x0, 
     const int rr = threadIdx.x >> 2;  // 0..63
     const int bh = blockIdx.y * kRope64RB + (rr >> 2);
     const int bhc = min(bh, BH - 1);
-    uint4 a[2], b[2];
-    const uint16_t *xr[2];
-    uint16_t *yr[2];
+    uint4 a[NP], b[NP];
+    const uint16_t *xr[NP];
+    uint16_t *yr[NP];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {  // positions t0 + (rr & 3) and t0 + (rr & 3) + 4
+    for (int h = 0; h < NP; ++h) {  // positions t0 + (rr & 3) (and t0 + (rr & 3) + 4)
         const int tc = min(t0 + (rr & 3) + 4 * h, T - 1);
         const size_t packed = ((size_t)bhc * T + tc) * 64;
         xr[h] = x + (STRIDED ? io.x.head(bhc, heads) + (long long)tc * io.x.st : packed);
@@ -110,7 +111,7 @@ __global__ __launch_bounds__(256) void rope_bf16_d64_kernel(const uint16_t *x0, 
         a[h] = *reinterpret_cast<const uint4 *>(xr[h] + 8 * g);
         b[h] = *reinterpret_cast<const uint4 *>(xr[h] + 32 + 8 * g);
     }
-    {
+    if (threadIdx.x < kRope64TP * 32) {
         float c, sv;
         rope_cs(t0 + (threadIdx.x >> 5), rf.inv[threadIdx.x & 31], c, sv);
         cs[threadIdx.x] = c;
@@ -119,7 +120,7 @@ __global__ __launch_bounds__(256) void rope_bf16_d64_kernel(const uint16_t *x0, 
     __syncthreads();
     if (bh >= BH) return;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < NP; ++h) {
         const int tt = (rr & 3) + 4 * h;
         if (t0 + tt >= T) continue;
         const uint32_t aw[4] = {a[h].x, a[h].y, a[h].z, a[h].w}, bw[4] = {b[h].x, b[h].y, b[h].z, b[h].w};
@@ -184,9 +185,11 @@ hipError_t launch_rope(int dtype, int D, const void *x0, void *y0, const Layout 
         const bool strided = !same(lx0, heads) || !same(ly0, heads) ||
                              (x1 && (!same(lx1, heads1) || !same(ly1, heads1)));
         const int rows = x1 ? max(BH, BH1) : BH;
-        return launch(kRope, strided ? rope_bf16_d64_kernel<true> : rope_bf16_d64_kernel<false>,
-                      dim3((T + kRope64TP - 1) / kRope64TP, (rows + kRope64RB - 1) / kRope64RB,
-                           x1 ? 2 : 1),
+        const int tp = x1 ? 8 : 4;  // positions per workgroup
+        auto kern = x1 ? (strided ? rope_bf16_d64_kernel<true, 2> : rope_bf16_d64_kernel<false, 2>)
+                       : (strided ? rope_bf16_d64_kernel<true, 1> : rope_bf16_d64_kernel<false, 1>);
+        return launch(kRope, kern,
+                      dim3((T + tp - 1) / tp, (rows + kRope64RB - 1) / kRope64RB, x1 ? 2 : 1),
                       dim3(256), 0, s, x0, y0, x1, y1, T, rf, transpose, RopeIO{lx0, ly0, BH, heads},
                       RopeIO{lx1, ly1, BH1, heads1}, tj);
     }

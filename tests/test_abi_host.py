@@ -142,6 +142,16 @@ def test_invalid_arguments_return_codes_without_gpu():
         assert L.fibattn_forward_gqa(16, 16, 16, 16, 16, 1, 8, hkv, 8, 64, 8, b, 15, one, 1, None) == 1
         assert L.fibattn_backward_gqa(16, 16, 16, 16, 16, 16, 16, 16, 16, 16, 16, 1 << 30,
                                       1, 8, hkv, 8, 64, 8, b, 15, one, zero, 1, None) == 1
+    # queries rotated on load: q_out aligned or null, rope_base > 1, H_kv dividing H; a null
+    # q_out only where the rotation runs inside the forward (bf16, d_head 64, W <= 16)
+    rq, r4 = L.fibattn_forward_rope_q, ctypes.c_float(1e4)
+    assert rq(16, 16, 16, 16, 16, 18, 1, 8, 8, 8, 64, 8, b, 15, one, r4, 1, None) == 1
+    assert rq(16, 16, 16, 16, 16, 16, 1, 8, 8, 8, 64, 8, b, 15, one, ctypes.c_float(1.0), 1, None) == 1
+    assert rq(16, 16, 16, 16, 16, 16, 1, 8, 3, 8, 64, 8, b, 15, one, r4, 1, None) == 1
+    assert rq(None, 16, 16, 16, 16, 16, 1, 8, 8, 8, 64, 8, b, 15, one, r4, 1, None) == 1
+    assert rq(16, 16, 16, 16, 16, 16, 1, 8, 8, 8, 48, 8, b, 15, one, r4, 1, None) == 2
+    assert rq(16, 16, 16, 16, 16, None, 1, 8, 8, 8, 64, 8, b, 15, one, r4, 0, None) == 2   # float32
+    assert rq(16, 16, 16, 16, 16, None, 1, 8, 8, 8, 64, 20, b, 15, one, r4, 1, None) == 2  # W > 16
     # device alpha: the base table is checked on the host, pointers before any launch
     bad = (ctypes.c_int32 * 3)(5, 3, 8)
     assert L.fibattn_device_table(16, bad, 3, 8, 16, None) == 1

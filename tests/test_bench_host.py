@@ -21,6 +21,10 @@ def test_algorithmic_bytes_per_query_head():
     assert bench.alg_bytes("fwd+bwd", 64, 2) == 1544
     assert bench.alg_bytes("bwd_dq", 64, 2) == bench.alg_bytes("bwd_dkdv", 64, 2) == 776
     assert bench.alg_bytes("rope", 64, 2) == 512
+    # the step's forward rotates q on load: it also writes R q; its RoPE launch takes k only
+    assert bench.alg_bytes("forward_rope_q", 64, 2) == 516 + 128
+    assert bench.alg_bytes("rope_k", 64, 2) == 256
+    assert set(bench.STEP_ALG) == {"forward", "bwd_dq", "bwd_dkdv", "rope"}
     # float32 with d_head 32 moves the same bytes per query-head
     assert bench.alg_bytes("fwd+bwd", 32, 4) == 1544
 

@@ -184,6 +184,82 @@ def test_pipeline_with_rope(dtype, D, W, alpha):
             dtype, f"pipeline {dtype} D{D} W{W}", lse_slack=slack)
 
 
+ROPE_Q = [
+    # (B, H, H_kv, T, D, dtype, W, alpha): bf16 with d_head 64 and W <= 16 rotates q inside
+    # the forward (1, 2 or 4 query heads per workgroup, integer and interpolated offsets,
+    # ragged tails, a single position, the window limit); the other shapes run the RoPE
+    # launch on q, then the forward
+    (2, 2, 2, 300, 64, "bf16", 8, 1.0),
+    (1, 3, 3, 333, 64, "bf16", 8, 0.85),
+    (1, 8, 2, 300, 64, "bf16", 12, 1.0),
+    (1, 4, 2, 257, 64, "bf16", 16, 0.9),
+    (1, 2, 2, 1, 64, "bf16", 0, 1.0),
+    (1, 2, 2, 200, 64, "fp32", 8, 0.85),
+    (1, 2, 1, 150, 128, "bf16", 8, 1.0),
+]
+
+
+@pytest.mark.parametrize("B,H,Hkv,T,D,dtype,W,alpha", ROPE_Q)
+def test_forward_rotating_q_on_load(B, H, Hkv, T, D, dtype, W, alpha):
+    # raw q and rotated k -> the forward that rotates q itself -> the backward with R^T
+    # fused; the oracle runs the same chain on its own rotations, rounded to the storage
+    # dtype (the lse bound allows for the rounding flips of a float32 rotation)
+    idx = ROPE_Q.index((B, H, Hkv, T, D, dtype, W, alpha))
+    print(f"rope-q case {idx}: B{B} H{H}/{Hkv} T{T} D{D} {dtype} W{W} alpha={alpha}", flush=True)
+    x = _gqa_inputs(B, H, Hkv, T, D, dtype, 110 + idx)
+    q = x["q"].cuda()
+    K = F.fibattn_rope(x["k"].cuda(), 10000.0)
+    V, G = x["v"].cuda(), x["dO"].cuda()
+    o, lse, Q = F.fibattn_forward_rope_q(q, K, V, W, FIB, alpha, 10000.0)
+    dq, dk, dv, da = F.fibattn_backward(Q, K, V, o, lse, G, W, FIB, alpha, rope_base=10000.0)
+    torch.cuda.synchronize()
+    eq, ek = oracle.rope(x["q"]), oracle.rope(x["k"])  # exact rotations
+    rq, rk = (inputs.round_to(r.astype(np.float32), dtype).double().numpy() for r in (eq, ek))
+    slack = rope_rounding_slack(x["q"].double().numpy(), x["k"].double().numpy(), eq, ek, dtype, W, FIB, alpha)
+    if dtype == "fp32":
+        np.testing.assert_allclose(Q.double().cpu().numpy(), rq, atol=1e-5, rtol=0)
+    else:  # the oracle's rounding, or the other neighbour where a float32 rotation may flip it
+        assert np.all(np.abs(Q.double().cpu().numpy() - rq) <= rope_flip_size(x["q"].double().numpy(), eq))
+    ro, rl = oracle.forward(rq, rk, x["v"], W, FIB, alpha)
+    rdq, rdk, rdv, rda, l1 = oracle.backward(rq, rk, x["v"], x["dO"], W, FIB, alpha)
+    rdq, rdk = oracle.rope(rdq, transpose=True), oracle.rope(rdk, transpose=True)
+    got = {"o": o, "lse": lse, "dq": dq, "dk": dk, "dv": dv}
+    got = {kk: vv.double().cpu().numpy() for kk, vv in got.items()}
+    got["dalpha"] = float(da.item())
+    compare(got, {"o": ro, "lse": rl, "dq": rdq, "dk": rdk, "dv": rdv, "dalpha": rda, "l1": l1},
+            dtype, f"rope-q case {idx}", lse_slack=slack)
+    if dtype == "bf16" and D == 64 and W <= 16:
+        # forward only (no q_out): the same kernel without the store, so the same bits;
+        # and q_out may be q itself (each query row is read by its own wave only)
+        o2, l2, none = F.fibattn_forward_rope_q(q, K, V, W, FIB, alpha, 10000.0, keep_q=False)
+        q3 = q.clone()
+        o3, l3, Q3 = F.fibattn_forward_rope_q(q3, K, V, W, FIB, alpha, 10000.0, q_out=q3)
+        torch.cuda.synchronize()
+        assert none is None and torch.equal(o2, o) and torch.equal(l2, lse)
+        assert Q3.data_ptr() == q3.data_ptr() and torch.equal(q3, Q) and torch.equal(o3, o) and torch.equal(l3, lse)
+
+
+@pytest.mark.parametrize("name,ci", [("layer_60m_fixed_T1024", 0), ("extrap_coprime16_T4096", 1)])
+def test_forward_rotating_q_on_load_full_size(name, ci):
+    # forward only at the workload's shape: raw q, the keys rotated by the RoPE launch,
+    # nothing written but o and lse
+    wl = workloads.workload(name)
+    call = wl.calls[ci]
+    print(f"rope-q full size {name} call {ci}: alpha={float(call.alpha):.7f}", flush=True)
+    x = workloads.layer_inputs(wl, ci, names=("q", "k", "v"))
+    K = F.fibattn_rope(x["k"].cuda(), 10000.0)
+    o, lse, _ = F.fibattn_forward_rope_q(x["q"].cuda(), K, x["v"].cuda(), call.W, call.base, call.alpha,
+                                         10000.0, keep_q=False)
+    torch.cuda.synchronize()
+    eq, ek = oracle.rope(x["q"]), oracle.rope(x["k"])
+    rq, rk = (inputs.round_to(r.astype(np.float32), wl.dtype).double().numpy() for r in (eq, ek))
+    slack = rope_rounding_slack(x["q"].double().numpy(), x["k"].double().numpy(), eq, ek, wl.dtype, call.W,
+                                call.base, call.alpha)
+    ro, rl = oracle.forward(rq, rk, x["v"], call.W, call.base, call.alpha)
+    print(compare({"o": o.double().cpu().numpy(), "lse": lse.double().cpu().numpy()}, {"o": ro, "lse": rl},
+                  wl.dtype, f"rope-q full size {name}", lse_slack=slack), flush=True)
+
+
 HEAD128 = [
     # (B, H, H_kv, T, D, dtype, W, base, alpha): d_head = 128 runs the generic kernels
     (1, 2, 2, 260, 128, "fp32", 8, FIB, 0.7310586),
