@@ -60,18 +60,18 @@ def parse_args():
 # HBM traffic per launch of the layer_60m_fixed_T1024 kernels, from two rocprofv3 --pmc
 # passes (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) over
 #   bench.py --eager --steps 10 --warmup 2 --no-cpu-baseline --no-t4096 --no-gqa
-#            --no-learned-alpha --no-integer-offsets --no-configs --copy-probe-mb 256
+#            --no-learned-alpha --no-integer-offsets --no-rope-on-load --no-configs --copy-probe-mb 256
 # each scaled by what the same counter reads for the plain 256 MiB device copy of that run.
 # They hold only for the kernel sources they were taken on (COUNTER_SOURCES_SHA).
-COUNTER_SOURCES_SHA = "28757283bda056403acd89de5829807f70146373e34224ef8d2e89985bb8c59a"
+COUNTER_SOURCES_SHA = "a2d4a1f5eaf6b2146493da3ca22aae9a403f10a02c32e302656d51600c2e665d"
 COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
 COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
-    "forward": (12390.6, 8550.5),
-    "bwd_dq": (20800.6, 10426.7),
-    "bwd_dkdv": (18507.5, 16610.2),
-    "rope": (8236.6, 16384.0),
+    "forward": (12402.5, 16750.5),
+    "bwd_dq": (20800.6, 10426.9),
+    "bwd_dkdv": (18539.3, 16610.8),
+    "rope": (4124.9, 8192.0),
 }
-COPY_PROBE_KIB = (262144.0, 131093.2, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
+COPY_PROBE_KIB = (262144.0, 131093.0, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
 
 
 def kernel_sources_sha() -> str:
@@ -426,8 +426,8 @@ def gqa_figure(steps: int, warmup: int, eager: bool, kv_heads: int = 2):
 def learned_alpha_figure(steps: int, warmup: int, eager: bool, layer: int = 0):
     """Learned-alpha layer of the pow2/fib workload (B=32, H=8, T=1024, W=10, Fibonacci
     base, alpha = 0.5 + sigmoid(theta)) with theta resident on the device: theta ->
-    alpha and rung table, in the RoPE launch -> forward -> backward with dtheta, against
-    the same layer with alpha passed from the host."""
+    alpha and rung table, in the RoPE launch of q and k -> forward -> backward with
+    dtheta, against the same launches with alpha passed from the host."""
     import torch
 
     from paper_2606_28560_amd import fibattn as F
@@ -455,9 +455,12 @@ def learned_alpha_figure(steps: int, warmup: int, eager: bool, layer: int = 0):
                                   dk=st.dk, dv=st.dv, dalpha=st.da, dtheta=st.dtheta, workspace=st.ws,
                                   rope_base=ROPE_BASE)
         dev.append(run_dev)
+    # alpha from the host, with the same launches: RoPE of q and k in one launch (the
+    # forward that rotates q on load takes host tables only), forward, backward
+    host = [lambda st=st: (st.forward_two_launch(), st.backward()) for st in sets]
     out = {"workload": wl.name, "layer": layer, "alpha": float(call.alpha)}
     runs = {}
-    for tag, fns in (("device_alpha", dev), ("host_alpha", sets)):
+    for tag, fns in (("device_alpha", dev), ("host_alpha", host)):
         if eager:
             run = lambda i, fns=fns: fns[i % len(fns)]()  # noqa: E731
         else:

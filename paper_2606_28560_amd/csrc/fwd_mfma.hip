@@ -162,8 +162,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
             float x0, y0, x1, y1;
             rope_rotate(bf16_lo(aw[w]), bf16_lo(bw[w]), rc[2 * w], rs[2 * w], x0, y0);
             rope_rotate(bf16_hi(aw[w]), bf16_hi(bw[w]), rc[2 * w + 1], rs[2 * w + 1], x1, y1);
-            aw[w] = f32_to_bf16(x0) | (f32_to_bf16(x1) << 16);
-            bw[w] = f32_to_bf16(y0) | (f32_to_bf16(y1) << 16);
+            aw[w] = pack_bf16(x0, x1);  // round to nearest even, as the RoPE launch
+            bw[w] = pack_bf16(y0, y1);
         }
         qq.a = make_uint4(aw[0], aw[1], aw[2], aw[3]);
         qq.b = make_uint4(bw[0], bw[1], bw[2], bw[3]);

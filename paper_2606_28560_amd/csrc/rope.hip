@@ -73,6 +73,13 @@ __global__ __launch_bounds__(256) void rope_kernel(const S *x, S *y, int BH, int
 // The loads are issued before the angles are evaluated.
 constexpr int kRope64RB = 16;
 
+// two float32 -> bfloat16 (round to nearest even) in one conversion instruction
+typedef __bf16 rope_bf16x2 __attribute__((ext_vector_type(2)));
+typedef float rope_f32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((rope_f32x2){lo, hi}, rope_bf16x2));
+}
+
 // blockIdx.z selects the tensor: (x0 -> y0) or (x1 -> y1), each with its own row count
 // (batch * heads) and head count (k may have fewer heads than q) and placed by its io
 // (STRIDED; else every tensor is packed [BH, T, 64]).
@@ -132,8 +139,8 @@ __global__ __launch_bounds__(256) void rope_bf16_d64_kernel(const uint16_t *x0, 
             const float u0 = bf16_lo(aw[w]), u1 = bf16_hi(aw[w]);
             const float v0 = bf16_lo(bw[w]), v1 = bf16_hi(bw[w]);
             const float c0 = C[2 * w], c1 = C[2 * w + 1], s0 = Sn[2 * w], s1 = Sn[2 * w + 1];
-            ow[w] = f32_to_bf16(u0 * c0 - v0 * s0) | (f32_to_bf16(u1 * c1 - v1 * s1) << 16);
-            pw[w] = f32_to_bf16(v0 * c0 + u0 * s0) | (f32_to_bf16(v1 * c1 + u1 * s1) << 16);
+            ow[w] = pack2_bf16(u0 * c0 - v0 * s0, u1 * c1 - v1 * s1);
+            pw[w] = pack2_bf16(v0 * c0 + u0 * s0, v1 * c1 + u1 * s1);
         }
         *reinterpret_cast<uint4 *>(yr[h] + 8 * g) = make_uint4(ow[0], ow[1], ow[2], ow[3]);
         *reinterpret_cast<uint4 *>(yr[h] + 32 + 8 * g) = make_uint4(pw[0], pw[1], pw[2], pw[3]);
