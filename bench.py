@@ -63,15 +63,15 @@ def parse_args():
 #            --no-learned-alpha --no-integer-offsets --no-rope-on-load --no-configs --copy-probe-mb 256
 # each scaled by what the same counter reads for the plain 256 MiB device copy of that run.
 # They hold only for the kernel sources they were taken on (COUNTER_SOURCES_SHA).
-COUNTER_SOURCES_SHA = "a2d4a1f5eaf6b2146493da3ca22aae9a403f10a02c32e302656d51600c2e665d"
+COUNTER_SOURCES_SHA = "63537e6fb70a466c3e876cb1655052ecc1817827432ca18ad9ee3f67fb514af6"
 COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
 COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
-    "forward": (12402.5, 16750.5),
-    "bwd_dq": (20800.6, 10426.9),
-    "bwd_dkdv": (18539.3, 16610.8),
+    "forward": (12398.2, 16744.8),
+    "bwd_dq": (20800.6, 10426.6),
+    "bwd_dkdv": (18525.8, 16613.2),
     "rope": (4124.9, 8192.0),
 }
-COPY_PROBE_KIB = (262144.0, 131093.0, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
+COPY_PROBE_KIB = (262144.0, 131093.1, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
 
 
 def kernel_sources_sha() -> str:
@@ -426,7 +426,7 @@ def gqa_figure(steps: int, warmup: int, eager: bool, kv_heads: int = 2):
 def learned_alpha_figure(steps: int, warmup: int, eager: bool, layer: int = 0):
     """Learned-alpha layer of the pow2/fib workload (B=32, H=8, T=1024, W=10, Fibonacci
     base, alpha = 0.5 + sigmoid(theta)) with theta resident on the device: theta ->
-    alpha and rung table, in the RoPE launch of q and k -> forward -> backward with
+    alpha and rung table, in the RoPE launch of k -> forward rotating q -> backward with
     dtheta, against the same launches with alpha passed from the host."""
     import torch
 
@@ -448,19 +448,17 @@ def learned_alpha_figure(steps: int, warmup: int, eager: bool, layer: int = 0):
 
         def run_dev(st=st):
             c = st.call
-            F.fibattn_rope_qk_table(st.q, st.k, ROPE_BASE, theta=st.theta, base=c.base, W=c.W, table=st.table,
-                                    alpha=st.alpha, q_out=st.qr, k_out=st.kr)
-            F.fibattn_forward_dt(st.qr, st.kr, st.v, c.W, st.table, o=st.o, lse=st.lse)
+            F.fibattn_rope_qk_table(None, st.k, ROPE_BASE, theta=st.theta, base=c.base, W=c.W, table=st.table,
+                                    alpha=st.alpha, k_out=st.kr)
+            F.fibattn_forward_rope_q_dt(st.q, st.kr, st.v, c.W, st.table, ROPE_BASE, o=st.o, lse=st.lse,
+                                        q_out=st.qr)
             F.fibattn_backward_dt(st.qr, st.kr, st.v, st.o, st.lse, st.dO, c.W, st.table, dq=st.dq,
                                   dk=st.dk, dv=st.dv, dalpha=st.da, dtheta=st.dtheta, workspace=st.ws,
                                   rope_base=ROPE_BASE)
         dev.append(run_dev)
-    # alpha from the host, with the same launches: RoPE of q and k in one launch (the
-    # forward that rotates q on load takes host tables only), forward, backward
-    host = [lambda st=st: (st.forward_two_launch(), st.backward()) for st in sets]
     out = {"workload": wl.name, "layer": layer, "alpha": float(call.alpha)}
     runs = {}
-    for tag, fns in (("device_alpha", dev), ("host_alpha", host)):
+    for tag, fns in (("device_alpha", dev), ("host_alpha", sets)):
         if eager:
             run = lambda i, fns=fns: fns[i % len(fns)]()  # noqa: E731
         else:

@@ -260,6 +260,14 @@ fibattn_status_t fibattn_forward_dt(const void *q, const void *k, const void *v,
                                     int B, int H, int H_kv, int T, int d_head, int W,
                                     const void *table, fibattn_dtype_t dtype, hipStream_t stream);
 
+/* fibattn_forward_rope_q with the rung table in device memory (as fibattn_forward_dt):
+ * q unrotated, k rotated, q_out nullable; the same limits and errors as both. */
+fibattn_status_t fibattn_forward_rope_q_dt(const void *q, const void *k, const void *v,
+                                           void *o, float *lse, void *q_out,
+                                           int B, int H, int H_kv, int T, int d_head, int W,
+                                           const void *table, float rope_base,
+                                           fibattn_dtype_t dtype, hipStream_t stream);
+
 fibattn_status_t fibattn_backward_dt(const void *q, const void *k, const void *v,
                                      const void *o, const float *lse, const void *dO,
                                      void *dq, void *dk, void *dv, float *dalpha, float *dtheta,
@@ -333,7 +341,9 @@ fibattn_status_t fibattn_backward_noalloc(const void *q, const void *k, const vo
  * (base, K, W) written to `table`, which also records d alpha / d theta).  So the step
  * of a layer with a learned alpha launches as many kernels as one with a host alpha:
  * this, fibattn_forward_dt and fibattn_backward_dt (which then also returns dtheta).
- * With theta NULL, base, K, W and table are ignored.  Same limits and errors as
+ * With theta NULL, base, K, W and table are ignored.  q and q_out both NULL rotate k
+ * alone (the launch still carries the table job): the prologue of a step whose forward
+ * rotates q on load (fibattn_forward_rope_q_dt).  Same limits and errors as
  * fibattn_rope_qk and fibattn_device_table_theta.
  */
 fibattn_status_t fibattn_rope_qk_table(const void *q, const void *k, void *q_out, void *k_out,

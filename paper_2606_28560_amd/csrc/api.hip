@@ -191,6 +191,37 @@ fibattn_status_t fibattn_forward(const void *q, const void *k, const void *v, vo
     return fibattn_forward_gqa(q, k, v, o, lse, B, H, H, T, d_head, W, base, K, alpha, dtype, stream);
 }
 
+// The forward with q rotated on load, from a host table (rtp null) or a device table.
+static fibattn_status_t forward_rope_q_impl(const void *q, const void *k, const void *v, void *o, float *lse,
+                                            void *q_out, int B, int H, int H_kv, int T, int d_head, int W,
+                                            const RungTable &rt, const RungTable *rtp, float rope_base,
+                                            fibattn_dtype_t dtype, hipStream_t stream) {
+    if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
+    if (!q || !k || !v || !o || !lse) return FIBATTN_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse) ||
+        !aligned16(q_out) || !aligned16(rtp))
+        return FIBATTN_ERR_INVALID_ARG;
+    if (!(rope_base > 1.f) || !isfinite(rope_base)) return FIBATTN_ERR_INVALID_ARG;
+    const bool on_load = forward_mfma_supported((int)dtype, d_head, W);
+    if (!on_load && !q_out) return FIBATTN_ERR_UNSUPPORTED;  // the rotated rows need a home
+    const Heads hd{H, H / H_kv};
+    const Layouts lay = packed_layouts(H, H_kv, T, d_head);
+    hipError_t e;
+    if (on_load) {
+        // one launch: each query row is rotated where the forward loads it
+        const RopeFreq rf = make_rope_freq((double)rope_base, d_head);
+        e = launch_forward_mfma(q, k, v, o, lse, B * H, hd, T, W, rt, rtp, lay, stream, &rf, q_out);
+    } else {
+        // the RoPE launch on q into q_out, then the forward on it
+        const Layout l = Layout::packed(H, T, d_head);
+        e = launch_rope((int)dtype, d_head, q, q_out, l, l, nullptr, nullptr, l, l, B * H, H, T, rope_base,
+                        0, stream);
+        if (e == hipSuccess)
+            e = launch_forward((int)dtype, d_head, q_out, k, v, o, lse, B * H, hd, T, W, rt, rtp, lay, stream);
+    }
+    return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+}
+
 fibattn_status_t fibattn_forward_rope_q(const void *q, const void *k, const void *v, void *o,
                                         float *lse, void *q_out, int B, int H, int H_kv, int T,
                                         int d_head, int W, const int32_t *base, int K, float alpha,
@@ -198,33 +229,11 @@ fibattn_status_t fibattn_forward_rope_q(const void *q, const void *k, const void
     fibattn_status_t st = check_common(B, H, T, d_head, W, K, dtype);
     if (st != FIBATTN_OK) return st;
     if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
-    if (!q || !k || !v || !o || !lse) return FIBATTN_ERR_INVALID_ARG;
-    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse) ||
-        !aligned16(q_out))
-        return FIBATTN_ERR_INVALID_ARG;
-    if (!(rope_base > 1.f) || !isfinite(rope_base)) return FIBATTN_ERR_INVALID_ARG;
-    const bool on_load = forward_mfma_supported((int)dtype, d_head, W);
-    if (!on_load && !q_out) return FIBATTN_ERR_UNSUPPORTED;  // the rotated rows need a home
     RungTable rt;
     st = build_table(alpha, base, K, W, &rt);
     if (st != FIBATTN_OK) return st;
-    const Heads hd{H, H / H_kv};
-    const Layouts lay = packed_layouts(H, H_kv, T, d_head);
-    hipError_t e;
-    if (on_load) {
-        // one launch: each query row is rotated where the forward loads it
-        const RopeFreq rf = make_rope_freq((double)rope_base, d_head);
-        e = launch_forward_mfma(q, k, v, o, lse, B * H, hd, T, W, rt, nullptr, lay, stream, &rf, q_out);
-    } else {
-        // the RoPE launch on q into q_out, then the forward on it
-        const Layout l = Layout::packed(H, T, d_head);
-        e = launch_rope((int)dtype, d_head, q, q_out, l, l, nullptr, nullptr, l, l, B * H, H, T, rope_base,
-                        0, stream);
-        if (e == hipSuccess)
-            e = launch_forward((int)dtype, d_head, q_out, k, v, o, lse, B * H, hd, T, W, rt, nullptr, lay,
-                               stream);
-    }
-    return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
+    return forward_rope_q_impl(q, k, v, o, lse, q_out, B, H, H_kv, T, d_head, W, rt, nullptr, rope_base,
+                               dtype, stream);
 }
 
 // Backward workspace: Delta (float32 [B,H,T]), then the per-workgroup dalpha partials
@@ -398,6 +407,19 @@ fibattn_status_t fibattn_forward_dt(const void *q, const void *k, const void *v,
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
 }
 
+fibattn_status_t fibattn_forward_rope_q_dt(const void *q, const void *k, const void *v, void *o,
+                                           float *lse, void *q_out, int B, int H, int H_kv, int T,
+                                           int d_head, int W, const void *table, float rope_base,
+                                           fibattn_dtype_t dtype, hipStream_t stream) {
+    fibattn_status_t st = check_common(B, H, T, d_head, W, 0, dtype);
+    if (st != FIBATTN_OK) return st;
+    if (!table) return FIBATTN_ERR_INVALID_ARG;
+    RungTable unused;
+    memset(&unused, 0, sizeof(unused));
+    return forward_rope_q_impl(q, k, v, o, lse, q_out, B, H, H_kv, T, d_head, W, unused,
+                               (const RungTable *)table, rope_base, dtype, stream);
+}
+
 fibattn_status_t fibattn_backward_dt(const void *q, const void *k, const void *v, const void *o,
                                      const float *lse, const void *dO, void *dq, void *dk, void *dv,
                                      float *dalpha, float *dtheta, void *workspace, size_t workspace_bytes, int B,
@@ -476,7 +498,8 @@ fibattn_status_t fibattn_rope_qk_table(const void *q, const void *k, void *q_out
                                        int H_kv, int T, int d_head, float rope_base, const float *theta,
                                        float *alpha, const int32_t *base, int K, int W, void *table,
                                        fibattn_dtype_t dtype, hipStream_t stream) {
-    if (B < 1 || H < 1 || T < 1 || !q || !k || !q_out || !k_out) return FIBATTN_ERR_INVALID_ARG;
+    // q and q_out both null: k alone (its launch carries the table job)
+    if (B < 1 || H < 1 || T < 1 || !k || !k_out || !q != !q_out) return FIBATTN_ERR_INVALID_ARG;
     if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
     if (!aligned16(q) || !aligned16(k) || !aligned16(q_out) || !aligned16(k_out))
         return FIBATTN_ERR_INVALID_ARG;
@@ -495,8 +518,10 @@ fibattn_status_t fibattn_rope_qk_table(const void *q, const void *k, void *q_out
         job.W = W;
     }
     const Layout lq = Layout::packed(H, T, d_head), lk = Layout::packed(H_kv, T, d_head);
-    hipError_t e = launch_rope((int)dtype, d_head, q, q_out, lq, lq, k, k_out, lk, lk, B * H, H, T, rope_base,
-                               0, stream, B * H_kv, H_kv, theta ? &job : nullptr);
+    hipError_t e = q ? launch_rope((int)dtype, d_head, q, q_out, lq, lq, k, k_out, lk, lk, B * H, H, T, rope_base,
+                                   0, stream, B * H_kv, H_kv, theta ? &job : nullptr)
+                     : launch_rope((int)dtype, d_head, k, k_out, lk, lk, nullptr, nullptr, lk, lk, B * H_kv, H_kv, T,
+                                   rope_base, 0, stream, 0, 0, theta ? &job : nullptr);
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
 }
 

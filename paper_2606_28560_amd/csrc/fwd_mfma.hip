@@ -46,7 +46,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     uint16_t *__restrict__ o, float *__restrict__ lse, int T, int W, RungTable rt_arg,
     const RungTable *__restrict__ rtp, float sl2, int tiles, Heads hd, Layouts lay,
     uint16_t *qrot, RopeFreq rf) {
-    static_assert(!RQ || (!DEV && !STRIDED), "rotation on load: packed tensors, host table");
+    static_assert(!RQ || !STRIDED, "rotation on load: packed tensors");
     const RungTable &rt = DEV ? *rtp : rt_arg;
     constexpr int RB = INTERP ? 1 : 2;  // rungs per load batch; two batches in flight
     constexpr int NS = INTERP ? 2 : 1;  // rows per rung (r0, and r1 when interpolating)
@@ -300,7 +300,6 @@ hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void
     // device tables and rotation on load come with packed tensors only
     const bool strided = lay.q.st != kD || lay.k.st != kD || lay.v.st != kD || lay.o.st != kD;
     if ((rtp || rq) && strided) return hipErrorInvalidValue;
-    if (rq && rtp) return hipErrorInvalidValue;
     const bool interp = any_interp(rt);
     const int hs = (rtp || strided) ? 1 : heads_per_wg(hd.G);
     const int tiles = (T + kFwdBQ / hs - 1) / (kFwdBQ / hs);  // runs of 64 / hs queries
@@ -309,7 +308,7 @@ hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void
     (hs == 4   ? (interp ? FIBATTN_FWD(true, 4, R) : FIBATTN_FWD(false, 4, R))                \
      : hs == 2 ? (interp ? FIBATTN_FWD(true, 2, R) : FIBATTN_FWD(false, 2, R))                \
                : (interp ? FIBATTN_FWD(true, 1, R) : FIBATTN_FWD(false, 1, R)))
-    auto kern = rtp ? fwd_bf16_d64_kernel<true, true, false, 1, false>
+    auto kern = rtp ? (rq ? fwd_bf16_d64_kernel<true, true, false, 1, true> : fwd_bf16_d64_kernel<true, true, false, 1, false>)
               : strided ? (interp ? fwd_bf16_d64_kernel<true, false, true, 1, false>
                                   : fwd_bf16_d64_kernel<false, false, true, 1, false>)
               : rq ? FIBATTN_FWD_HS(true) : FIBATTN_FWD_HS(false);

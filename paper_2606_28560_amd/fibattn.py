@@ -27,7 +27,7 @@ EXPORTED = ("fibattn_rung_table", "fibattn_forward", "fibattn_backward_workspace
             "fibattn_backward_dt", "fibattn_alpha_from_theta", "fibattn_dtheta", "fibattn_rope",
             "fibattn_rope_qk", "fibattn_status_string", "fibattn_timing_begin", "fibattn_timing_end",
             "fibattn_backward_noalloc", "fibattn_device_table_theta", "fibattn_rope_qk_table",
-            "fibattn_forward_rope_q")
+            "fibattn_forward_rope_q", "fibattn_forward_rope_q_dt")
 SCRATCH_BYTES = 64 << 20  # FIBATTN_SCRATCH_BYTES: the allocation-free backward's static scratch
 
 
@@ -65,6 +65,8 @@ def lib():
     L.fibattn_forward_gqa.restype = i
     L.fibattn_forward_rope_q.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, ip, i, f, f, i, vp]
     L.fibattn_forward_rope_q.restype = i
+    L.fibattn_forward_rope_q_dt.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, vp, f, i, vp]
+    L.fibattn_forward_rope_q_dt.restype = i
     L.fibattn_backward_gqa.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                        i, i, i, i, i, i, ip, i, f, f, i, vp]
     L.fibattn_backward_gqa.restype = i
@@ -211,6 +213,33 @@ def fibattn_forward_rope_q(q, k, v, W: int, base, alpha: float, rope_base: float
                                       b.size, ctypes.c_float(alpha), ctypes.c_float(rope_base), _dtype_code(q),
                                       _stream(stream))
     _check("fibattn_forward_rope_q", st)
+    return o, lse, q_out
+
+
+def fibattn_forward_rope_q_dt(q, k, v, W: int, table, rope_base: float = 10000.0, *, o=None, lse=None,
+                              q_out=None, keep_q=True, stream=None):
+    """As fibattn_forward_rope_q, with the rung table built on the device."""
+    import torch
+
+    B, H, T, D = q.shape
+    Hkv = _kv_heads(q, k)
+    _check_tensor("q", q, q.shape, q.dtype)
+    for n_, t in (("k", k), ("v", v)):
+        _check_tensor(n_, t, (B, Hkv, T, D), q.dtype)
+    o = torch.empty_like(q) if o is None else o
+    lse = torch.empty((B, H, T), device=q.device, dtype=torch.float32) if lse is None else lse
+    _check_tensor("o", o, q.shape, q.dtype)
+    _check_tensor("lse", lse, (B, H, T), torch.float32)
+    if keep_q:
+        q_out = torch.empty_like(q) if q_out is None else q_out
+        _check_tensor("q_out", q_out, q.shape, q.dtype)
+    elif q_out is not None:
+        raise ValueError("q_out given with keep_q=False")
+    st = lib().fibattn_forward_rope_q_dt(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
+                                         q_out.data_ptr() if keep_q else None, B, H, Hkv, T, D, int(W),
+                                         table.data_ptr(), ctypes.c_float(rope_base), _dtype_code(q),
+                                         _stream(stream))
+    _check("fibattn_forward_rope_q_dt", st)
     return o, lse, q_out
 
 
@@ -478,30 +507,38 @@ def fibattn_rope_qk_table(q, k, rope_base: float = 10000.0, *, theta=None, base=
     """R q and R k in one launch (k may have fewer heads than q); with `theta` (a float32
     device tensor) the same launch builds the rung table of alpha = 0.5 + sigmoid(theta)
     for (base, W) into `table` (allocated when None) and writes alpha when given.
-    Returns (q_out, k_out, table)."""
+    q=None rotates k alone (q_out is then None).  Returns (q_out, k_out, table)."""
     import torch
 
-    B, H, T, D = q.shape
-    Hkv = _kv_heads(q, k)
-    _check_tensor("q", q, q.shape, q.dtype)
-    _check_tensor("k", k, (B, Hkv, T, D), q.dtype)
-    q_out = torch.empty_like(q) if q_out is None else q_out
+    if q is None:
+        if q_out is not None:
+            raise ValueError("q_out given without q")
+        B, Hkv, T, D = k.shape
+        H = Hkv
+        _check_tensor("k", k, k.shape, k.dtype)
+    else:
+        B, H, T, D = q.shape
+        Hkv = _kv_heads(q, k)
+        _check_tensor("q", q, q.shape, q.dtype)
+        _check_tensor("k", k, (B, Hkv, T, D), q.dtype)
+        q_out = torch.empty_like(q) if q_out is None else q_out
+        _check_tensor("q_out", q_out, q.shape, q.dtype)
     k_out = torch.empty_like(k) if k_out is None else k_out
-    _check_tensor("q_out", q_out, q.shape, q.dtype)
-    _check_tensor("k_out", k_out, k.shape, q.dtype)
+    _check_tensor("k_out", k_out, k.shape, k.dtype)
     b, bp = _base_array(base)
     if theta is not None:
         if theta.device.type != "cuda" or theta.dtype != torch.float32 or theta.numel() < 1:
             raise ValueError("theta: a float32 device tensor")
         nb = int(lib().fibattn_device_table_bytes())
-        table = torch.empty(nb, device=q.device, dtype=torch.uint8) if table is None else table
+        table = torch.empty(nb, device=k.device, dtype=torch.uint8) if table is None else table
         if table.numel() < nb or not table.is_contiguous():
             raise ValueError(f"table: {nb} contiguous bytes")
-    st = lib().fibattn_rope_qk_table(q.data_ptr(), k.data_ptr(), q_out.data_ptr(), k_out.data_ptr(), B, H, Hkv,
+    st = lib().fibattn_rope_qk_table(None if q is None else q.data_ptr(), k.data_ptr(),
+                                     None if q_out is None else q_out.data_ptr(), k_out.data_ptr(), B, H, Hkv,
                                      T, D, ctypes.c_float(rope_base),
                                      None if theta is None else theta.data_ptr(),
                                      None if alpha is None else alpha.data_ptr(), bp, b.size, int(W),
-                                     None if table is None else table.data_ptr(), _dtype_code(q),
+                                     None if table is None else table.data_ptr(), _dtype_code(k),
                                      _stream(stream))
     _check("fibattn_rope_qk_table", st)
     return q_out, k_out, table

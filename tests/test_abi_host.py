@@ -152,6 +152,15 @@ def test_invalid_arguments_return_codes_without_gpu():
     assert rq(16, 16, 16, 16, 16, 16, 1, 8, 8, 8, 48, 8, b, 15, one, r4, 1, None) == 2
     assert rq(16, 16, 16, 16, 16, None, 1, 8, 8, 8, 64, 8, b, 15, one, r4, 0, None) == 2   # float32
     assert rq(16, 16, 16, 16, 16, None, 1, 8, 8, 8, 64, 20, b, 15, one, r4, 1, None) == 2  # W > 16
+    # the same from a device table: the table pointer is required
+    rqd = L.fibattn_forward_rope_q_dt
+    assert rqd(16, 16, 16, 16, 16, 16, 1, 8, 8, 8, 64, 8, None, r4, 1, None) == 1
+    assert rqd(16, 16, 16, 16, 16, 16, 1, 8, 8, 8, 64, 8, 16, ctypes.c_float(0.5), 1, None) == 1
+    assert rqd(16, 16, 16, 16, 16, None, 1, 8, 8, 8, 64, 8, 16, r4, 0, None) == 2
+    # k alone through the prologue launch: q and q_out null together, or neither
+    rt = L.fibattn_rope_qk_table
+    assert rt(None, 16, 16, 16, 1, 8, 8, 8, 64, r4, None, None, b, 15, 8, None, 1, None) == 1
+    assert rt(16, 16, None, 16, 1, 8, 8, 8, 64, r4, None, None, b, 15, 8, None, 1, None) == 1
     # device alpha: the base table is checked on the host, pointers before any launch
     bad = (ctypes.c_int32 * 3)(5, 3, 8)
     assert L.fibattn_device_table(16, bad, 3, 8, 16, None) == 1

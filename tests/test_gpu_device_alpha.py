@@ -7,7 +7,7 @@ import torch
 import oracle
 from paper_2606_28560_amd import fibattn as F
 from paper_2606_28560_amd import inputs, schedules, workloads
-from tests.parity import compare, oracle_run, rope_rounding_slack
+from tests.parity import compare, oracle_run, rope_flip_size, rope_rounding_slack
 
 pytestmark = pytest.mark.gpu
 
@@ -182,12 +182,58 @@ def test_rope_qk_table_equals_separate_launches(dtype, D, H, Hkv):
     qo2, ko2, _ = F.fibattn_rope_qk_table(q, k, 10000.0, table=t2)
     torch.cuda.synchronize()
     assert torch.equal(qo2, rq) and torch.equal(ko2, rk) and bool((t2 == 7).all())
+    # k alone, the table job on that launch
+    a3 = torch.full((1,), float("nan"), device="cuda")
+    qo3, ko3, t3 = F.fibattn_rope_qk_table(None, k, 10000.0, theta=theta, base=FIB, W=8, alpha=a3)
+    torch.cuda.synchronize()
+    assert qo3 is None and torch.equal(ko3, rk)
+    assert torch.equal(t3[:400], tref[:400]) and torch.equal(a3, ta)
 
 
-def test_learned_alpha_step_in_a_graph():
+DEV_ROPE_Q = [
+    # (B, H, H_kv, T, W, alpha): the forward rotating q on load with a device table
+    (1, 8, 2, 300, 8, 0.9),
+    (2, 2, 2, 257, 16, 1.0),
+    (1, 3, 3, 1, 0, 1.2333333),
+]
+
+
+@pytest.mark.parametrize("B,H,Hkv,T,W,alpha", DEV_ROPE_Q)
+def test_device_alpha_rotating_q_on_load(B, H, Hkv, T, W, alpha):
+    # device alpha -> table; RoPE of k; forward rotating q with the device table;
+    # backward with R^T: the oracle runs the same chain on its own rounded rotations
+    idx = DEV_ROPE_Q.index((B, H, Hkv, T, W, alpha))
+    print(f"device alpha rope-q case {idx}: B{B} H{H}/{Hkv} T{T} W{W} alpha={alpha}", flush=True)
+    x = inputs.attention_inputs(B, H, T, 64, "bf16", 470 + idx, 0, names=("q", "dO"))
+    x.update(inputs.attention_inputs(B, Hkv, T, 64, "bf16", 470 + idx, 0, names=("k", "v")))
+    q, V, G = x["q"].cuda(), x["v"].cuda(), x["dO"].cuda()
+    table = F.fibattn_device_table(torch.tensor([alpha], dtype=torch.float32, device="cuda"), FIB, W)
+    K = F.fibattn_rope(x["k"].cuda(), 10000.0)
+    o, lse, Q = F.fibattn_forward_rope_q_dt(q, K, V, W, table, 10000.0)
+    o2, l2, none = F.fibattn_forward_rope_q_dt(q, K, V, W, table, 10000.0, keep_q=False)
+    ws = torch.empty(F.fibattn_backward_workspace_bytes(B, H, T, 64, W, 0), device="cuda", dtype=torch.uint8)
+    dq, dk, dv, da = F.fibattn_backward_dt(Q, K, V, o, lse, G, W, table, workspace=ws, rope_base=10000.0)
+    torch.cuda.synchronize()
+    assert none is None and torch.equal(o2, o) and torch.equal(l2, lse)
+    eq, ek = oracle.rope(x["q"]), oracle.rope(x["k"])
+    rq, rk = (inputs.round_to(r.astype(np.float32), "bf16").double().numpy() for r in (eq, ek))
+    assert np.all(np.abs(Q.double().cpu().numpy() - rq) <= rope_flip_size(x["q"].double().numpy(), eq))
+    slack = rope_rounding_slack(x["q"].double().numpy(), x["k"].double().numpy(), eq, ek, "bf16", W, FIB, alpha)
+    ro, rl = oracle.forward(rq, rk, x["v"], W, FIB, alpha)
+    rdq, rdk, rdv, rda, l1 = oracle.backward(rq, rk, x["v"], x["dO"], W, FIB, alpha)
+    rdq, rdk = oracle.rope(rdq, transpose=True), oracle.rope(rdk, transpose=True)
+    got = {kk: vv.double().cpu().numpy() for kk, vv in {"o": o, "lse": lse, "dq": dq, "dk": dk, "dv": dv}.items()}
+    got["dalpha"] = float(da.item())
+    compare(got, {"o": ro, "lse": rl, "dq": rdq, "dk": rdk, "dv": rdv, "dalpha": rda, "l1": l1}, "bf16",
+            f"device alpha rope-q case {idx}", lse_slack=slack)
+
+
+@pytest.mark.parametrize("on_load", [False, True])
+def test_learned_alpha_step_in_a_graph(on_load):
     # theta (device) -> alpha -> rung table -> RoPE -> forward -> backward -> dtheta,
     # captured once and replayed with theta changed in place between replays: every
-    # replay follows the new theta with no host involvement
+    # replay follows the new theta with no host involvement.  on_load: the prologue
+    # rotates k alone and the forward rotates q where it loads it
     wl = workloads.workload("pow2_fib_learned16_T1024")
     B, H, T, D, W = 2, 4, 256, 64, 10
     x = inputs.attention_inputs(B, H, T, D, "bf16", 460, 0)
@@ -203,9 +249,14 @@ def test_learned_alpha_step_in_a_graph():
     base = wl.calls[0].base
 
     def step():  # RoPE, theta -> alpha and table in one launch; dtheta from the backward
-        F.fibattn_rope_qk_table(q, k, 10000.0, theta=theta, base=base, W=W, table=table, alpha=alpha,
-                                q_out=qr, k_out=kr)
-        F.fibattn_forward_dt(qr, kr, v, W, table, o=o, lse=lse)
+        if on_load:
+            F.fibattn_rope_qk_table(None, k, 10000.0, theta=theta, base=base, W=W, table=table, alpha=alpha,
+                                    k_out=kr)
+            F.fibattn_forward_rope_q_dt(q, kr, v, W, table, 10000.0, o=o, lse=lse, q_out=qr)
+        else:
+            F.fibattn_rope_qk_table(q, k, 10000.0, theta=theta, base=base, W=W, table=table, alpha=alpha,
+                                    q_out=qr, k_out=kr)
+            F.fibattn_forward_dt(qr, kr, v, W, table, o=o, lse=lse)
         F.fibattn_backward_dt(qr, kr, v, o, lse, dO, W, table, dq=dq, dk=dk, dv=dv, dalpha=da,
                               dtheta=dth, workspace=ws, rope_base=10000.0)
 
