@@ -2,12 +2,12 @@
 """Throughput of the fibattn hot path on one MI355X.
 
 One step = one layer of the 60M-model shape (B=8, H=8, T=1024, d_head=64, bf16,
-W=8, Fibonacci base K=15, alpha=1): RoPE of q and k at true positions, the forward
-(o, lse) and the backward (dq, dk, dv, dalpha, with R^T carrying dq, dk back to the
-unrotated inputs), all in libfibattn.so's HIP kernels on one stream.  Inputs are
-seeded N(0,1) tensors resident in HBM; several buffer sets rotate so that the
-256 MB last-level cache cannot hold a step's working set.  Steps are replayed from
-HIP graphs (one captured step per buffer set).
+W=8, Fibonacci base K=15, alpha=1): RoPE of k at true positions, the forward that
+rotates q where it loads it (o, lse, R q) and the backward (dq, dk, dv, dalpha, with
+R^T carrying dq, dk back to the unrotated inputs), all in libfibattn.so's HIP kernels
+on one stream.  Inputs are seeded N(0,1) tensors resident in HBM; several buffer sets
+rotate so that the 256 MB last-level cache cannot hold a step's working set.  Steps
+are replayed from a HIP graph holding one step per buffer set back to back.
 
 Printed: one JSON line with queries*heads per second, the roofline of the dominant
 kernel (algorithmic bytes per launch over its mean launch duration, timed with HIP
@@ -66,12 +66,12 @@ def parse_args():
 COUNTER_SOURCES_SHA = "63537e6fb70a466c3e876cb1655052ecc1817827432ca18ad9ee3f67fb514af6"
 COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
 COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
-    "forward": (12398.2, 16744.8),
-    "bwd_dq": (20800.6, 10426.6),
-    "bwd_dkdv": (18525.8, 16613.2),
+    "forward": (12398.3, 16748.1),
+    "bwd_dq": (20800.6, 10425.8),
+    "bwd_dkdv": (18535.0, 16613.7),
     "rope": (4124.9, 8192.0),
 }
-COPY_PROBE_KIB = (262144.0, 131093.1, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
+COPY_PROBE_KIB = (262144.0, 131092.9, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
 
 
 def kernel_sources_sha() -> str:
@@ -226,6 +226,44 @@ def timed(run, steps: int, warmup: int):
     return t0.elapsed_time(t1) / steps, wall
 
 
+def timed_steps(fns, steps: int, warmup: int, eager: bool, whole: bool = True):
+    """(mean ms per step, host wall ms per step) over `steps` steps after `warmup`, step i
+    running fns[i % n], one function per buffer set.  With graphs, the n steps of one
+    rotation over the buffer sets are captured back to back in one graph, as the layers
+    of a model's training step are captured together; the timed region replays it
+    steps // n times and then single-step graphs for the remaining steps, so it runs
+    exactly `steps` steps, continuing the rotation where the warm-up left it.  (Replaying
+    one single-step graph per step leaves the GPU idle for several microseconds between
+    replays on this runtime: `one_graph_per_step_ms` in the output.)  whole: round `steps`
+    up to whole rotations (the figures); the headline passes False and runs exactly the
+    steps asked for."""
+    import torch
+
+    n = len(fns)
+    if whole:
+        steps = -(-steps // n) * n
+    if eager:
+        return timed(lambda i: fns[i % n](), steps, warmup)
+    start = warmup % n
+    singles = [capture(f) for f in fns]
+    rot = capture(lambda: [fns[(start + j) % n]() for j in range(n)])
+    for i in range(warmup):
+        singles[i % n].replay()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    t0.record()
+    for _ in range(steps // n):
+        rot.replay()
+    for j in range(steps % n):
+        singles[(start + j) % n].replay()
+    t1.record()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - w0) * 1e3 / steps
+    return t0.elapsed_time(t1) / steps, wall
+
+
 def kernel_time(F, sets, kernel: str, steps: int, per_step: int):
     """Mean launch duration (ms) of one library kernel over `steps` eager steps.  The
     library launches that kernel with a HIP event pair that takes the dispatch's own
@@ -290,16 +328,8 @@ def t4096_figure(steps: int, warmup: int, eager: bool):
     wl = workloads.workload("extrap_coprime16_T4096")
     call = wl.calls[1]
     sets = [Step(wl, call, i) for i in range(buffer_sets(step_bytes(wl, call)))]
-    if eager:
-        run = lambda i: sets[i % len(sets)]()  # noqa: E731
-        fwd = lambda i: sets[i % len(sets)].forward()  # noqa: E731
-    else:
-        gs = [capture(s) for s in sets]
-        gf = [capture(s.forward) for s in sets]
-        run = lambda i: gs[i % len(gs)].replay()  # noqa: E731
-        fwd = lambda i: gf[i % len(gf)].replay()  # noqa: E731
-    ms, _ = timed(run, steps, warmup)
-    msf, _ = timed(fwd, steps, warmup)
+    ms, _ = timed_steps(sets, steps, warmup, eager)
+    msf, _ = timed_steps([s.forward for s in sets], steps, warmup, eager)
     qh = wl.queries_heads
     from paper_2606_28560_amd import fibattn as F
     kt = {k: round(kernel_time(F, sets, k, steps, 1)[0], 6) for k in ("forward", "bwd_dq", "bwd_dkdv", "rope")}
@@ -337,17 +367,11 @@ def rope_on_load_figure(steps: int, warmup: int, eager: bool, rounds: int = 3):
         if train:
             variants["two_launch_step"] = lambda st: (st.forward_two_launch(), st.backward())
             variants["on_load_step"] = lambda st: st()
-        runs = {}
-        for vname, fn in variants.items():
-            if eager:
-                runs[vname] = lambda i, fn=fn: fn(sets[i % len(sets)])
-            else:
-                gs = [capture(lambda st=st, fn=fn: fn(st)) for st in sets]
-                runs[vname] = lambda i, gs=gs: gs[i % len(gs)].replay()
+        runs = {v: [lambda st=st, fn=fn: fn(st) for st in sets] for v, fn in variants.items()}
         res = {v: [] for v in variants}
         for _ in range(rounds):
             for vname in variants:
-                res[vname].append(timed(runs[vname], steps, warmup)[0])
+                res[vname].append(timed_steps(runs[vname], steps, warmup, eager)[0])
         fig = {v + "_ms": statistics.median(t) for v, t in res.items()}
         # launch durations of the rotating forward and of the RoPE launch on k alone
         fsets = [lambda st=st: st.forward_q_on_load(False) for st in sets]
@@ -377,12 +401,7 @@ def integer_offsets_figure(steps: int, warmup: int, eager: bool, layer: int = 3)
     for tag, c in (("continuous", call), ("integer", rounded)):
         from paper_2606_28560_amd import fibattn as F
         sets = [Step(wl, c, i) for i in range(buffer_sets(step_bytes(wl, c)))]
-        if eager:
-            run = lambda i: attn_one(F, sets[i % len(sets)])  # noqa: E731
-        else:
-            gs = [capture(lambda st=st: attn_one(F, st)) for st in sets]
-            run = lambda i: gs[i % len(gs)].replay()  # noqa: E731
-        ms, _ = timed(run, steps, warmup)
+        ms, _ = timed_steps([lambda st=st: attn_one(F, st) for st in sets], steps, warmup, eager)
         out[tag + "_ms"] = ms
         out[tag + "_value"] = wl.queries_heads / (ms * 1e-3)
         del sets
@@ -401,12 +420,7 @@ def gqa_figure(steps: int, warmup: int, eager: bool, kv_heads: int = 2):
     call = wl.calls[0]
     sets = [Step(wl, call, i, kv_heads=kv_heads)
             for i in range(buffer_sets(step_bytes(wl, call, kv_heads)))]
-    if eager:
-        run = lambda i: sets[i % len(sets)]()  # noqa: E731
-    else:
-        gs = [capture(s) for s in sets]
-        run = lambda i: gs[i % len(gs)].replay()  # noqa: E731
-    ms, _ = timed(run, steps, warmup)
+    ms, _ = timed_steps(sets, steps, warmup, eager)
     kt = {}
     for k in ("forward", "bwd_dq", "bwd_dkdv", "rope"):
         kms, n = kernel_time(F, sets, k, steps, 1)
@@ -457,21 +471,14 @@ def learned_alpha_figure(steps: int, warmup: int, eager: bool, layer: int = 0):
                                   rope_base=ROPE_BASE)
         dev.append(run_dev)
     out = {"workload": wl.name, "layer": layer, "alpha": float(call.alpha)}
-    runs = {}
-    for tag, fns in (("device_alpha", dev), ("host_alpha", sets)):
-        if eager:
-            run = lambda i, fns=fns: fns[i % len(fns)]()  # noqa: E731
-        else:
-            gs = [capture(fn) for fn in fns]
-            run = lambda i, gs=gs: gs[i % len(gs)].replay()  # noqa: E731
-        runs[tag] = (fns, run)
+    runs = {"device_alpha": dev, "host_alpha": sets}
     # The two steps alternate over three rounds and the medians are reported: whichever
     # is measured first otherwise carries the GPU's ramp-up (7% on one run).
     ms_r = {tag: [] for tag in runs}
     kt_r = {tag: {} for tag in runs}
     for _ in range(3):
-        for tag, (fns, run) in runs.items():
-            ms_r[tag].append(timed(run, steps, warmup)[0])
+        for tag, fns in runs.items():
+            ms_r[tag].append(timed_steps(fns, steps, warmup, eager)[0])
             for k in ("forward", "bwd_dq", "bwd_dkdv", "rope"):
                 kms, n = kernel_time(F, fns, k, steps, 1)
                 if n:
@@ -588,22 +595,20 @@ def main():
     sets = [Step(wl, call, i) for i in range(nsets)]
     torch.cuda.synchronize()
 
-    if args.eager:
-        run = lambda i: sets[i % nsets]()  # noqa: E731
-    else:
-        graphs = [capture(st) for st in sets]
-        run = lambda i: graphs[i % nsets].replay()  # noqa: E731
-    ms, wall_ms = timed(run, args.steps, args.warmup)
+    ms, wall_ms = timed_steps(sets, args.steps, args.warmup, args.eager, whole=False)
     qh = wl.queries_heads
     print(f"# step {ms:.4f} ms (host wall {wall_ms:.4f} ms/step)", file=sys.stderr, flush=True)
 
+    # the same steps with one single-step graph replayed per step (launch-gap comparison)
+    one_ms = None
+    if not args.eager:
+        graphs = [capture(st) for st in sets]
+        one_ms, _ = timed(lambda i: graphs[i % nsets].replay(), args.steps, args.warmup)
+        del graphs
+
     # attention only (forward + backward kernels, no RoPE)
-    if args.eager:
-        attn_run = lambda i: attn_one(F, sets[i % nsets])  # noqa: E731
-    else:
-        ag = [capture(lambda st=st: attn_one(F, st)) for st in sets]
-        attn_run = lambda i: ag[i % nsets].replay()  # noqa: E731
-    ms_attn, _ = timed(attn_run, args.steps, args.warmup)
+    ms_attn, _ = timed_steps([lambda st=st: attn_one(F, st) for st in sets], args.steps, args.warmup, args.eager,
+                             whole=False)
 
     # per-kernel mean durations (eager steps, library HIP events on the launch stream)
     kt = {}
@@ -636,7 +641,9 @@ def main():
         "config": {"workload": wl.name, "B": wl.B, "H": wl.H, "T": wl.T, "d_head": wl.D,
                    "W": call.W, "base": call.base_name, "alpha": float(call.alpha),
                    "step": "rope(k) + forward rotating q on load + backward (dq, dk w.r.t. unrotated q, k)",
-                   "launch": "eager" if args.eager else "hip_graph", "buffer_sets": nsets},
+                   "launch": "eager" if args.eager else f"hip_graph of {nsets} steps (one per buffer set)",
+                   "buffer_sets": nsets},
+        "one_graph_per_step_ms": one_ms,
         "roofline": roofline,
         "attention_only": {"ms_per_step": ms_attn, "value": qh / (ms_attn * 1e-3),
                            "alg_GBs": alg_bytes("fwd+bwd", wl.D, s) * qh / (ms_attn * 1e-3) / 1e9,
