@@ -221,6 +221,17 @@ fibattn_status_t fibattn_backward_strided(const void *q, const void *k, const vo
                                           const int32_t *base, int K, float alpha, float rope_base,
                                           fibattn_dtype_t dtype, hipStream_t stream);
 
+/* fibattn_forward_rope_q with per-tensor placements (the fibattn_layout_t rules above):
+ * layouts holds 5 entries, for q, k, v, o and q_out (the last ignored when q_out is
+ * NULL), e.g. q, k, v as slices of a fused [B,T,3,H,d] projection output. */
+fibattn_status_t fibattn_forward_rope_q_strided(const void *q, const void *k, const void *v,
+                                                void *o, float *lse, void *q_out,
+                                                const fibattn_layout_t *layouts,
+                                                int B, int H, int H_kv, int T, int d_head, int W,
+                                                const int32_t *base, int K, float alpha,
+                                                float rope_base, fibattn_dtype_t dtype,
+                                                hipStream_t stream);
+
 /*
  * Device-resident alpha (Section 2, "The per-layer scalar": alpha = 0.5 + sigmoid(theta)
  * with theta learned per layer), so that a training step never reads alpha on the host.

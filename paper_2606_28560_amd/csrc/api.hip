@@ -191,11 +191,12 @@ fibattn_status_t fibattn_forward(const void *q, const void *k, const void *v, vo
     return fibattn_forward_gqa(q, k, v, o, lse, B, H, H, T, d_head, W, base, K, alpha, dtype, stream);
 }
 
-// The forward with q rotated on load, from a host table (rtp null) or a device table.
+// The forward with q rotated on load, from a host table (rtp null) or a device table;
+// lay.dq places q_out.
 static fibattn_status_t forward_rope_q_impl(const void *q, const void *k, const void *v, void *o, float *lse,
                                             void *q_out, int B, int H, int H_kv, int T, int d_head, int W,
                                             const RungTable &rt, const RungTable *rtp, float rope_base,
-                                            fibattn_dtype_t dtype, hipStream_t stream) {
+                                            const Layouts &lay, fibattn_dtype_t dtype, hipStream_t stream) {
     if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
     if (!q || !k || !v || !o || !lse) return FIBATTN_ERR_INVALID_ARG;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse) ||
@@ -205,7 +206,6 @@ static fibattn_status_t forward_rope_q_impl(const void *q, const void *k, const 
     const bool on_load = forward_mfma_supported((int)dtype, d_head, W);
     if (!on_load && !q_out) return FIBATTN_ERR_UNSUPPORTED;  // the rotated rows need a home
     const Heads hd{H, H / H_kv};
-    const Layouts lay = packed_layouts(H, H_kv, T, d_head);
     hipError_t e;
     if (on_load) {
         // one launch: each query row is rotated where the forward loads it
@@ -213,11 +213,13 @@ static fibattn_status_t forward_rope_q_impl(const void *q, const void *k, const 
         e = launch_forward_mfma(q, k, v, o, lse, B * H, hd, T, W, rt, rtp, lay, stream, &rf, q_out);
     } else {
         // the RoPE launch on q into q_out, then the forward on it
-        const Layout l = Layout::packed(H, T, d_head);
-        e = launch_rope((int)dtype, d_head, q, q_out, l, l, nullptr, nullptr, l, l, B * H, H, T, rope_base,
-                        0, stream);
+        if ((long long)B * H > 65535ll * 16) return FIBATTN_ERR_UNSUPPORTED;
+        e = launch_rope((int)dtype, d_head, q, q_out, lay.q, lay.dq, nullptr, nullptr, lay.q, lay.dq, B * H, H,
+                        T, rope_base, 0, stream);
+        Layouts lr = lay;
+        lr.q = lay.dq;
         if (e == hipSuccess)
-            e = launch_forward((int)dtype, d_head, q_out, k, v, o, lse, B * H, hd, T, W, rt, rtp, lay, stream);
+            e = launch_forward((int)dtype, d_head, q_out, k, v, o, lse, B * H, hd, T, W, rt, rtp, lr, stream);
     }
     return e == hipSuccess ? FIBATTN_OK : FIBATTN_ERR_HIP;
 }
@@ -233,6 +235,28 @@ fibattn_status_t fibattn_forward_rope_q(const void *q, const void *k, const void
     st = build_table(alpha, base, K, W, &rt);
     if (st != FIBATTN_OK) return st;
     return forward_rope_q_impl(q, k, v, o, lse, q_out, B, H, H_kv, T, d_head, W, rt, nullptr, rope_base,
+                               packed_layouts(H, H_kv, T, d_head), dtype, stream);
+}
+
+fibattn_status_t fibattn_forward_rope_q_strided(const void *q, const void *k, const void *v, void *o,
+                                                float *lse, void *q_out, const fibattn_layout_t *layouts,
+                                                int B, int H, int H_kv, int T, int d_head, int W,
+                                                const int32_t *base, int K, float alpha, float rope_base,
+                                                fibattn_dtype_t dtype, hipStream_t stream) {
+    if (!layouts || T < 1) return FIBATTN_ERR_INVALID_ARG;
+    fibattn_status_t st = check_common(B, H, T, d_head, W, K, dtype);
+    if (st != FIBATTN_OK) return st;
+    if (H_kv < 1 || H_kv > H || H % H_kv != 0) return FIBATTN_ERR_INVALID_ARG;
+    Layouts lay = packed_layouts(H, H_kv, T, d_head);
+    Layout *dst[5] = {&lay.q, &lay.k, &lay.v, &lay.o, &lay.dq};  // q_out is placed by the dq slot
+    for (int a = 0; a < (q_out ? 5 : 4); ++a) {
+        st = check_layout(layouts[a], T, d_head, dtype, dst[a]);
+        if (st != FIBATTN_OK) return st;
+    }
+    RungTable rt;
+    st = build_table(alpha, base, K, W, &rt);
+    if (st != FIBATTN_OK) return st;
+    return forward_rope_q_impl(q, k, v, o, lse, q_out, B, H, H_kv, T, d_head, W, rt, nullptr, rope_base, lay,
                                dtype, stream);
 }
 
@@ -417,7 +441,8 @@ fibattn_status_t fibattn_forward_rope_q_dt(const void *q, const void *k, const v
     RungTable unused;
     memset(&unused, 0, sizeof(unused));
     return forward_rope_q_impl(q, k, v, o, lse, q_out, B, H, H_kv, T, d_head, W, unused,
-                               (const RungTable *)table, rope_base, dtype, stream);
+                               (const RungTable *)table, rope_base, packed_layouts(H, H_kv, T, d_head), dtype,
+                               stream);
 }
 
 fibattn_status_t fibattn_backward_dt(const void *q, const void *k, const void *v, const void *o,

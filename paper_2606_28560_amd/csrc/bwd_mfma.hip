@@ -613,8 +613,10 @@ static hipError_t launch_dkdv(bool interp, const void *q, const void *k, const v
     constexpr int keys = 64 / NH;
     const int tiles = (T + keys - 1) / keys;
     const bool one = hd.G == NH;
-    const bool strided = lay.q.st != kD || lay.k.st != kD || lay.v.st != kD || lay.g.st != kD ||
-                         lay.dk.st != kD || lay.dv.st != kD;
+    const int hk = hd.kv_heads();
+    const bool strided = !is_packed(lay.q, hd.H, T, kD) || !is_packed(lay.k, hk, T, kD) ||
+                         !is_packed(lay.v, hk, T, kD) || !is_packed(lay.g, hd.H, T, kD) ||
+                         !is_packed(lay.dk, hk, T, kD) || !is_packed(lay.dv, hk, T, kD);
     if (rtp && strided) return hipErrorInvalidValue;  // device tables come with packed tensors
 #define FIBATTN_DKDV(I, S)                                                                     \
     (one ? bwd_dkdv_bf16_d64_kernel<I, NH, true, false, S> : bwd_dkdv_bf16_d64_kernel<I, NH, false, false, S>)
@@ -637,8 +639,10 @@ hipError_t launch_backward_mfma(const void *q, const void *k, const void *v, con
     const float tau = 1.f / sqrtf(64.f);
     bool interp = rtp != nullptr;  // a device table may hold any weights
     for (int r = 0; r < rt.n && !interp; ++r) interp = rt.w[r] != 0.f;
-    const bool strided = lay.q.st != kD || lay.k.st != kD || lay.v.st != kD || lay.o.st != kD ||
-                         lay.g.st != kD || lay.dq.st != kD;
+    const int hk = hd.kv_heads();
+    const bool strided = !is_packed(lay.q, hd.H, T, kD) || !is_packed(lay.k, hk, T, kD) ||
+                         !is_packed(lay.v, hk, T, kD) || !is_packed(lay.o, hd.H, T, kD) ||
+                         !is_packed(lay.g, hd.H, T, kD) || !is_packed(lay.dq, hd.H, T, kD);
     if (rtp && strided) return hipErrorInvalidValue;  // device tables come with packed tensors
     // query heads per dq workgroup: the group's heads side by side for packed tensors with
     // a host table (as the forward)

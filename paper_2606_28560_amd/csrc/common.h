@@ -137,6 +137,13 @@ __device__ __forceinline__ long long head_at(const Layout &l, int bh, int heads,
 struct Layouts {
     Layout q, k, v, o, g, dq, dk, dv;
 };
+// Whether a placement is exactly the packed one, the only one the kernels' packed
+// (STRIDED = false) instances address: equal row strides alone do not make it so (a
+// slice of a longer sequence has packed rows but a larger head stride).
+inline bool is_packed(const Layout &l, int heads, int T, int D) {
+    const Layout p = Layout::packed(heads, T, D);
+    return l.sb == p.sb && l.sh == p.sh && l.st == p.st;
+}
 
 // RoPE inverse frequencies base^(-2j/D) for j < D/2 <= 32, evaluated in float64 on
 // the host; `on` = 0 when no rotation is requested.

@@ -37,7 +37,7 @@ constexpr float kSlack = 8.f;              // log2 units a logit may exceed the 
 // RQ: q holds the raw (unrotated) queries and k the rotated keys.  Each lane rotates its
 // own slice of its query row at the query's position (RoPE, Section 2 "Attended set"),
 // attends with the rotated row and, when qrot is not null, writes it there for the
-// backward.  A query row is used by one query only, so rotating it where it is loaded
+// backward, placed by lay.dq (the forward has no dq of its own).  A query row is used by one query only, so rotating it where it is loaded
 // costs no extra row traffic; a key row is read by up to 1 + W + K queries and stays
 // with the RoPE launch.  rf: the RoPE frequencies (unused without RQ).
 template <bool INTERP, bool DEV, bool STRIDED, int HS, bool RQ>
@@ -46,7 +46,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     uint16_t *__restrict__ o, float *__restrict__ lse, int T, int W, RungTable rt_arg,
     const RungTable *__restrict__ rtp, float sl2, int tiles, Heads hd, Layouts lay,
     uint16_t *qrot, RopeFreq rf) {
-    static_assert(!RQ || !STRIDED, "rotation on load: packed tensors");
     const RungTable &rt = DEV ? *rtp : rt_arg;
     constexpr int RB = INTERP ? 1 : 2;  // rungs per load batch; two batches in flight
     constexpr int NS = INTERP ? 2 : 1;  // rows per rung (r0, and r1 when interpolating)
@@ -168,7 +167,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
         qq.a = make_uint4(aw[0], aw[1], aw[2], aw[3]);
         qq.b = make_uint4(bw[0], bw[1], bw[2], bw[3]);
         if (qrot && i < T) {  // read by the backward: ordinary stores
-            uint16_t *qr = qrot + ((size_t)bh * T + i) * kD;
+            uint16_t *qr = qrot + head_at<STRIDED, kD>(lay.dq, bh, hd.H, T) +
+                           (size_t)i * (STRIDED ? (int)lay.dq.st : kD);
             *reinterpret_cast<uint4 *>(qr + 8 * gq) = qq.a;
             *reinterpret_cast<uint4 *>(qr + 32 + 8 * gq) = qq.b;
         }
@@ -297,9 +297,12 @@ hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void
                                const RungTable *rtp, const Layouts &lay, hipStream_t s,
                                const RopeFreq *rq, void *q_rot) {
     const float sl2 = kLog2e / sqrtf(64.f);
-    // device tables and rotation on load come with packed tensors only
-    const bool strided = lay.q.st != kD || lay.k.st != kD || lay.v.st != kD || lay.o.st != kD;
-    if ((rtp || rq) && strided) return hipErrorInvalidValue;
+    // device tables come with packed tensors only; rotation on load places R q by lay.dq
+    const int hk = hd.kv_heads();
+    const bool strided = !is_packed(lay.q, hd.H, T, kD) || !is_packed(lay.k, hk, T, kD) ||
+                         !is_packed(lay.v, hk, T, kD) || !is_packed(lay.o, hd.H, T, kD) ||
+                         (rq && q_rot && !is_packed(lay.dq, hd.H, T, kD));
+    if (rtp && strided) return hipErrorInvalidValue;
     const bool interp = any_interp(rt);
     const int hs = (rtp || strided) ? 1 : heads_per_wg(hd.G);
     const int tiles = (T + kFwdBQ / hs - 1) / (kFwdBQ / hs);  // runs of 64 / hs queries
@@ -309,8 +312,10 @@ hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void
      : hs == 2 ? (interp ? FIBATTN_FWD(true, 2, R) : FIBATTN_FWD(false, 2, R))                \
                : (interp ? FIBATTN_FWD(true, 1, R) : FIBATTN_FWD(false, 1, R)))
     auto kern = rtp ? (rq ? fwd_bf16_d64_kernel<true, true, false, 1, true> : fwd_bf16_d64_kernel<true, true, false, 1, false>)
-              : strided ? (interp ? fwd_bf16_d64_kernel<true, false, true, 1, false>
-                                  : fwd_bf16_d64_kernel<false, false, true, 1, false>)
+              : strided ? (rq ? (interp ? fwd_bf16_d64_kernel<true, false, true, 1, true>
+                                        : fwd_bf16_d64_kernel<false, false, true, 1, true>)
+                              : (interp ? fwd_bf16_d64_kernel<true, false, true, 1, false>
+                                        : fwd_bf16_d64_kernel<false, false, true, 1, false>))
               : rq ? FIBATTN_FWD_HS(true) : FIBATTN_FWD_HS(false);
 #undef FIBATTN_FWD_HS
 #undef FIBATTN_FWD

@@ -50,8 +50,8 @@ hipError_t launch_backward(int dtype, int D, const void *q, const void *k, const
 
 // bfloat16, d_head = 64, W <= 16: matrix-core band + VALU rungs (fwd_mfma.hip, bwd_mfma.hip).
 bool forward_mfma_supported(int dtype, int D, int W);
-// rq (packed tensors): q is unrotated and each query row is rotated with these
-// frequencies where the forward loads it; the rotated rows go to q_rot unless it is null.
+// rq: q is unrotated and each query row is rotated with these frequencies where the
+// forward loads it; the rotated rows go to q_rot, placed by lay.dq, unless it is null.
 hipError_t launch_forward_mfma(const void *q, const void *k, const void *v, void *o, float *lse,
                                int BH, const Heads &hd, int T, int W, const RungTable &rt,
                                const RungTable *rtp, const Layouts &lay, hipStream_t s,

@@ -27,7 +27,7 @@ EXPORTED = ("fibattn_rung_table", "fibattn_forward", "fibattn_backward_workspace
             "fibattn_backward_dt", "fibattn_alpha_from_theta", "fibattn_dtheta", "fibattn_rope",
             "fibattn_rope_qk", "fibattn_status_string", "fibattn_timing_begin", "fibattn_timing_end",
             "fibattn_backward_noalloc", "fibattn_device_table_theta", "fibattn_rope_qk_table",
-            "fibattn_forward_rope_q", "fibattn_forward_rope_q_dt")
+            "fibattn_forward_rope_q", "fibattn_forward_rope_q_dt", "fibattn_forward_rope_q_strided")
 SCRATCH_BYTES = 64 << 20  # FIBATTN_SCRATCH_BYTES: the allocation-free backward's static scratch
 
 
@@ -66,6 +66,8 @@ def lib():
     L.fibattn_forward_rope_q.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, ip, i, f, f, i, vp]
     L.fibattn_forward_rope_q.restype = i
     L.fibattn_forward_rope_q_dt.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, vp, f, i, vp]
+    L.fibattn_forward_rope_q_strided.argtypes = [vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, ip, i, f, f, i, vp]
+    L.fibattn_forward_rope_q_strided.restype = i
     L.fibattn_forward_rope_q_dt.restype = i
     L.fibattn_backward_gqa.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                        i, i, i, i, i, i, ip, i, f, f, i, vp]
@@ -189,30 +191,37 @@ def fibattn_forward_rope_q(q, k, v, W: int, base, alpha: float, rope_base: float
     """o, lse, q_out = forward of the UNROTATED q with keys k already rotated (fibattn_rope,
     same rope_base); the queries are rotated where the forward loads them.  q_out = R q
     (may be q itself), the rotated queries a later backward takes; keep_q=False writes no
-    q_out (forward only) and returns None for it.  Packed tensors: q [B,H,T,D]; k, v
-    [B,H_kv,T,D] with H_kv dividing H."""
+    q_out (forward only) and returns None for it.  q [B,H,T,D]; k, v [B,H_kv,T,D] with
+    H_kv dividing H; q, k, v, o, q_out may be views with contiguous rows (e.g. slices of
+    a fused [B,T,3,H,D] projection output)."""
     import torch
 
     B, H, T, D = q.shape
     Hkv = _kv_heads(q, k)
-    _check_tensor("q", q, q.shape, q.dtype)
+    _check_tensor("q", q, q.shape, q.dtype, strided=True)
     for n_, t in (("k", k), ("v", v)):
-        _check_tensor(n_, t, (B, Hkv, T, D), q.dtype)
+        _check_tensor(n_, t, (B, Hkv, T, D), q.dtype, strided=True)
     o = torch.empty_like(q) if o is None else o
     lse = torch.empty((B, H, T), device=q.device, dtype=torch.float32) if lse is None else lse
-    _check_tensor("o", o, q.shape, q.dtype)
+    _check_tensor("o", o, q.shape, q.dtype, strided=True)
     _check_tensor("lse", lse, (B, H, T), torch.float32)
     if keep_q:
         q_out = torch.empty_like(q) if q_out is None else q_out
-        _check_tensor("q_out", q_out, q.shape, q.dtype)
+        _check_tensor("q_out", q_out, q.shape, q.dtype, strided=True)
     elif q_out is not None:
         raise ValueError("q_out given with keep_q=False")
     b, bp = _base_array(base)
-    st = lib().fibattn_forward_rope_q(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
-                                      q_out.data_ptr() if keep_q else None, B, H, Hkv, T, D, int(W), bp,
-                                      b.size, ctypes.c_float(alpha), ctypes.c_float(rope_base), _dtype_code(q),
-                                      _stream(stream))
-    _check("fibattn_forward_rope_q", st)
+    ptrs = (q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
+            q_out.data_ptr() if keep_q else None)
+    tail = (T, D, int(W), bp, b.size, ctypes.c_float(alpha), ctypes.c_float(rope_base), _dtype_code(q),
+            _stream(stream))
+    if all(t.is_contiguous() for t in (q, k, v, o) + ((q_out,) if keep_q else ())):
+        st = lib().fibattn_forward_rope_q(*ptrs, B, H, Hkv, *tail)
+        _check("fibattn_forward_rope_q", st)
+    else:
+        lay = _layouts(q, k, v, o, q_out if keep_q else q)
+        st = lib().fibattn_forward_rope_q_strided(*ptrs, lay, B, H, Hkv, *tail)
+        _check("fibattn_forward_rope_q_strided", st)
     return o, lse, q_out
 
 

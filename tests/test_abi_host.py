@@ -152,6 +152,11 @@ def test_invalid_arguments_return_codes_without_gpu():
     assert rq(16, 16, 16, 16, 16, 16, 1, 8, 8, 8, 48, 8, b, 15, one, r4, 1, None) == 2
     assert rq(16, 16, 16, 16, 16, None, 1, 8, 8, 8, 64, 8, b, 15, one, r4, 0, None) == 2   # float32
     assert rq(16, 16, 16, 16, 16, None, 1, 8, 8, 8, 64, 20, b, 15, one, r4, 1, None) == 2  # W > 16
+    # with placements: the layouts are checked before any launch
+    rqs = L.fibattn_forward_rope_q_strided
+    assert rqs(16, 16, 16, 16, 16, 16, None, 1, 8, 8, 8, 64, 8, b, 15, one, r4, 1, None) == 1
+    bad_lay = (ctypes.c_int64 * 15)(*([8 * 64 * 8, 64 * 8, 64] * 4 + [8 * 64 * 8, 64 * 8, 3]))
+    assert rqs(16, 16, 16, 16, 16, 16, bad_lay, 1, 8, 8, 8, 64, 8, b, 15, one, r4, 1, None) == 1
     # the same from a device table: the table pointer is required
     rqd = L.fibattn_forward_rope_q_dt
     assert rqd(16, 16, 16, 16, 16, 16, 1, 8, 8, 8, 64, 8, None, r4, 1, None) == 1

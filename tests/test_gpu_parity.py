@@ -435,10 +435,16 @@ def test_deterministic_and_stream_independent():
 def _placed(x, how, slot=0):
     """A device view of x ([B,H,T,D], CPU) with the same values in placement `how`:
     "bthd" = a transposed [B,T,H,D] buffer; "qkv" = one slot of a [B,T,3,H,D] buffer
-    (a fused projection output); "packed" = contiguous."""
+    (a fused projection output); "tslice" = the first T rows of each head of a NaN-filled
+    [B,H,T+37,D] buffer (packed rows, larger head and batch strides); "packed" =
+    contiguous."""
     B, H, T, D = x.shape
     if how == "packed":
         return x.cuda().contiguous()
+    if how == "tslice":
+        buf = torch.full((B, H, T + 37, D), float("nan"), dtype=x.dtype, device="cuda")
+        buf[:, :, :T].copy_(x)
+        return buf[:, :, :T]
     if how == "bthd":
         buf = torch.empty((B, T, H, D), dtype=x.dtype, device="cuda")
         buf.copy_(x.transpose(1, 2))
@@ -455,6 +461,10 @@ STRIDED = [
     (1, 8, 2, 257, 64, "bf16", 8, 1.0, "bthd", "bthd"),       # grouped heads
     (2, 3, 3, 200, 32, "fp32", 6, 0.7310586, "qkv", "bthd"),  # generic kernels
     (1, 4, 2, 130, 128, "bf16", 10, 1.2, "bthd", "qkv"),      # d_head 128, outputs in a qkv buffer
+    # packed rows with non-packed head strides: the matrix-core kernels' strided instances
+    (2, 4, 4, 300, 64, "bf16", 8, 1.0, "tslice", "tslice"),
+    (1, 8, 2, 257, 64, "bf16", 8, 0.85, "tslice", "packed"),
+    (2, 2, 2, 200, 64, "bf16", 12, 1.0, "packed", "tslice"),
 ]
 
 
@@ -485,3 +495,35 @@ def test_strided_layouts(B, H, Hkv, T, D, dtype, W, alpha, pin, pout, rope_base)
         for t, slot in ((o, 0), (dq, 0), (dk, 1), (dv, 2)):
             others = [s_ for s_ in range(3) if s_ != slot]
             assert torch.isnan(t._base[:, :, others].float()).all().item()
+    if pout == "tslice":
+        # nothing written past each head's T rows
+        for t in (o, dq, dk, dv):
+            assert torch.isnan(t._base[:, :, T:].float()).all().item()
+
+
+ROPE_Q_STRIDED = [
+    # (B, H, Hkv, T, D, dtype, W, alpha, placement of q, k, v, placement of o and q_out)
+    (2, 4, 4, 300, 64, "bf16", 8, 1.0, "qkv", "bthd"),
+    (1, 8, 2, 257, 64, "bf16", 12, 0.85, "tslice", "tslice"),
+    (1, 4, 4, 200, 64, "bf16", 16, 1.0, "bthd", "packed"),
+    (1, 2, 2, 200, 64, "fp32", 8, 0.85, "qkv", "bthd"),  # the RoPE launch, then the forward
+]
+
+
+@pytest.mark.parametrize("B,H,Hkv,T,D,dtype,W,alpha,pin,pout", ROPE_Q_STRIDED)
+def test_forward_rotating_q_on_load_strided(B, H, Hkv, T, D, dtype, W, alpha, pin, pout):
+    # the same o, lse and R q bits as the packed call: placement changes addressing only
+    x = _gqa_inputs(B, H, Hkv, T, D, dtype, 171 + D)
+    K = F.fibattn_rope(x["k"].cuda(), 10000.0)
+    q, k, v = _placed(x["q"], pin, 0), _placed(K.cpu(), pin, 1), _placed(x["v"], pin, 2)
+    o = _placed(torch.zeros((B, H, T, D), dtype=x["q"].dtype), pout, 0)
+    qo = _placed(torch.zeros((B, H, T, D), dtype=x["q"].dtype), pout, 1)
+    assert not (q.is_contiguous() and o.is_contiguous())
+    o1, l1, q1 = F.fibattn_forward_rope_q(q, k, v, W, FIB, alpha, 10000.0, o=o, q_out=qo)
+    o2, l2, q2 = F.fibattn_forward_rope_q(x["q"].cuda(), K, x["v"].cuda(), W, FIB, alpha, 10000.0)
+    torch.cuda.synchronize()
+    assert o1.data_ptr() == o.data_ptr() and q1.data_ptr() == qo.data_ptr()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2) and torch.equal(q1, q2)
+    if pout == "tslice":
+        for t in (o1, q1):
+            assert torch.isnan(t._base[:, :, T:].float()).all().item()
