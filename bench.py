@@ -63,15 +63,15 @@ def parse_args():
 #            --no-learned-alpha --no-integer-offsets --no-rope-on-load --no-configs --copy-probe-mb 256
 # each scaled by what the same counter reads for the plain 256 MiB device copy of that run.
 # They hold only for the kernel sources they were taken on (COUNTER_SOURCES_SHA).
-COUNTER_SOURCES_SHA = "63537e6fb70a466c3e876cb1655052ecc1817827432ca18ad9ee3f67fb514af6"
+COUNTER_SOURCES_SHA = "5fd42aa5f3dc51015e331a28822874ccdea73c6a10c2e08446cee9a4e519d822"
 COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
 COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
-    "forward": (12398.3, 16748.1),
-    "bwd_dq": (20800.6, 10425.8),
-    "bwd_dkdv": (18535.0, 16613.7),
+    "forward": (12407.3, 16754.7),
+    "bwd_dq": (20800.6, 10426.1),
+    "bwd_dkdv": (18565.1, 16601.0),
     "rope": (4124.9, 8192.0),
 }
-COPY_PROBE_KIB = (262144.0, 131092.9, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
+COPY_PROBE_KIB = (262144.0, 131093.1, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
 
 
 def kernel_sources_sha() -> str:
