@@ -18,7 +18,8 @@
 // Softmax runs in base 2: the band's maximum is the first running reference, then
 // rungs are taken a batch at a time (their key and value rows loaded together),
 // rescaling the running sum and weighted values only when a logit exceeds the
-// reference by a wide margin.
+// reference by a wide margin.  The layer step's instance also applies RoPE to q where
+// it loads it (RQ below).
 #include "launch.h"
 #include "mfma.h"
 
@@ -37,9 +38,10 @@ constexpr float kSlack = 8.f;              // log2 units a logit may exceed the 
 // RQ: q holds the raw (unrotated) queries and k the rotated keys.  Each lane rotates its
 // own slice of its query row at the query's position (RoPE, Section 2 "Attended set"),
 // attends with the rotated row and, when qrot is not null, writes it there for the
-// backward, placed by lay.dq (the forward has no dq of its own).  A query row is used by one query only, so rotating it where it is loaded
-// costs no extra row traffic; a key row is read by up to 1 + W + K queries and stays
-// with the RoPE launch.  rf: the RoPE frequencies (unused without RQ).
+// backward, placed by lay.dq (the forward has no dq of its own).  A query row is used by
+// one query only, so rotating it where it is loaded costs no extra row traffic; a key
+// row is read by up to 1 + W + K queries and stays with the RoPE launch.  rf: the RoPE
+// frequencies (unused without RQ).
 template <bool INTERP, bool DEV, bool STRIDED, int HS, bool RQ>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void fwd_bf16_d64_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k, const uint16_t *__restrict__ v,
