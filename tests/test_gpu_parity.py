@@ -196,6 +196,7 @@ ROPE_Q = [
     (1, 2, 2, 1, 64, "bf16", 0, 1.0),
     (1, 2, 2, 200, 64, "fp32", 8, 0.85),
     (1, 2, 1, 150, 128, "bf16", 8, 1.0),
+    (1, 2, 2, 150, 64, "bf16", 20, 0.9),  # past the matrix-core window limit
 ]
 
 
@@ -237,6 +238,11 @@ def test_forward_rotating_q_on_load(B, H, Hkv, T, D, dtype, W, alpha):
         torch.cuda.synchronize()
         assert none is None and torch.equal(o2, o) and torch.equal(l2, lse)
         assert Q3.data_ptr() == q3.data_ptr() and torch.equal(q3, Q) and torch.equal(o3, o) and torch.equal(l3, lse)
+    else:
+        # outside the matrix-core kernels the rotated rows need a buffer: refused before
+        # any launch
+        with pytest.raises(F.FibattnError):
+            F.fibattn_forward_rope_q(q, K, V, W, FIB, alpha, 10000.0, keep_q=False)
 
 
 @pytest.mark.parametrize("name,ci", [("layer_60m_fixed_T1024", 0), ("extrap_coprime16_T4096", 1)])
