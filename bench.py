@@ -63,15 +63,15 @@ def parse_args():
 #            --no-learned-alpha --no-integer-offsets --no-rope-on-load --no-configs --copy-probe-mb 256
 # each scaled by what the same counter reads for the plain 256 MiB device copy of that run.
 # They hold only for the kernel sources they were taken on (COUNTER_SOURCES_SHA).
-COUNTER_SOURCES_SHA = "6b356280429adb2e2e7a41fa88b51299bc2fd18dc894759e6c27dd2f9112cc43"
+COUNTER_SOURCES_SHA = "344e437b3afa06225bb4aeb4eea21d3a8b2183039bad721361a2dcbfe099f86c"
 COUNTER_WORKLOAD = "layer_60m_fixed_T1024"
 COUNTER_KIB = {  # kernel: (FETCH_SIZE, WRITE_SIZE) mean KiB per dispatch
-    "forward": (12407.5, 16754.7),
-    "bwd_dq": (20800.7, 10426.6),
-    "bwd_dkdv": (18513.9, 16613.2),
+    "forward": (12407.4, 16750.9),
+    "bwd_dq": (20800.6, 10426.2),
+    "bwd_dkdv": (18547.8, 16613.7),
     "rope": (4124.9, 8192.0),
 }
-COPY_PROBE_KIB = (262144.0, 131092.8, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
+COPY_PROBE_KIB = (262144.0, 131093.7, 262144.0)  # bytes moved each way; FETCH_SIZE; WRITE_SIZE
 
 
 def kernel_sources_sha() -> str:

@@ -64,9 +64,11 @@ __global__ __launch_bounds__(256) void rope_kernel(const S *x, S *y, int BH, int
 }
 
 // bfloat16, d_head 64: a workgroup owns 4 NP positions of 16 (b, h) rows; each lane group
-// of four handles NP positions (t, t + 4) of one head.  NP = 2 for two tensors (two rows'
-// loads in flight per lane: 10.7 -> 10.2 us for q and k of the 60M layer); NP = 1 for one
-// tensor, which doubles the workgroup count of that smaller launch.
+// of four handles NP positions (t, t + 4) of one head.  NP = 2 (two rows' loads in flight
+// per lane) for two tensors (10.7 -> 10.2 us for q and k of the 60M layer) and for one
+// tensor of at least 2^17 rows (k of the T = 4096 layer: 11.4 -> 10.1 us); NP = 1 for a
+// smaller single tensor, which doubles its workgroup count (k of the T = 1024 layer keeps
+// 1024 workgroups).
 // Lane group g of a row's four lanes holds dims [8g, 8g+8) and [32+8g, 32+8g+8),
 // i.e. the eight rotate-half pairs (j, j+32), j in [8g, 8g+8): two 16-byte loads
 // and stores per lane and row, reading 64 contiguous bytes per row per instruction.
@@ -192,9 +194,10 @@ hipError_t launch_rope(int dtype, int D, const void *x0, void *y0, const Layout 
         const bool strided = !same(lx0, heads) || !same(ly0, heads) ||
                              (x1 && (!same(lx1, heads1) || !same(ly1, heads1)));
         const int rows = x1 ? max(BH, BH1) : BH;
-        const int tp = x1 ? 8 : 4;  // positions per workgroup
-        auto kern = x1 ? (strided ? rope_bf16_d64_kernel<true, 2> : rope_bf16_d64_kernel<false, 2>)
-                       : (strided ? rope_bf16_d64_kernel<true, 1> : rope_bf16_d64_kernel<false, 1>);
+        const bool np2 = x1 || (long long)BH * T >= (1ll << 17);
+        const int tp = np2 ? 8 : 4;  // positions per workgroup
+        auto kern = np2 ? (strided ? rope_bf16_d64_kernel<true, 2> : rope_bf16_d64_kernel<false, 2>)
+                        : (strided ? rope_bf16_d64_kernel<true, 1> : rope_bf16_d64_kernel<false, 1>);
         return launch(kRope, kern,
                       dim3((T + tp - 1) / tp, (rows + kRope64RB - 1) / kRope64RB, x1 ? 2 : 1),
                       dim3(256), 0, s, x0, y0, x1, y1, T, rf, transpose, RopeIO{lx0, ly0, BH, heads},
