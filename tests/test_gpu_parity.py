@@ -124,10 +124,14 @@ def test_backward_at_extrapolation_length():
     compare(got, ref, wl.dtype, "T4096 backward")
 
 
-@pytest.mark.parametrize("dtype,D,transpose", [("fp32", 32, False), ("fp32", 64, True),
-                                               ("bf16", 64, False), ("bf16", 32, True)])
-def test_rope_parity(dtype, D, transpose):
-    x = _case_inputs(2, 3, 1029, D, dtype, 50)["q"]
+@pytest.mark.parametrize("dtype,D,transpose,B,H,T", [
+    ("fp32", 32, False, 2, 3, 1029), ("fp32", 64, True, 2, 3, 1029),
+    ("bf16", 64, False, 2, 3, 1029), ("bf16", 32, True, 2, 3, 1029),
+    # at least 2^17 rows: the bf16 d_head 64 launch of one tensor takes two positions per
+    # lane group; T = 3999 leaves a ragged last workgroup of positions
+    ("bf16", 64, False, 1, 33, 3999), ("bf16", 64, True, 1, 33, 3999)])
+def test_rope_parity(dtype, D, transpose, B, H, T):
+    x = _case_inputs(B, H, T, D, dtype, 50)["q"]
     got = F.fibattn_rope(x.cuda(), 10000.0, transpose).double().cpu().numpy()
     ref = oracle.rope(x, 10000.0, transpose)
     err = np.abs(got - ref).max()

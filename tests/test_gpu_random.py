@@ -13,7 +13,7 @@ from tests.parity import compare, gpu_run, oracle_run
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 40
+N_CASES = 64
 
 
 def _config(seed):
