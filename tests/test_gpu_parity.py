@@ -517,6 +517,9 @@ ROPE_Q_STRIDED = [
     (1, 8, 2, 257, 64, "bf16", 12, 0.85, "tslice", "tslice"),
     (1, 4, 4, 200, 64, "bf16", 16, 1.0, "bthd", "packed"),
     (1, 2, 2, 200, 64, "fp32", 8, 0.85, "qkv", "bthd"),  # the RoPE launch, then the forward
+    # the same past the matrix-core window, on 2^17+ rows of q: the RoPE launch of one
+    # strided tensor with two positions per lane group, a ragged last position block
+    (1, 33, 33, 3999, 64, "bf16", 20, 0.9, "bthd", "bthd"),
 ]
 
 
